@@ -1,0 +1,648 @@
+"""Seeded synthetic trace-shaped task graphs and variant tables.
+
+This module only *describes* inputs: tasks (CPU launch / sync tasks, GPU
+kernels, memcpys, communication tasks), the execution thread of each task
+and its order on that thread, dependency edges, integer-nanosecond durations
+and gaps, and per-variant transform tables (rational duration scales,
+removal bits, active edge classes).  It contains no simulation arithmetic:
+no start, finish or release time is ever computed here.  Both the oracle
+and the GPU path read the same objects.
+
+Shapes follow the paper's description of training traces: one or two CPU
+threads issuing every kernel through a launch call, one main compute stream,
+a memcpy stream, an optional auxiliary stream joined through events, and a
+communication channel for gradient all-reduces (Sec. 2 "Key Ideas",
+Sec. 3.2.1 task types, Sec. 3.2.2 dependency types).  Durations follow the
+recipe stated in the design notes: kernels lognormal(median, sigma=1),
+CPU launch calls U[5,15] us, CPU gaps U[0,3] us, device and communication
+gaps 0, all int64 ns.
+"""
+from __future__ import annotations
+
+import dataclasses
+import hashlib
+from typing import List, Optional, Tuple
+
+import numpy as np
+
+# ---------------------------------------------------------------------------
+# task kinds (metadata only; the simulation sees threads, edges, classes)
+K_LAUNCH, K_SYNC, K_GEMM, K_ELEM, K_AUX, K_WU, K_MEMCPY, K_COMM, K_CONV, \
+    K_GPU_OTHER, K_OPT, K_EMB = range(12)
+N_KINDS = 12
+GPU_KINDS = (K_GEMM, K_ELEM, K_AUX, K_WU, K_CONV, K_GPU_OTHER, K_OPT, K_EMB)
+CPU_KINDS = (K_LAUNCH, K_SYNC)
+
+SEED_BASE = 2006033180
+
+
+@dataclasses.dataclass
+class TaskGraph:
+    """A dependency graph G(V, E) in the layout the C-ABI accepts.
+
+    in_ptr/in_src/edge_cls: CSR of dependency in-edges (src -> dst).
+    thread_prev: previous task on the same execution thread (-1 = first).
+    thread_id: execution thread of each task.
+    dur, gap: int64 ns.  node_cls: transform class of each task.
+    """
+    n: int
+    n_threads: int
+    in_ptr: np.ndarray
+    in_src: np.ndarray
+    edge_cls: np.ndarray
+    thread_prev: np.ndarray
+    thread_id: np.ndarray
+    dur: np.ndarray
+    gap: np.ndarray
+    node_cls: np.ndarray
+    n_node_cls: int
+    n_edge_cls: int
+    kind: np.ndarray
+    layer: np.ndarray
+    launch_of: np.ndarray          # for device tasks: the CPU call that issued it, else -1
+    name: str = ""
+
+    @property
+    def n_edges(self) -> int:
+        return int(self.in_ptr[-1])
+
+    def digest(self) -> str:
+        h = hashlib.sha256()
+        for a in (self.in_ptr, self.in_src, self.edge_cls, self.thread_prev,
+                  self.thread_id, self.dur, self.gap, self.node_cls):
+            h.update(np.ascontiguousarray(a).tobytes())
+        return h.hexdigest()[:16]
+
+
+@dataclasses.dataclass
+class VariantSet:
+    """Per-variant transform tables.
+
+    scale: int32 [n_cls][V][2] = (p, q): duration of a task of class c in
+      variant v becomes floor(d * p / q).
+    remove_bits: uint32 [N][ceil(V/32)]; bit (v % 32) of word v // 32 set
+      means the task is removed in variant v.
+    edge_on: uint64 [V][ceil(K/64)]; bit k set means edges of class k are
+      present in variant v.
+    batches: list of (v0, v1, active_class_mask): variant ranges that share
+      one levelization (their active edge classes have an acyclic union).
+    """
+    n_variants: int
+    scale: np.ndarray
+    remove_bits: np.ndarray
+    edge_on: np.ndarray
+    batches: List[Tuple[int, int, int]]
+
+    def digest(self) -> str:
+        h = hashlib.sha256()
+        for a in (self.scale, self.remove_bits, self.edge_on):
+            h.update(np.ascontiguousarray(a).tobytes())
+        return h.hexdigest()[:16]
+
+    def subset(self, v0: int, v1: int) -> "VariantSet":
+        """Variants [v0, v1) as their own set (bit columns re-packed)."""
+        V = v1 - v0
+        W = (V + 31) // 32
+        bits = unpack_bits(self.remove_bits, self.n_variants)[:, v0:v1]
+        rb = pack_bits(bits)
+        assert rb.shape[1] == W
+        return VariantSet(V, np.ascontiguousarray(self.scale[:, v0:v1]), rb,
+                          np.ascontiguousarray(self.edge_on[v0:v1]),
+                          [(0, V, self.batches[0][2])])
+
+
+def pack_bits(bits: np.ndarray) -> np.ndarray:
+    """bool [N][V] -> uint32 [N][ceil(V/32)], bit v%32 of word v//32."""
+    N, V = bits.shape
+    W = (V + 31) // 32
+    padded = np.zeros((N, W * 32), dtype=np.uint8)
+    padded[:, :V] = bits
+    b8 = np.packbits(padded, axis=1, bitorder="little")
+    return np.ascontiguousarray(b8).view("<u4").reshape(N, W).astype(np.uint32)
+
+
+def unpack_bits(words: np.ndarray, V: int) -> np.ndarray:
+    N = words.shape[0]
+    b8 = np.ascontiguousarray(words.astype("<u4")).view(np.uint8).reshape(N, -1)
+    return np.unpackbits(b8, axis=1, bitorder="little")[:, :V].astype(bool)
+
+
+# ---------------------------------------------------------------------------
+class _Builder:
+    """Emits tasks in trace (program) order.  Node ids are emission order."""
+
+    def __init__(self, n_threads: int):
+        self.n_threads = n_threads
+        self.thread: List[int] = []
+        self.kind: List[int] = []
+        self.layer: List[int] = []
+        self.launch_of: List[int] = []
+        self.cls_override: List[int] = []
+        self.edges: List[Tuple[int, int, int]] = []
+        self.last: dict = {}
+
+    def task(self, thread: int, kind: int, layer: int, launch_of: int = -1,
+             cls_override: int = -1) -> int:
+        i = len(self.thread)
+        self.thread.append(thread)
+        self.kind.append(kind)
+        self.layer.append(layer)
+        self.launch_of.append(launch_of)
+        self.cls_override.append(cls_override)
+        self.last[thread] = i
+        return i
+
+    def edge(self, src: int, dst: int, ecls: int = 0):
+        self.edges.append((src, dst, ecls))
+
+    def launch(self, cpu: int, stream: int, kind: int, layer: int,
+               cls_override: int = -1) -> Tuple[int, int]:
+        """A CPU launch call followed by the device task it issues
+        (correlation dependency, Sec. 3.2.2)."""
+        l = self.task(cpu, K_LAUNCH, layer)
+        k = self.task(stream, kind, layer, launch_of=l, cls_override=cls_override)
+        self.edge(l, k)
+        return l, k
+
+    def sync(self, cpu: int, streams, layer: int) -> int:
+        """CPU synchronization call: waits for the last task on each stream."""
+        srcs = [self.last[s] for s in streams if s in self.last]
+        t = self.task(cpu, K_SYNC, layer)
+        for s in srcs:
+            self.edge(s, t)
+        return t
+
+
+@dataclasses.dataclass
+class _Template:
+    thread: np.ndarray
+    kind: np.ndarray
+    layer: np.ndarray
+    launch_of: np.ndarray
+    cls_override: np.ndarray
+    esrc: np.ndarray
+    edst: np.ndarray
+    ecls: np.ndarray
+    n_threads: int
+    n_layers: int
+
+
+def _template(b: _Builder, n_layers: int) -> _Template:
+    e = np.array(b.edges, dtype=np.int64).reshape(-1, 3)
+    return _Template(np.array(b.thread, np.int32), np.array(b.kind, np.uint8),
+                     np.array(b.layer, np.int32), np.array(b.launch_of, np.int64),
+                     np.array(b.cls_override, np.int32),
+                     e[:, 0], e[:, 1], e[:, 2].astype(np.uint8), b.n_threads, n_layers)
+
+
+_KERNEL_MEDIAN_NS = {K_GEMM: 400_000, K_ELEM: 20_000, K_AUX: 20_000, K_WU: 20_000,
+                     K_CONV: 50_000, K_GPU_OTHER: 50_000, K_OPT: 50_000, K_EMB: 30_000}
+
+
+def _durations(rng, kind: np.ndarray, medians: dict, memcpy_range, comm_ns=None):
+    n = kind.shape[0]
+    dur = np.zeros(n, np.int64)
+    gap = np.zeros(n, np.int64)
+    cpu = np.isin(kind, CPU_KINDS)
+    dur[cpu] = rng.integers(5_000, 15_001, size=int(cpu.sum()))
+    gap[cpu] = rng.integers(0, 3_001, size=int(cpu.sum()))
+    for k, med in medians.items():
+        m = kind == k
+        c = int(m.sum())
+        if c:
+            z = rng.standard_normal(c)
+            dur[m] = np.maximum(1, np.rint(med * np.exp(1.0 * z))).astype(np.int64)
+    m = kind == K_MEMCPY
+    if m.any():
+        dur[m] = rng.integers(memcpy_range[0], memcpy_range[1] + 1, size=int(m.sum()))
+    if comm_ns is not None:
+        m = kind == K_COMM
+        dur[m] = comm_ns
+    return dur, gap
+
+
+def _tile(t: _Template, iters: int, rng, medians, memcpy_range, name: str,
+          comm_ns=None) -> TaskGraph:
+    """Chain `iters` copies of one iteration: thread order continues across
+    iterations; dependency edges stay inside an iteration."""
+    n1 = t.thread.shape[0]
+    N = n1 * iters
+    thread = np.tile(t.thread, iters)
+    kind = np.tile(t.kind, iters)
+    layer = np.tile(t.layer, iters)
+    off = (np.arange(iters, dtype=np.int64) * n1)
+    lo = np.where(t.launch_of[None, :] >= 0, t.launch_of[None, :] + off[:, None], -1).reshape(-1)
+    # thread order: previous task on the same thread, across iteration borders
+    prev = np.full(N, -1, np.int32)
+    order = np.argsort(thread, kind="stable")
+    th_sorted = thread[order]
+    same = th_sorted[1:] == th_sorted[:-1]
+    prev[order[1:][same]] = order[:-1][same].astype(np.int32)
+    # edges
+    esrc = (t.esrc[None, :] + off[:, None]).reshape(-1)
+    edst = (t.edst[None, :] + off[:, None]).reshape(-1)
+    ecls = np.tile(t.ecls, iters)
+    ordr = np.argsort(edst, kind="stable")
+    esrc, edst, ecls = esrc[ordr], edst[ordr], ecls[ordr]
+    in_ptr = np.zeros(N + 1, np.int64)
+    np.add.at(in_ptr, edst + 1, 1)
+    in_ptr = np.cumsum(in_ptr)
+    dur, gap = _durations(rng, kind, medians, memcpy_range, None)
+    if comm_ns is not None:
+        m = kind == K_COMM
+        dur[m] = np.tile(comm_ns, iters)
+    L1 = t.n_layers + 1
+    node_cls = (np.where(layer >= 0, layer, t.n_layers) * N_KINDS + kind).astype(np.int64)
+    co = np.tile(t.cls_override, iters)
+    node_cls = np.where(co >= 0, L1 * N_KINDS + co, node_cls)
+    n_cls = int(L1 * N_KINDS + max(0, int(t.cls_override.max()) + 1))
+    return TaskGraph(N, t.n_threads, in_ptr, esrc.astype(np.int32), ecls.astype(np.uint8),
+                     prev, thread.astype(np.int32), dur, gap, node_cls.astype(np.uint16),
+                     n_cls, int(ecls.max()) + 1 if ecls.size else 1, kind, layer, lo, name)
+
+
+# ---------------------------------------------------------------------------
+# workload structures
+CPU, S0, MEMCPY_S, AUX_S = 0, 1, 2, 3
+
+
+def _cnn_iteration(n_layers=20) -> _Template:
+    """Small CNN: per layer 3 fwd + 6 bwd kernels (1 fwd + 2 bwd conv-like)
+    and 1 optimizer kernel, each issued by a CPU launch; one H2D memcpy at
+    the start; one end-of-iteration synchronization."""
+    b = _Builder(3)
+    _, mc = b.launch(CPU, MEMCPY_S, K_MEMCPY, -1)
+    first = True
+    for l in range(n_layers):
+        for j in range(3):
+            _, k = b.launch(CPU, S0, K_CONV if j == 0 else K_GPU_OTHER, l)
+            if first:
+                b.edge(mc, k)   # input batch must arrive before the first kernel
+                first = False
+    for l in reversed(range(n_layers)):
+        for j in range(6):
+            b.launch(CPU, S0, K_CONV if j < 2 else K_GPU_OTHER, l)
+    for l in range(n_layers):
+        b.launch(CPU, S0, K_OPT, l)
+    b.sync(CPU, [S0, MEMCPY_S], -1)
+    return _template(b, n_layers)
+
+
+def _transformer_iteration(n_layers=24, n_wu=554, comm=False, bucket_bytes=25 << 20,
+                           layer_grad_bytes=None):
+    """Transformer encoder iteration (Sec. 4 workloads; BERT-like): per layer
+    40 fwd kernels (8 GEMM-like) with one fork/join group of 8 aux-stream
+    kernels joined back through events, 80 bwd kernels (16 GEMM-like) and
+    n_wu element-wise weight-update kernels.  With comm=True, one all-reduce
+    per gradient bucket is issued on its own channel after the last backward
+    kernel of its bucket; the first weight-update kernel waits for all of
+    them (Sec. 3.2.1 communication tasks)."""
+    b = _Builder(4)
+    _, mc = b.launch(CPU, MEMCPY_S, K_MEMCPY, -1)
+    ks = []
+    for j in range(5):
+        _, k = b.launch(CPU, S0, K_EMB, -1)
+        if j == 0:
+            b.edge(mc, k)
+    fwd = {}
+    for l in range(n_layers):
+        fwd[l] = []
+        for j in range(40):
+            kind = K_GEMM if j % 5 == 0 else K_ELEM
+            _, k = b.launch(CPU, S0, kind, l)
+            fwd[l].append(k)
+            if j == 19:                    # fork: aux stream waits on this kernel
+                fork_src = k
+                for a in range(8):
+                    _, ka = b.launch(CPU, AUX_S, K_AUX, l)
+                    if a == 0:
+                        b.edge(fork_src, ka)
+                join_src = ka
+            if j == 29:                    # join: this kernel waits on the aux group
+                b.edge(join_src, k)
+    for j in range(8):
+        b.launch(CPU, S0, K_EMB, -1)       # loss
+    _, dl = b.launch(CPU, MEMCPY_S, K_MEMCPY, -1)   # D2H loss copy
+    b.sync(CPU, [MEMCPY_S], -1)
+    last_bwd = {}
+    bwd = {}
+    for l in reversed(range(n_layers)):
+        bwd[l] = []
+        for j in range(80):
+            kind = K_GEMM if j % 5 == 0 else K_ELEM
+            _, k = b.launch(CPU, S0, kind, l)
+            b.edge(fwd[l][j % 40], k)       # saved activation (same stream: dominated)
+            bwd[l].append(k)
+        last_bwd[l] = k
+    comm_nodes = []
+    if comm:
+        # gradient buckets: the byte stream of layer gradients in backward
+        # order cut every bucket_bytes (PyTorch DDP grouping); a bucket's
+        # all-reduce follows the last backward kernel among its layers
+        lg = layer_grad_bytes
+        total = n_layers * lg
+        buckets = []
+        for i in range((total + bucket_bytes - 1) // bucket_bytes):
+            hi = min((i + 1) * bucket_bytes, total)
+            r_last = (hi - 1) // lg                 # backward position of the last member
+            buckets.append((n_layers - 1 - r_last, hi - i * bucket_bytes))
+        for bi, (lay, nbytes) in enumerate(buckets):
+            ar = b.task(4 + bi, K_COMM, -1, cls_override=bi)
+            b.edge(last_bwd[lay], ar)
+            comm_nodes.append((ar, nbytes))
+        b.n_threads = 4 + len(buckets)
+    first_wu = None
+    for l in range(n_layers):
+        for j in range(n_wu):
+            _, k = b.launch(CPU, S0, K_WU, l)
+            if first_wu is None:
+                first_wu = k
+                for ar, _ in comm_nodes:
+                    b.edge(ar, k)
+            b.edge(bwd[l][j % 80], k)       # gradient producer (same stream: dominated)
+    b.sync(CPU, [S0, AUX_S], -1)
+    t = _template(b, n_layers)
+    return t, comm_nodes
+
+
+def _seq2seq_iteration(n_enc=8, n_dec=8, steps=50):
+    """Recurrent seq2seq: encoder and decoder stacks unrolled over timesteps,
+    6 small forward kernels per cell, 12 backward per cell, one optimizer
+    kernel per layer, an H2D memcpy and an end-of-iteration sync."""
+    b = _Builder(3)
+    _, mc = b.launch(CPU, MEMCPY_S, K_MEMCPY, -1)
+    L = n_enc + n_dec
+    first = True
+    for t_ in range(steps):
+        for l in range(L):
+            for j in range(6):
+                _, k = b.launch(CPU, S0, K_ELEM if j % 3 else K_GEMM, l)
+                if first:
+                    b.edge(mc, k)
+                    first = False
+    for t_ in reversed(range(steps)):
+        for l in reversed(range(L)):
+            for j in range(12):
+                b.launch(CPU, S0, K_ELEM if j % 3 else K_GEMM, l)
+    for l in range(L):
+        b.launch(CPU, S0, K_OPT, l)
+    b.sync(CPU, [S0, MEMCPY_S], -1)
+    return _template(b, L)
+
+
+# ---------------------------------------------------------------------------
+# variant tables
+def _identity_scale(C: int, V: int) -> np.ndarray:
+    s = np.ones((C, V, 2), np.int32)
+    return s
+
+
+def _cls_of(layer: int, kind: int, n_layers: int) -> int:
+    return (layer if layer >= 0 else n_layers) * N_KINDS + kind
+
+
+def _removal_bits(rng, N: int, V: int, kernels: np.ndarray, launches: np.ndarray,
+                  density: np.ndarray, chunk: int = 1 << 15) -> np.ndarray:
+    """Bernoulli(density[v]) removal of each removable kernel together with
+    its launch call, packed [N][ceil(V/32)]."""
+    W = (V + 31) // 32
+    out = np.zeros((N, W), np.uint32)
+    thr = np.minimum(np.rint(density * 65536.0), 65536).astype(np.uint32)
+    for s in range(0, kernels.shape[0], chunk):
+        kk = kernels[s:s + chunk]
+        u = rng.integers(0, 65536, size=(kk.shape[0], V), dtype=np.uint16)
+        words = pack_bits(u.astype(np.uint32) < thr[None, :])
+        out[kk] = words
+        ll = launches[s:s + chunk]
+        ok = ll >= 0
+        out[ll[ok]] = words[ok]
+    return out
+
+
+def _random_pq(rng, qs, pmax_factor=2, pmin=0):
+    q = int(rng.choice(qs))
+    p = int(rng.integers(pmin, pmax_factor * q + 1))
+    return p, q
+
+
+# ---------------------------------------------------------------------------
+def config(k: int, seed: Optional[int] = None, variants: Optional[int] = None,
+           iters: Optional[int] = None) -> Tuple[TaskGraph, VariantSet]:
+    """The five workloads.  `variants`/`iters` shrink a workload for tests."""
+    rng = np.random.default_rng(SEED_BASE + k if seed is None else seed)
+    if k == 1:
+        t = _cnn_iteration()
+        g = _tile(t, iters or 4, rng, _KERNEL_MEDIAN_NS, (500_000, 2_000_000), "cnn")
+        V = variants or 8
+        vs = _cnn_variants(rng, g, t.n_layers, V)
+    elif k in (2, 5):
+        t, _ = _transformer_iteration()
+        it = iters or (1 if k == 2 else 32)
+        g = _tile(t, it, rng, _KERNEL_MEDIAN_NS, (100_000, 400_000),
+                  "transformer" if k == 2 else "transformer-x%d" % it)
+        V = variants or (256 if k == 2 else 2048)
+        if k == 2:
+            vs = _transformer_variants(rng, g, t.n_layers, V, qs=(1, 2, 3, 4, 8))
+        else:
+            vs = _transformer_variants(rng, g, t.n_layers, V, qs=(1, 2, 4, 8))
+    elif k == 3:
+        hidden = 1024
+        layer_grad = 12 * hidden * hidden * 4 + 13 * hidden * 4   # fp32 grads per layer
+        t, comm = _transformer_iteration(comm=True, layer_grad_bytes=layer_grad)
+        # base all-reduce duration: bytes at 10 GB/s (1 GB/s = 1 byte/ns)
+        comm_ns = np.array([nb // 10 for _, nb in comm], np.int64)
+        g = _tile(t, iters or 1, rng, _KERNEL_MEDIAN_NS, (100_000, 400_000),
+                  "transformer+allreduce", comm_ns=comm_ns)
+        V = variants or 1024
+        # order edges between all-reduce channels live in classes 1..4
+        g, vs = _comm_variants(rng, g, t, [ar for ar, _ in comm], V)
+    elif k == 4:
+        t = _seq2seq_iteration()
+        g = _tile(t, iters or 9, rng, {K_GEMM: 15_000, K_ELEM: 15_000, K_OPT: 15_000},
+                  (100_000, 400_000), "seq2seq")
+        V = variants or 64
+        vs = _seq2seq_variants(rng, g, t.n_layers, V)
+    else:
+        raise ValueError("config must be 1..5")
+    return g, vs
+
+
+def _cnn_variants(rng, g: TaskGraph, L: int, V: int) -> VariantSet:
+    C = g.n_node_cls
+    s = _identity_scale(C, V)
+    gpu_cls = [_cls_of(l, kd, L) for l in list(range(L)) + [-1] for kd in GPU_KINDS + (K_MEMCPY,)]
+    conv_cls = [_cls_of(l, K_CONV, L) for l in range(L)]
+    launch_cls = [_cls_of(l, K_LAUNCH, L) for l in list(range(L)) + [-1]]
+    for v in range(V):
+        kind = v % 8
+        if kind == 1:
+            for c in gpu_cls:
+                s[c, v] = (2, 1)
+        elif kind == 2:
+            for c in conv_cls:
+                s[c, v] = (1, 2)
+        elif kind == 3:
+            for c in launch_cls:
+                s[c, v] = (0, 1)
+        elif kind >= 4:
+            for l in range(L):
+                if rng.random() < 0.5:
+                    for kd in (K_CONV, K_GPU_OTHER, K_OPT):
+                        s[_cls_of(l, kd, L), v] = _random_pq(rng, (2, 4, 8), 2, 1)
+    rb = np.zeros((g.n, (V + 31) // 32), np.uint32)
+    eo = np.ones((V, 1), np.uint64)
+    return VariantSet(V, s, rb, eo, [(0, V, 1)])
+
+
+def _removable(g: TaskGraph, kinds) -> Tuple[np.ndarray, np.ndarray]:
+    k = np.nonzero(np.isin(g.kind, kinds))[0]
+    return k.astype(np.int64), g.launch_of[k].astype(np.int64)
+
+
+def _transformer_variants(rng, g: TaskGraph, L: int, V: int, qs) -> VariantSet:
+    C = g.n_node_cls
+    s = _identity_scale(C, V)
+    kinds = (K_GEMM, K_ELEM, K_AUX, K_WU, K_LAUNCH)
+    for v in range(1, V):
+        for l in range(L):
+            for kd in kinds:
+                if rng.random() < 0.5:
+                    s[_cls_of(l, kd, L), v] = _random_pq(rng, qs, 2, 0)
+    dens = rng.uniform(0.1, 0.5, size=V)
+    dens[0] = 0.0
+    kern, lau = _removable(g, (K_ELEM, K_WU, K_AUX))
+    rb = _removal_bits(rng, g.n, V, kern, lau, dens)
+    eo = np.ones((V, 1), np.uint64)
+    return VariantSet(V, s, rb, eo, [(0, V, 1)])
+
+
+def _comm_variants(rng, g: TaskGraph, t: _Template, ars: List[int], V: int):
+    """Four channel-order groups (ready order, reverse, front-layers-first,
+    seeded permutation) x bandwidth {10, 25, 100} GB/s x per-bucket 1/4
+    compression.  Order edges are added to the graph with classes 1..4."""
+    n1 = t.thread.shape[0]
+    iters = g.n // n1
+    B = len(ars)
+    orders = [list(range(B)), list(reversed(range(B))),
+              list(range(0, B, 2)) + list(range(1, B, 2)),      # interleaved priority
+              [int(x) for x in rng.permutation(B)]]
+    extra_src, extra_dst, extra_cls = [], [], []
+    for it in range(iters):
+        base = it * n1
+        for gi, od in enumerate(orders):
+            for a, bq in zip(od[:-1], od[1:]):
+                extra_src.append(base + ars[a])
+                extra_dst.append(base + ars[bq])
+                extra_cls.append(1 + gi)
+    # rebuild CSR with the extra edges
+    dst_old = np.repeat(np.arange(g.n, dtype=np.int64), np.diff(g.in_ptr))
+    src = np.concatenate([g.in_src.astype(np.int64), np.array(extra_src, np.int64)])
+    dst = np.concatenate([dst_old, np.array(extra_dst, np.int64)])
+    cls = np.concatenate([g.edge_cls, np.array(extra_cls, np.uint8)])
+    o = np.argsort(dst, kind="stable")
+    src, dst, cls = src[o], dst[o], cls[o]
+    in_ptr = np.zeros(g.n + 1, np.int64)
+    np.add.at(in_ptr, dst + 1, 1)
+    in_ptr = np.cumsum(in_ptr)
+    g = dataclasses.replace(g, in_ptr=in_ptr, in_src=src.astype(np.int32),
+                            edge_cls=cls.astype(np.uint8), n_edge_cls=5)
+    C = g.n_node_cls
+    L = t.n_layers
+    s = _identity_scale(C, V)
+    ar_cls0 = (L + 1) * N_KINDS
+    per = V // 4
+    eo = np.zeros((V, 1), np.uint64)
+    batches = []
+    for gi in range(4):
+        v0 = gi * per
+        v1 = V if gi == 3 else (gi + 1) * per
+        batches.append((v0, v1, 1 | (1 << (1 + gi))))
+        for v in range(v0, v1):
+            eo[v, 0] = np.uint64(1 | (1 << (1 + gi)))
+            j = v - v0
+            bw = j % 3
+            bwp, bwq = [(1, 1), (2, 5), (1, 10)][bw]
+            comp = rng.random(B) < 0.5 if j >= 3 else np.zeros(B, bool)
+            for b_ in range(B):
+                p, q = bwp, bwq * (4 if comp[b_] else 1)
+                gg = np.gcd(p, q)
+                s[ar_cls0 + b_, v] = (p // gg, q // gg)
+            if j >= 6 and rng.random() < 0.5:     # AMP-like GPU scaling on some variants
+                for l in range(L):
+                    s[_cls_of(l, K_GEMM, L), v] = (1, 3)
+                    s[_cls_of(l, K_ELEM, L), v] = (1, 2)
+    rb = np.zeros((g.n, (V + 31) // 32), np.uint32)
+    return g, VariantSet(V, s, rb, eo, batches)
+
+
+def _seq2seq_variants(rng, g: TaskGraph, L: int, V: int) -> VariantSet:
+    C = g.n_node_cls
+    s = _identity_scale(C, V)
+    lscales = [(1, 1), (0, 1), (1, 4), (1, 2), (2, 1)]
+    launch_cls = [_cls_of(l, K_LAUNCH, L) for l in list(range(L)) + [-1]]
+    for v in range(V):
+        p, q = lscales[v % 5]
+        for c in launch_cls:
+            s[c, v] = (p, q)
+    dens = rng.uniform(0.1, 0.5, size=V)
+    dens[0] = 0.0
+    kern, lau = _removable(g, (K_ELEM,))
+    rb = _removal_bits(rng, g.n, V, kern, lau, dens)
+    eo = np.ones((V, 1), np.uint64)
+    return VariantSet(V, s, rb, eo, [(0, V, 1)])
+
+
+# ---------------------------------------------------------------------------
+def random_graph(rng, n: int, n_threads: int, p_edge: float = 0.3, max_dur: int = 20,
+                 zero_frac: float = 0.2, n_edge_cls: int = 1,
+                 same_thread_edges: bool = True) -> TaskGraph:
+    """A small random DAG: tasks in id order (topological), random thread
+    assignment, random forward dependency edges, durations incl. 0."""
+    thread = rng.integers(0, n_threads, size=n).astype(np.int32)
+    prev = np.full(n, -1, np.int32)
+    last = {}
+    for i in range(n):
+        t = int(thread[i])
+        if t in last:
+            prev[i] = last[t]
+        last[t] = i
+    srcs, dsts, cls = [], [], []
+    for j in range(n):
+        for i in range(j):
+            if rng.random() < p_edge and (same_thread_edges or thread[i] != thread[j]):
+                srcs.append(i)
+                dsts.append(j)
+                cls.append(int(rng.integers(0, n_edge_cls)))
+    in_ptr = np.zeros(n + 1, np.int64)
+    for d in dsts:
+        in_ptr[d + 1] += 1
+    in_ptr = np.cumsum(in_ptr)
+    dur = rng.integers(0, max_dur + 1, size=n).astype(np.int64)
+    dur[rng.random(n) < zero_frac] = 0
+    gap = rng.integers(0, max_dur // 2 + 1, size=n).astype(np.int64)
+    gap[rng.random(n) < 0.5] = 0
+    kind = np.zeros(n, np.uint8)
+    return TaskGraph(n, n_threads, in_ptr, np.array(srcs, np.int32),
+                     np.array(cls, np.uint8), prev, thread, dur, gap,
+                     rng.integers(0, 3, size=n).astype(np.uint16), 3, n_edge_cls,
+                     kind, np.full(n, -1, np.int32), np.full(n, -1, np.int64), "random")
+
+
+def random_variants(rng, g: TaskGraph, V: int, p_remove: float = 0.2,
+                    qs=(1, 2, 3, 4, 5, 7, 8, 10)) -> VariantSet:
+    C = g.n_node_cls
+    s = np.ones((C, V, 2), np.int32)
+    for v in range(1, V):
+        for c in range(C):
+            if rng.random() < 0.6:
+                s[c, v] = _random_pq(rng, qs, 3, 0)
+    bits = rng.random((g.n, V)) < p_remove
+    bits[:, 0] = False
+    rb = pack_bits(bits)
+    K = g.n_edge_cls
+    eo = np.zeros((V, 1), np.uint64)
+    for v in range(V):
+        m = int(rng.integers(0, 1 << K)) | 1
+        eo[v, 0] = np.uint64(m)
+    eo[0, 0] = np.uint64((1 << K) - 1)
+    return VariantSet(V, s, rb, eo, [(0, V, (1 << K) - 1)])

@@ -1,0 +1,89 @@
+"""The pins are sensitive: each plausible mistake planted in a temporary copy
+of the oracle (never in the oracle itself) makes at least one pin fail."""
+import ctypes
+import os
+import subprocess
+import tempfile
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from tests import test_oracle_pins as P
+
+SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                   "oracle", "dd_oracle.c")
+
+MUTANTS = {
+    "gap_not_propagated": ("int64_t rel = s + w->dd[u] + w->gg[u];",
+                           "int64_t rel = s + w->dd[u];"),
+    "ceil_instead_of_floor": ("return (int64_t)(a / (__int128)q);",
+                              "return (int64_t)((a + q - 1) / (__int128)q);"),
+    "edge_classes_ignored": ("return (int)((w >> (cls % 64)) & 1u);", "return 1;"),
+    "removed_task_in_makespan": ("if (!w->rm[u] && f > ms) ms = f;", "if (f > ms) ms = f;"),
+    "removed_keeps_gap": ("w->gg[u] = r ? 0 : g->gap[u];", "w->gg[u] = g->gap[u];"),
+    "finish_includes_gap": ("int64_t f = w->S[u] + w->dd[u];",
+                            "int64_t f = w->S[u] + w->dd[u] + w->gg[u];"),
+    "wrong_variant_bit": ("return (int)((vs->rm_bits[(int64_t)u * W + v / 32] >> (v % 32)) & 1u);",
+                          "return (int)((vs->rm_bits[(int64_t)u * W + v / 32] >> ((v + 1) % 32)) & 1u);"),
+}
+
+
+def _build_mutant(name):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) >= 1, name
+    src = src.replace(old, new, 1)
+    d = tempfile.mkdtemp(prefix="ddo_mut_")
+    c = os.path.join(d, "m.c")
+    so = os.path.join(d, "libm.so")
+    open(c, "w").write(src)
+    subprocess.check_call(["gcc", "-O1", "-std=gnu11", "-fPIC", "-shared", "-pthread",
+                           "-w", "-o", so, c])
+    return so
+
+
+class _Mut:
+    def __init__(self, so):
+        lib = ctypes.CDLL(so)
+        lib.ddo_run.restype = ctypes.c_int
+        lib.ddo_run.argtypes = O._load().ddo_run.argtypes
+        self.lib = lib
+        self.OracleError = O.OracleError
+        self.ECYCLE = O.ECYCLE
+
+    def run(self, *a, **k):
+        saved = O._lib
+        O._lib = self.lib
+        try:
+            return O.run(*a, **k)
+        finally:
+            O._lib = saved
+
+
+def _pins_fail(m):
+    """Run a fast subset of the pins against the mutant; True if any fails."""
+    checks = []
+    for seed in range(60):
+        g, vs = P._random_case(seed)
+        try:
+            S, F, ms, _ = m.run(g, vs)
+        except Exception:
+            return True
+        for v in range(vs.n_variants):
+            bS, bF, bms = P.brute_force(g, vs, v)
+            if list(S[v]) != bS or list(F[v]) != bF or ms[v] != bms:
+                return True
+    for d, p, q, e in P._floor_rows():
+        g = P.H.graph(1, [0], [], [d], [0])
+        _, _, ms, _ = m.run(g, P.H.variants(g, scales=[{0: (p, q)}]))
+        if ms[0] != e:
+            return True
+    return False
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_planted_mistake_is_caught(name):
+    O.build(force=False)
+    m = _Mut(_build_mutant(name))
+    assert _pins_fail(m), "pins did not catch mutant " + name

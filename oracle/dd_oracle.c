@@ -463,3 +463,56 @@ int ddo_run(const ddo_graph *g, const ddo_variants *vs,
     free_struct(&st);
     return j.rc;
 }
+
+/* ------------------------------------------------------------------ */
+/* Topological steps of the graph restricted to the edge classes in `mask`
+ * (thread order always present), by Kahn's algorithm (the reference counts
+ * and frontier of Sec. 3.1, Algorithm 1, popped first-in first-out):
+ *   level[u] = longest path to u counted in edges (Kahn level);
+ *   phase[u] = longest path to u where a dependency between two different
+ *              threads counts 1 and thread order (or a dependency inside
+ *              one thread) counts 0.
+ * Returns DDO_ECYCLE if some task is never freed. */
+int ddo_steps(const ddo_graph *g, uint64_t mask, int32_t *level, int32_t *phase) {
+    const int32_t n = g->n;
+    ddo_struct st;
+    memset(&st, 0, sizeof(st));
+    int rc = build_struct(g, &st);
+    int32_t *ref = malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
+    int32_t *queue = malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
+    if (rc || !ref || !queue) { free_struct(&st); free(ref); free(queue); return DDO_ENOMEM; }
+    for (int32_t u = 0; u < n; u++) {
+        int32_t r = g->thread_prev[u] >= 0 ? 1 : 0;
+        for (int64_t e = g->in_ptr[u]; e < g->in_ptr[u + 1]; e++) {
+            int c = g->edge_cls ? g->edge_cls[e] : 0;
+            if ((mask >> c) & 1u) r++;
+        }
+        ref[u] = r;
+        level[u] = 0;
+        phase[u] = 0;
+    }
+    int32_t head = 0, tail = 0;
+    for (int32_t u = 0; u < n; u++)
+        if (ref[u] == 0) queue[tail++] = u;
+    while (head < tail) {
+        int32_t u = queue[head++];
+        for (int64_t e = st.out_ptr[u]; e < st.out_ptr[u + 1]; e++) {
+            if (!((mask >> st.out_cls[e]) & 1u)) continue;
+            int32_t c = st.out_dst[e];
+            int32_t w = g->thread_id[c] != g->thread_id[u] ? 1 : 0;
+            if (level[u] + 1 > level[c]) level[c] = level[u] + 1;
+            if (phase[u] + w > phase[c]) phase[c] = phase[u] + w;
+            if (--ref[c] == 0) queue[tail++] = c;
+        }
+        int32_t c = st.thread_next[u];
+        if (c >= 0) {
+            if (level[u] + 1 > level[c]) level[c] = level[u] + 1;
+            if (phase[u] > phase[c]) phase[c] = phase[u];
+            if (--ref[c] == 0) queue[tail++] = c;
+        }
+    }
+    free_struct(&st);
+    free(ref);
+    free(queue);
+    return tail == n ? DDO_OK : DDO_ECYCLE;
+}

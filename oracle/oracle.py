@@ -61,6 +61,9 @@ def _load():
                                  ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                  ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32]
+        _lib.ddo_steps.restype = ctypes.c_int
+        _lib.ddo_steps.argtypes = [ctypes.POINTER(_Graph), ctypes.c_uint64, ctypes.c_void_p,
+                                   ctypes.c_void_p]
     return _lib
 
 
@@ -72,6 +75,34 @@ class OracleError(RuntimeError):
     def __init__(self, code):
         super().__init__("oracle status %d" % code)
         self.code = code
+
+
+def _graph_struct(g):
+    arrs = dict(in_ptr=np.ascontiguousarray(g.in_ptr, np.int64),
+                in_src=np.ascontiguousarray(g.in_src, np.int32),
+                edge_cls=np.ascontiguousarray(g.edge_cls, np.uint8),
+                thread_prev=np.ascontiguousarray(g.thread_prev, np.int32),
+                thread_id=np.ascontiguousarray(g.thread_id, np.int32),
+                dur=np.ascontiguousarray(g.dur, np.int64),
+                gap=np.ascontiguousarray(g.gap, np.int64),
+                node_cls=np.ascontiguousarray(g.node_cls, np.uint16))
+    gs = _Graph(int(g.n), int(g.n_threads), *[_p(arrs[k]) for k in
+                ("in_ptr", "in_src", "edge_cls", "thread_prev", "thread_id", "dur", "gap",
+                 "node_cls")])
+    return gs, arrs
+
+
+def steps(g, mask: int = (1 << 64) - 1):
+    """Kahn levels and phases of every task (edge classes in `mask`)."""
+    lib = _load()
+    gs, keep = _graph_struct(g)
+    level = np.zeros(max(g.n, 1), np.int32)
+    phase = np.zeros(max(g.n, 1), np.int32)
+    rc = lib.ddo_steps(ctypes.byref(gs), ctypes.c_uint64(mask & (2 ** 64 - 1)), _p(level),
+                       _p(phase))
+    if rc != OK:
+        raise OracleError(rc)
+    return level[:g.n], phase[:g.n]
 
 
 def run(g, vs, variants: Optional[Sequence[int]] = None, mode: int = 0, tie: int = 0,

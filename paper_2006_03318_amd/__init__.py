@@ -1,0 +1,10 @@
+"""Batched what-if simulation of trace-derived task graphs on MI355X.
+
+The compute path is libdd.so (HIP kernels for gfx950 behind the C-ABI of
+include/dd.h); `binding` exposes it with the same names.
+"""
+from . import binding  # noqa: F401
+from .binding import (DD_LEVELS, DD_PHASES, DDError, dd_apply_transforms, dd_graph_free,  # noqa: F401
+                      dd_graph_load, dd_last_error, dd_levelize, dd_sched_free,
+                      dd_sched_info, dd_sched_task_steps, dd_simulate_batch, dd_status_str,
+                      dd_variants_free)

@@ -1,0 +1,411 @@
+// C-ABI of the dd library: handle management, argument checks, and the
+// order in which the device passes of each call run.
+
+#include <atomic>
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "dd_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+std::atomic<uint64_t> g_next_id{1};
+
+dd_status fail(dd_status s, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+dd_status hip_fail(hipError_t e, const char *what) {
+    return fail(e == hipErrorOutOfMemory ? DD_ENOMEM : DD_EHIP, "%s: %s", what,
+                hipGetErrorString(e));
+}
+
+void configure_pool_once() {
+    static std::atomic<uint64_t> done_mask{0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev >= 64) return;
+    const uint64_t bit = 1ull << dev;
+    if (done_mask.load() & bit) return;
+    hipMemPool_t pool;
+    if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+        uint64_t thr = UINT64_MAX;   // keep freed blocks cached for the next call
+        (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
+    }
+    done_mask.fetch_or(bit);
+}
+
+dd_status map_err_bits(uint32_t e) {
+    using namespace dd;
+    if (e & ERR_THREAD_RANGE) return fail(DD_EINVAL, "thread_id outside [0, n_threads)");
+    if (e & ERR_PREV_RANGE) return fail(DD_EINVAL, "thread_prev outside [-1, n) or naming the task itself");
+    if (e & ERR_NEG_TIME) return fail(DD_EINVAL, "negative duration or gap");
+    if (e & ERR_PTR_ORDER) return fail(DD_EINVAL, "in_ptr is not non-decreasing");
+    if (e & ERR_SRC_RANGE) return fail(DD_EINVAL, "in_src outside [0, n)");
+    if (e & ERR_EDGE_CLS) return fail(DD_EINVAL, "edge class >= 64");
+    if (e & ERR_SCALE) return fail(DD_EINVAL, "scale with p < 0 or q < 1");
+    if (e & ERR_BIG_TIME) return fail(DD_ERANGE, "duration or gap >= 2^62 ns");
+    if (e & ERR_PREV_THREAD) return fail(DD_ECHAIN, "thread_prev names a task on another thread");
+    if (e & ERR_SUCC) return fail(DD_ECHAIN, "two tasks name the same thread_prev");
+    if (e & ERR_HEADS) return fail(DD_ECHAIN, "a thread has more than one first task");
+    if (e & ERR_CHAIN_CYCLE) return fail(DD_ECHAIN, "thread order loops");
+    if (e & ERR_SELF_LOOP) return fail(DD_ECYCLE, "dependency from a task to itself");
+    if (e & ERR_BACK_EDGE) return fail(DD_ECYCLE, "dependency goes backwards along one thread");
+    if (e & ERR_KAHN_CYCLE) return fail(DD_ECYCLE, "dependencies plus thread order contain a cycle");
+    return DD_OK;
+}
+
+template <class T>
+hipError_t copy_in(T **dst, const T *src, size_t count, hipStream_t s) {
+    hipError_t e = dd::dalloc_n(dst, count, s);
+    if (e != hipSuccess) return e;
+    if (count == 0) return hipSuccess;
+    if (src) return hipMemcpyAsync(*dst, src, count * sizeof(T), hipMemcpyDefault, s);
+    return hipMemsetAsync(*dst, 0, count * sizeof(T), s);
+}
+
+void free_graph_arrays(dd_graph *g) {
+    hipStream_t s = g->stream;
+    dd::dfree(g->thread_prev, s); dd::dfree(g->thread_id, s); dd::dfree(g->dur, s);
+    dd::dfree(g->gap, s); dd::dfree(g->cls, s); dd::dfree(g->rank, s);
+    dd::dfree(g->thread_base, s); dd::dfree(g->order, s); dd::dfree(g->xin_ptr, s);
+    dd::dfree(g->xin_src, s); dd::dfree(g->xin_cls, s);
+}
+
+void free_sched_arrays(dd_sched *x) {
+    hipStream_t s = x->stream;
+    dd::dfree(x->step_ptr, s); dd::dfree(x->pos_node, s); dd::dfree(x->pos_flags, s);
+    dd::dfree(x->pos_dur, s); dd::dfree(x->pos_gap, s); dd::dfree(x->pos_cls, s);
+    dd::dfree(x->gat_ptr, s); dd::dfree(x->gat_src, s); dd::dfree(x->gat_pos, s);
+    dd::dfree(x->gat_cls, s); dd::dfree(x->gat_gap, s); dd::dfree(x->node_step, s);
+}
+
+}  // namespace
+
+namespace dd {
+
+hipError_t dalloc(void **p, size_t bytes, hipStream_t s) {
+    configure_pool_once();
+    *p = nullptr;
+    if (bytes == 0) bytes = 16;
+    return hipMallocAsync(p, bytes, s);
+}
+
+void dfree(void *p, hipStream_t s) {
+    if (p) (void)hipFreeAsync(p, s);
+}
+
+}  // namespace dd
+
+#define TRY(x, what)                                           \
+    do {                                                       \
+        hipError_t e_ = (x);                                   \
+        if (e_ != hipSuccess) { st = hip_fail(e_, what); goto fail_out; } \
+    } while (0)
+
+extern "C" {
+
+const char *dd_status_str(dd_status s) {
+    switch (s) {
+        case DD_OK: return "DD_OK";
+        case DD_EINVAL: return "DD_EINVAL";
+        case DD_ECYCLE: return "DD_ECYCLE";
+        case DD_ECHAIN: return "DD_ECHAIN";
+        case DD_ERANGE: return "DD_ERANGE";
+        case DD_ENOMEM: return "DD_ENOMEM";
+        case DD_EHIP: return "DD_EHIP";
+        case DD_EMISMATCH: return "DD_EMISMATCH";
+    }
+    return "DD_UNKNOWN";
+}
+
+const char *dd_last_error(void) { return g_err; }
+
+dd_status dd_graph_load(int32_t n, int32_t n_threads, const int64_t *in_ptr, const int32_t *in_src,
+                        const uint8_t *edge_cls, const int32_t *thread_prev,
+                        const int32_t *thread_id, const int64_t *dur_ns, const int64_t *gap_ns,
+                        const uint16_t *node_cls, void *stream, dd_graph **out) {
+    g_err[0] = 0;
+    if (!out) return fail(DD_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (n < 0) return fail(DD_EINVAL, "n < 0");
+    if (n_threads < 1) return fail(DD_EINVAL, "n_threads < 1");
+    if (!in_ptr) return fail(DD_EINVAL, "in_ptr is NULL");
+    if (n > 0 && (!thread_prev || !thread_id || !dur_ns || !gap_ns))
+        return fail(DD_EINVAL, "thread_prev, thread_id, dur_ns and gap_ns are required");
+    hipStream_t s = (hipStream_t)stream;
+    dd_status st = DD_OK;
+    dd_graph *g = new dd_graph();
+    g->n = n;
+    g->n_threads = n_threads;
+    g->stream = s;
+    g->id = g_next_id.fetch_add(1);
+    (void)hipGetDevice(&g->device);
+    int64_t *d_in_ptr = nullptr, *cnt = nullptr, *len = nullptr;
+    int32_t *d_in_src = nullptr, *succ = nullptr, *heads = nullptr, *nxt = nullptr,
+            *nxt2 = nullptr, *rank2 = nullptr;
+    uint8_t *d_ecls = nullptr;
+    uint32_t *err = nullptr;
+    dd::LoadStats *stats = nullptr;
+    int64_t ends[2] = {0, 0};
+    uint32_t h_err = 0;
+    dd::LoadStats hs{};
+    const size_t N1 = (size_t)n + 1;
+    int64_t E = 0;
+
+    TRY(copy_in(&d_in_ptr, in_ptr, N1, s), "copy in_ptr");
+    TRY(hipMemcpyAsync(&ends[0], d_in_ptr, sizeof(int64_t), hipMemcpyDeviceToHost, s), "read in_ptr");
+    TRY(hipMemcpyAsync(&ends[1], d_in_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s), "read in_ptr");
+    TRY(hipStreamSynchronize(s), "sync");
+    if (ends[0] != 0) { st = fail(DD_EINVAL, "in_ptr[0] != 0"); goto fail_out; }
+    E = ends[1];
+    if (E < 0 || E >= (int64_t(1) << 31)) { st = fail(DD_EINVAL, "edge count outside [0, 2^31)"); goto fail_out; }
+    if (E > 0 && !in_src) { st = fail(DD_EINVAL, "in_src is NULL"); goto fail_out; }
+    g->n_edges = E;
+    TRY(copy_in(&d_in_src, in_src, (size_t)E, s), "copy in_src");
+    TRY(copy_in(&d_ecls, edge_cls, (size_t)E, s), "copy edge_cls");
+    TRY(copy_in(&g->thread_prev, thread_prev, (size_t)n, s), "copy thread_prev");
+    TRY(copy_in(&g->thread_id, thread_id, (size_t)n, s), "copy thread_id");
+    TRY(copy_in(&g->dur, dur_ns, (size_t)n, s), "copy dur");
+    TRY(copy_in(&g->gap, gap_ns, (size_t)n, s), "copy gap");
+    TRY(copy_in(&g->cls, node_cls, (size_t)n, s), "copy node_cls");
+    TRY(copy_in(&succ, (const int32_t *)nullptr, (size_t)n, s), "alloc");
+    TRY(copy_in(&heads, (const int32_t *)nullptr, (size_t)n_threads, s), "alloc");
+    TRY(copy_in(&err, (const uint32_t *)nullptr, 2, s), "alloc");
+    TRY(copy_in(&stats, (const dd::LoadStats *)nullptr, 1, s), "alloc");
+    if (n > 0) TRY(dd::launch_validate_nodes(g, d_in_ptr, succ, heads, err, stats, s), "validate");
+    TRY(hipMemcpyAsync(&h_err, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "read err");
+    TRY(hipStreamSynchronize(s), "sync");
+    if (h_err) { st = map_err_bits(h_err); goto fail_out; }
+    if (n > 0) TRY(dd::launch_validate_edges(g, d_in_ptr, d_in_src, edge_cls ? d_ecls : nullptr, err, s), "validate edges");
+    TRY(dd::dalloc_n(&g->rank, N1, s), "alloc rank");
+    TRY(dd::dalloc_n(&nxt, N1, s), "alloc");
+    TRY(dd::dalloc_n(&nxt2, N1, s), "alloc");
+    TRY(dd::dalloc_n(&rank2, N1, s), "alloc");
+    if (n > 0) TRY(dd::launch_rank_chains(g, succ, nxt, nxt2, rank2, err, s), "rank chains");
+    TRY(hipMemcpyAsync(&h_err, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "read err");
+    TRY(hipStreamSynchronize(s), "sync");
+    if (h_err) { st = map_err_bits(h_err); goto fail_out; }
+    TRY(dd::dalloc_n(&g->thread_base, (size_t)n_threads + 1, s), "alloc");
+    TRY(dd::dalloc_n(&len, (size_t)n_threads + 1, s), "alloc");
+    TRY(dd::dalloc_n(&g->order, N1, s), "alloc");
+    TRY(dd::launch_build_order(g, succ, len, s), "order");
+    TRY(dd::dalloc_n(&g->xin_ptr, N1, s), "alloc");
+    TRY(dd::dalloc_n(&cnt, N1, s), "alloc");
+    if (n > 0) {
+        TRY(dd::launch_cross_edges(g, d_in_ptr, d_in_src, edge_cls ? d_ecls : nullptr, cnt, err, stats, s), "cross edges");
+    } else {
+        TRY(hipMemsetAsync(g->xin_ptr, 0, sizeof(int64_t), s), "memset");
+    }
+    TRY(hipMemcpyAsync(&h_err, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "read err");
+    TRY(hipMemcpyAsync(&g->n_cross, g->xin_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s), "read");
+    TRY(hipMemcpyAsync(&hs, stats, sizeof(hs), hipMemcpyDeviceToHost, s), "read stats");
+    TRY(hipStreamSynchronize(s), "sync");
+    if (h_err) { st = map_err_bits(h_err); goto fail_out; }
+    TRY(dd::dalloc_n(&g->xin_src, (size_t)g->n_cross + 1, s), "alloc");
+    TRY(dd::dalloc_n(&g->xin_cls, (size_t)g->n_cross + 1, s), "alloc");
+    if (n > 0) TRY(dd::launch_cross_fill(g, d_in_ptr, d_in_src, edge_cls ? d_ecls : nullptr, s), "cross fill");
+    g->dsum = ((__int128)hs.dsum_hi << 32) + (__int128)hs.dsum_lo;
+    {
+        const __int128 gs = ((__int128)hs.gsum_hi << 32) + (__int128)hs.gsum_lo;
+        g->gsum = gs >= ((__int128)1 << 62) ? ((int64_t)1 << 62) : (int64_t)gs;
+    }
+    g->dmax = (int64_t)hs.dmax;
+    g->max_cls = (int32_t)hs.cls_max;
+    g->cross_mask = hs.cross_mask;
+    if (g->dsum + (__int128)g->gsum >= ((__int128)1 << 62)) {
+        st = fail(DD_ERANGE, "sum of durations and gaps reaches 2^62 ns");
+        goto fail_out;
+    }
+    TRY(hipStreamSynchronize(s), "sync");
+    dd::dfree(d_in_ptr, s); dd::dfree(d_in_src, s); dd::dfree(d_ecls, s); dd::dfree(succ, s);
+    dd::dfree(heads, s); dd::dfree(err, s); dd::dfree(stats, s); dd::dfree(nxt, s);
+    dd::dfree(nxt2, s); dd::dfree(rank2, s); dd::dfree(cnt, s); dd::dfree(len, s);
+    *out = g;
+    return DD_OK;
+fail_out:
+    (void)hipStreamSynchronize(s);
+    dd::dfree(d_in_ptr, s); dd::dfree(d_in_src, s); dd::dfree(d_ecls, s); dd::dfree(succ, s);
+    dd::dfree(heads, s); dd::dfree(err, s); dd::dfree(stats, s); dd::dfree(nxt, s);
+    dd::dfree(nxt2, s); dd::dfree(rank2, s); dd::dfree(cnt, s); dd::dfree(len, s);
+    free_graph_arrays(g);
+    delete g;
+    return st;
+}
+
+dd_status dd_levelize(const dd_graph *g, uint64_t active_edge_classes, int32_t mode, void *stream,
+                      dd_sched **out, int64_t *n_steps_out) {
+    g_err[0] = 0;
+    if (!out) return fail(DD_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!g) return fail(DD_EINVAL, "graph is NULL");
+    if (mode != DD_LEVELS && mode != DD_PHASES) return fail(DD_EINVAL, "mode must be DD_LEVELS or DD_PHASES");
+    hipStream_t s = (hipStream_t)stream;
+    dd_sched *x = new dd_sched();
+    x->graph_id = g->id;
+    x->stream = s;
+    char msg[256] = "";
+    dd_status st = dd::levelize_device(g, active_edge_classes, mode, x, s, msg, sizeof(msg));
+    if (st != DD_OK) {
+        fail(st, "%s", msg);
+        (void)hipStreamSynchronize(s);
+        free_sched_arrays(x);
+        delete x;
+        return st;
+    }
+    if (n_steps_out) *n_steps_out = x->n_steps;
+    *out = x;
+    return DD_OK;
+}
+
+dd_status dd_apply_transforms(const dd_graph *g, int32_t n_variants, int32_t n_cls,
+                              const dd_ratio *scale, const uint32_t *remove_bits,
+                              const uint64_t *edge_on, void *stream, dd_variants **out) {
+    g_err[0] = 0;
+    if (!out) return fail(DD_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!g) return fail(DD_EINVAL, "graph is NULL");
+    if (n_variants < 1) return fail(DD_EINVAL, "n_variants < 1");
+    if (!scale) n_cls = g->max_cls + 1;
+    if (n_cls < 1 || n_cls <= g->max_cls)
+        return fail(DD_EINVAL, "n_cls (%d) must exceed the largest task class (%d)", n_cls, g->max_cls);
+    if ((int64_t)n_cls * n_variants >= (int64_t(1) << 31))
+        return fail(DD_EINVAL, "n_cls * n_variants too large");
+    hipStream_t s = (hipStream_t)stream;
+    dd_status st = DD_OK;
+    dd_variants *x = new dd_variants();
+    x->graph_id = g->id;
+    x->n = g->n;
+    x->V = n_variants;
+    x->W = (n_variants + 31) / 32;
+    x->n_cls = n_cls;
+    x->stream = s;
+    dd_ratio *d_scale = nullptr;
+    uint32_t *err = nullptr;
+    uint32_t h_err[6] = {0, 0, 0, 0, 0, 0};
+    uint64_t *h_on = nullptr;
+    const size_t cv = (size_t)n_cls * n_variants;
+    TRY(dd::dalloc_n(&x->table, cv, s), "alloc table");
+    if (scale) TRY(copy_in(&d_scale, scale, cv, s), "copy scale");
+    TRY(copy_in(&err, (const uint32_t *)nullptr, 6, s), "alloc");
+    TRY(dd::launch_build_scale_table(d_scale, n_cls, n_variants, x->table, err, s), "scale table");
+    TRY(copy_in(&x->rm_bits, remove_bits, (size_t)g->n * x->W, s), "copy remove_bits");
+    TRY(dd::dalloc_n(&x->edge_on, (size_t)n_variants, s), "alloc edge_on");
+    h_on = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)n_variants);
+    if (!h_on) { st = fail(DD_ENOMEM, "host allocation"); goto fail_out; }
+    if (edge_on) {
+        TRY(hipMemcpyAsync(h_on, edge_on, sizeof(uint64_t) * (size_t)n_variants, hipMemcpyDefault, s), "read edge_on");
+    } else {
+        for (int32_t v = 0; v < n_variants; v++) h_on[v] = ~0ull;
+    }
+    TRY(hipMemcpyAsync(h_err, err, sizeof(h_err), hipMemcpyDeviceToHost, s), "read err");
+    TRY(hipStreamSynchronize(s), "sync");
+    TRY(hipMemcpyAsync(x->edge_on, h_on, sizeof(uint64_t) * (size_t)n_variants, hipMemcpyHostToDevice, s), "copy edge_on");
+    x->used_mask = 0;
+    for (int32_t v = 0; v < n_variants; v++) x->used_mask |= h_on[v];
+    if (h_err[0]) { st = map_err_bits(h_err[0]); goto fail_out; }
+    {
+        uint64_t pmax, rbits;
+        memcpy(&pmax, &h_err[2], 8);
+        memcpy(&rbits, &h_err[4], 8);
+        double rmax;
+        memcpy(&rmax, &rbits, 8);
+        // d * p must stay below 2^62, and so must every time in the simulation
+        if ((__int128)g->dmax * (__int128)pmax >= ((__int128)1 << 62)) {
+            st = fail(DD_ERANGE, "largest duration times largest p reaches 2^62");
+            goto fail_out;
+        }
+        long double bound = (long double)g->dsum * (long double)rmax + (long double)g->gsum;
+        if (bound >= 4.0e18L) {   // 2^62 = 4.61e18, kept a margin for rounding
+            st = fail(DD_ERANGE, "scaled durations could sum past 2^62 ns");
+            goto fail_out;
+        }
+    }
+    TRY(hipStreamSynchronize(s), "sync");
+    free(h_on);
+    dd::dfree(d_scale, s);
+    dd::dfree(err, s);
+    *out = x;
+    return DD_OK;
+fail_out:
+    (void)hipStreamSynchronize(s);
+    free(h_on);
+    dd::dfree(d_scale, s);
+    dd::dfree(err, s);
+    dd::dfree(x->table, s); dd::dfree(x->rm_bits, s); dd::dfree(x->edge_on, s);
+    delete x;
+    return st;
+}
+
+dd_status dd_simulate_batch(const dd_graph *g, const dd_sched *sched, const dd_variants *var,
+                            int64_t *d_finish, int64_t *d_start, int64_t *d_makespan, void *stream) {
+    g_err[0] = 0;
+    if (!g || !sched || !var) return fail(DD_EINVAL, "NULL handle");
+    if (!d_makespan || (!d_finish && g->n > 0))
+        return fail(DD_EINVAL, "d_finish and d_makespan are required");
+    if (sched->graph_id != g->id || var->graph_id != g->id)
+        return fail(DD_EMISMATCH, "handles come from different graphs");
+    const uint64_t missing = var->used_mask & g->cross_mask & ~sched->mask;
+    if (missing)
+        return fail(DD_EMISMATCH, "variants switch on edge classes 0x%llx that the schedule was not built for",
+                    (unsigned long long)missing);
+    int vs = 0;
+    if (const char *e = getenv("DD_VS")) vs = atoi(e);
+    hipError_t e = dd::launch_simulate(g, sched, var, d_finish, d_start, d_makespan, vs,
+                                       (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "simulate launch");
+    return DD_OK;
+}
+
+dd_status dd_sched_task_steps(const dd_sched *sched, int32_t *steps_out, void *stream) {
+    g_err[0] = 0;
+    if (!sched || !steps_out) return fail(DD_EINVAL, "NULL argument");
+    hipStream_t s = (hipStream_t)stream;
+    if (sched->n == 0) return DD_OK;
+    hipError_t e = hipMemcpyAsync(steps_out, sched->node_step, sizeof(int32_t) * (size_t)sched->n,
+                                  hipMemcpyDefault, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "copy steps");
+    return DD_OK;
+}
+
+dd_status dd_sched_info(const dd_sched *sched, int64_t *n_steps, int64_t *n_segments,
+                        int64_t *max_step_width, int64_t *n_gathers) {
+    g_err[0] = 0;
+    if (!sched) return fail(DD_EINVAL, "NULL schedule");
+    if (n_steps) *n_steps = sched->n_steps;
+    if (n_segments) *n_segments = sched->n_segments;
+    if (max_step_width) *max_step_width = sched->max_width;
+    if (n_gathers) *n_gathers = sched->n_gathers;
+    return DD_OK;
+}
+
+void dd_graph_free(dd_graph *g) {
+    if (!g) return;
+    free_graph_arrays(g);
+    delete g;
+}
+
+void dd_sched_free(dd_sched *x) {
+    if (!x) return;
+    free_sched_arrays(x);
+    delete x;
+}
+
+void dd_variants_free(dd_variants *x) {
+    if (!x) return;
+    hipStream_t s = x->stream;
+    dd::dfree(x->table, s);
+    dd::dfree(x->rm_bits, s);
+    dd::dfree(x->edge_on, s);
+    delete x;
+}
+
+}  // extern "C"

@@ -1,0 +1,157 @@
+// Internal declarations shared by the HIP sources of the dd library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dd.h"
+
+namespace dd {
+
+// ---------------------------------------------------------------------------
+// error bits raised by device-side validation (one 32-bit word per check run)
+enum : uint32_t {
+    ERR_THREAD_RANGE = 1u << 0,   // thread id outside [0, n_threads)       EINVAL
+    ERR_PREV_RANGE = 1u << 1,     // thread_prev outside [-1, n) or == self  EINVAL
+    ERR_PREV_THREAD = 1u << 2,    // thread_prev on another thread           ECHAIN
+    ERR_NEG_TIME = 1u << 3,       // negative duration or gap                EINVAL
+    ERR_BIG_TIME = 1u << 4,       // duration or gap >= 2^62                 ERANGE
+    ERR_PTR_ORDER = 1u << 5,      // in_ptr decreasing                       EINVAL
+    ERR_SRC_RANGE = 1u << 6,      // in_src outside [0, n)                   EINVAL
+    ERR_SELF_LOOP = 1u << 7,      // edge u -> u                             ECYCLE
+    ERR_EDGE_CLS = 1u << 8,       // edge class >= 64                        EINVAL
+    ERR_SUCC = 1u << 9,           // two tasks name the same thread_prev     ECHAIN
+    ERR_HEADS = 1u << 10,         // a thread with two first tasks           ECHAIN
+    ERR_CHAIN_CYCLE = 1u << 11,   // thread order loops                      ECHAIN
+    ERR_BACK_EDGE = 1u << 12,     // same-thread dependency points backwards ECYCLE
+    ERR_KAHN_CYCLE = 1u << 13,    // Kahn rounds stall before the end        ECYCLE
+    ERR_SCALE = 1u << 14,         // p < 0 or q < 1                          EINVAL
+};
+
+constexpr int64_t kTimeLimit = int64_t(1) << 62;
+
+// Per-(class, variant) shrink/scale entry: floor(d * p / q) evaluated as
+// a = d * p; q a power of two: a >> shift; otherwise the high 64 bits of
+// a * magic shifted right by `shift` (Granlund & Montgomery, PLDI 1994,
+// round-up method; exact for every a < 2^62).
+struct alignas(16) ScaleEntry {
+    uint64_t magic;   // 0 when q is a power of two
+    uint32_t p;
+    uint32_t shift;
+};
+
+// Statistics reduced on the device while loading (hi/lo split sums cannot
+// overflow for n < 2^31 values below 2^62).
+struct LoadStats {
+    unsigned long long dsum_hi, dsum_lo, gsum_hi, gsum_lo;
+    unsigned long long dmax, cls_max, cross_mask, pad;
+};
+
+}  // namespace dd
+
+struct dd_graph {
+    int32_t n = 0, n_threads = 0;
+    int64_t n_edges = 0, n_cross = 0;
+    int device = 0;
+    hipStream_t stream = nullptr;
+    uint64_t id = 0;
+    // statistics (host)
+    int64_t dmax = 0, gsum = 0;
+    __int128 dsum = 0;
+    int32_t max_cls = 0;
+    uint64_t cross_mask = 0;      // edge classes present among cross-thread edges
+    // device arrays
+    int32_t *thread_prev = nullptr, *thread_id = nullptr;
+    int64_t *dur = nullptr, *gap = nullptr;
+    uint16_t *cls = nullptr;
+    int32_t *rank = nullptr;      // position of each task on its thread
+    int64_t *thread_base = nullptr;  // [T+1]
+    int32_t *order = nullptr;     // [n] tasks thread-major in thread order
+    int64_t *xin_ptr = nullptr;   // [n+1] cross-thread in-edges
+    int32_t *xin_src = nullptr;
+    uint8_t *xin_cls = nullptr;
+};
+
+struct dd_sched {
+    uint64_t graph_id = 0;
+    int32_t n = 0, mode = 0;
+    uint64_t mask = 0;
+    int64_t n_steps = 0, n_segments = 0, max_width = 0, n_gathers = 0;
+    hipStream_t stream = nullptr;
+    int32_t *step_ptr = nullptr;  // [n_steps+1] position offsets
+    int32_t *pos_node = nullptr;  // [n]
+    uint8_t *pos_flags = nullptr; // [n] bit0: first task of a thread run
+    int64_t *pos_dur = nullptr, *pos_gap = nullptr;
+    uint16_t *pos_cls = nullptr;
+    int64_t *gat_ptr = nullptr;   // [n+1] per position
+    int32_t *gat_src = nullptr;   // source task of each gather
+    int32_t *gat_pos = nullptr;   // position it feeds
+    uint8_t *gat_cls = nullptr;   // edge class; 255 = always present (thread order)
+    int64_t *gat_gap = nullptr;   // gap of the source task
+    int32_t *node_step = nullptr; // [n]
+};
+
+struct dd_variants {
+    uint64_t graph_id = 0;
+    int32_t n = 0, V = 0, W = 0, n_cls = 0;
+    uint64_t used_mask = 0;       // OR of edge_on over all variants
+    hipStream_t stream = nullptr;
+    dd::ScaleEntry *table = nullptr;  // [n_cls][V]
+    uint32_t *rm_bits = nullptr;      // [n][W]
+    uint64_t *edge_on = nullptr;      // [V]
+};
+
+namespace dd {
+
+// device memory (stream-ordered pool)
+hipError_t dalloc(void **p, size_t bytes, hipStream_t s);
+void dfree(void *p, hipStream_t s);
+template <class T>
+hipError_t dalloc_n(T **p, size_t count, hipStream_t s) {
+    return dalloc(reinterpret_cast<void **>(p), count * sizeof(T) + 16, s);
+}
+
+// exclusive prefix sum: out[i] = sum_{j<i} in[j] for i in [0, n]; in/out may alias
+hipError_t scan_exclusive(const int64_t *in, int64_t *out, int64_t n, hipStream_t s);
+
+inline int grid_for(int64_t n, int bs) {
+    int64_t g = (n + bs - 1) / bs;
+    if (g < 1) g = 1;
+    if (g > (int64_t(1) << 30)) g = int64_t(1) << 30;
+    return (int)g;
+}
+
+// graph load kernels (k_graph.hip)
+hipError_t launch_validate_nodes(const dd_graph *g, const int64_t *in_ptr, int32_t *succ,
+                                 int32_t *heads, uint32_t *err, LoadStats *st, hipStream_t s);
+hipError_t launch_validate_edges(const dd_graph *g, const int64_t *in_ptr, const int32_t *in_src,
+                                 const uint8_t *edge_cls, uint32_t *err, hipStream_t s);
+hipError_t launch_rank_chains(const dd_graph *g, const int32_t *succ, int32_t *tmp_nxt,
+                              int32_t *tmp_nxt2, int32_t *tmp_rank2, uint32_t *err,
+                              hipStream_t s);
+hipError_t launch_build_order(const dd_graph *g, const int32_t *succ, int64_t *len_tmp,
+                              hipStream_t s);
+hipError_t launch_cross_edges(dd_graph *g, const int64_t *in_ptr, const int32_t *in_src,
+                              const uint8_t *edge_cls, int64_t *cnt_tmp, uint32_t *err,
+                              LoadStats *st, hipStream_t s);
+hipError_t launch_cross_fill(dd_graph *g, const int64_t *in_ptr, const int32_t *in_src,
+                             const uint8_t *edge_cls, hipStream_t s);
+
+// levelization (k_levelize.hip)
+struct LevelizeOut {
+    int64_t n_steps, n_segments, max_width, n_gathers;
+    uint32_t err;
+};
+dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sched *sch,
+                          hipStream_t s, char *msg, size_t msg_len);
+
+// transforms (k_transform.hip)
+hipError_t launch_build_scale_table(const dd_ratio *scale_dev, int32_t n_cls, int32_t V,
+                                    ScaleEntry *table, uint32_t *err, hipStream_t s);
+
+// simulation (k_simulate.hip)
+hipError_t launch_simulate(const dd_graph *g, const dd_sched *sch, const dd_variants *var,
+                           int64_t *finish, int64_t *start, int64_t *makespan, int vs_hint,
+                           hipStream_t s);
+
+}  // namespace dd

@@ -1,0 +1,637 @@
+// Levelization on the GPU: Kahn's algorithm over the task graph (the
+// reference counts and ready frontier of Sec. 3.1, Algorithm 1), taken one
+// whole frontier per round.
+//
+// Phases.  Because tasks on one thread run in their recorded order
+// (Sec. 3.2.2), the graph is a set of thread chains plus cross-thread
+// dependencies.  A round advances the front of every thread past all tasks
+// whose cross-thread parents lie behind the fronts of their own threads at
+// the start of the round; the tasks passed in round r form phase r, one
+// contiguous run ("segment") per thread.  This is Kahn's algorithm where
+// "parent done" is read off the parent thread's front instead of a
+// decremented counter.  Phase = longest path counting 1 per cross-thread
+// edge and 0 per thread-order edge.  A round that advances no thread while
+// tasks remain means a cycle.
+//
+// Levels.  Kahn level = longest path counting 1 per edge.  Inside a
+// segment, level_i = max(level_{i-1} + 1, X_i) with X_i = 1 + the largest
+// level of a cross-thread parent; with the phases known, every segment is a
+// segmented prefix maximum of X_j - j.
+//
+// The schedule handed to the simulation lists tasks by step (phase or
+// level); within a phase step, thread runs are contiguous and in thread
+// order.  Each position carries its "gathers": the cross-thread parents,
+// plus the previous task on the thread for the first task of a run.
+
+#include "dd_common.cuh"
+#include "dd_internal.h"
+
+#include <stdio.h>
+
+namespace dd {
+namespace {
+
+constexpr int kBS = 256;
+constexpr int kWG = 1024;   // the single workgroup running the rounds
+
+struct Req {
+    const int64_t *base;      // [T+1] thread start in order space
+    const int32_t *order;
+    const int32_t *rank;
+    const int32_t *tid;
+    const int64_t *xin_ptr;
+    const int32_t *xin_src;
+    const uint8_t *xin_cls;
+};
+
+__device__ __forceinline__ bool on(uint64_t mask, uint8_t c) { return (mask >> c) & 1ull; }
+
+// per order position: number of active cross-thread parents
+__global__ __launch_bounds__(kBS) void k_req_count(int32_t n, Req r, uint64_t mask,
+                                                   int64_t *__restrict__ cnt,
+                                                   int64_t *__restrict__ flag) {
+    const int64_t p = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (p >= n) return;
+    const int32_t u = r.order[p];
+    int64_t c = 0;
+    for (int64_t k = r.xin_ptr[u]; k < r.xin_ptr[u + 1]; k++) c += on(mask, r.xin_cls[k]);
+    cnt[p] = c;
+    flag[p] = c > 0;
+}
+
+// candidates (positions with a cross-thread parent) and their requirements
+__global__ __launch_bounds__(kBS) void k_req_fill(int32_t n, Req r, uint64_t mask,
+                                                  const int64_t *__restrict__ cidx,
+                                                  const int64_t *__restrict__ rptr_by_pos,
+                                                  int64_t *__restrict__ cand_pos,
+                                                  int64_t *__restrict__ req_ptr,
+                                                  int32_t *__restrict__ req_chain,
+                                                  int64_t *__restrict__ req_gpos) {
+    const int64_t p = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (p >= n) return;
+    if (cidx[p + 1] == cidx[p]) return;
+    const int64_t i = cidx[p];
+    cand_pos[i] = p;
+    int64_t o = rptr_by_pos[p];
+    req_ptr[i] = o;
+    const int32_t u = r.order[p];
+    for (int64_t k = r.xin_ptr[u]; k < r.xin_ptr[u + 1]; k++) {
+        if (!on(mask, r.xin_cls[k])) continue;
+        const int32_t s = r.xin_src[k];
+        const int32_t ts = r.tid[s];
+        req_chain[o] = ts;
+        req_gpos[o] = r.base[ts] + r.rank[s];
+        o++;
+    }
+}
+
+__global__ __launch_bounds__(kBS) void k_cand_base(int32_t T, const int64_t *__restrict__ base,
+                                                   const int64_t *__restrict__ cidx,
+                                                   int64_t *__restrict__ cbase,
+                                                   int64_t *__restrict__ front,
+                                                   int64_t *__restrict__ ci) {
+    const int64_t t = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (t > T) return;
+    cbase[t] = cidx[base[t]];
+    if (t < T) {
+        front[t] = base[t];
+        ci[t] = cidx[base[t]];
+    }
+}
+
+struct KahnArgs {
+    int32_t T;
+    int64_t n;
+    const int64_t *base;      // [T+1]
+    const int64_t *cand_pos;  // [C]
+    const int64_t *cbase;     // [T+1]
+    const int64_t *req_ptr;   // [C+1]
+    const int32_t *req_chain;
+    const int64_t *req_gpos;
+    int64_t *front, *cidx, *nfront, *ncidx;   // [T]
+    int32_t *long_list;       // [T]
+    int64_t *seg_start;       // [n] order position of each segment's first task
+    int64_t *seg_len;         // [n]
+    int32_t *seg_step;        // [n]
+    int64_t *step_seg;        // [n+1] first segment of each step
+    int64_t *result;          // [0] steps, [1] segments
+    uint32_t *err;
+};
+
+__device__ __forceinline__ bool blocked(const KahnArgs &a, int64_t j) {
+    for (int64_t k = a.req_ptr[j]; k < a.req_ptr[j + 1]; k++)
+        if (a.req_gpos[k] >= a.front[a.req_chain[k]]) return true;
+    return false;
+}
+
+__global__ __launch_bounds__(kWG) void k_kahn_rounds(KahnArgs a) {
+    __shared__ int s_nlong;
+    __shared__ int s_unfinished;
+    __shared__ unsigned long long s_first;
+    __shared__ int64_t s_carry_cnt;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    constexpr int NWAVE = kWG / 64;
+    int64_t nseg = 0;
+    int64_t round = 0;
+    for (;;) {
+        if (threadIdx.x == 0) {
+            s_nlong = 0;
+            s_unfinished = 0;
+        }
+        __syncthreads();
+        // A: each wave scans up to two windows of 64 candidates of a thread
+        for (int t = wave; t < a.T; t += NWAVE) {
+            const int64_t f = a.front[t], end = a.base[t + 1];
+            int64_t ci = a.cidx[t];
+            const int64_t ce = a.cbase[t + 1];
+            if (f >= end) {
+                if (lane == 0) { a.nfront[t] = f; a.ncidx[t] = ci; }
+                continue;
+            }
+            if (lane == 0) atomicAdd(&s_unfinished, 1);
+            bool done = false;
+            int64_t cnew = ce;
+            for (int w = 0; w < 2 && !done; w++) {
+                const int64_t j = ci + lane;
+                const bool b = j < ce && blocked(a, j);
+                const unsigned long long bal = __ballot(b);
+                if (bal) {
+                    cnew = ci + __ffsll((long long)bal) - 1;
+                    done = true;
+                } else if (ci + 64 >= ce) {
+                    cnew = ce;
+                    done = true;
+                } else {
+                    ci += 64;
+                }
+            }
+            if (lane == 0) {
+                if (done) {
+                    a.ncidx[t] = cnew;
+                    a.nfront[t] = cnew < ce ? a.cand_pos[cnew] : end;
+                } else {
+                    a.ncidx[t] = ci;
+                    a.long_list[atomicAdd(&s_nlong, 1)] = t;
+                }
+            }
+        }
+        __syncthreads();
+        // B: threads with long ready runs, scanned by the whole workgroup
+        const int nlong = s_nlong;
+        for (int i = 0; i < nlong; i++) {
+            const int t = a.long_list[i];
+            int64_t ci = a.ncidx[t];
+            const int64_t ce = a.cbase[t + 1];
+            int64_t cnew = ce;
+            for (;;) {
+                if (threadIdx.x == 0) s_first = ~0ull;
+                __syncthreads();
+                const int64_t j = ci + threadIdx.x;
+                if (j < ce && blocked(a, j)) atomicMin(&s_first, (unsigned long long)j);
+                __syncthreads();
+                const unsigned long long fb = s_first;
+                __syncthreads();
+                if (fb != ~0ull) { cnew = (int64_t)fb; break; }
+                if (ci + kWG >= ce) { cnew = ce; break; }
+                ci += kWG;
+            }
+            if (threadIdx.x == 0) {
+                a.ncidx[t] = cnew;
+                a.nfront[t] = cnew < ce ? a.cand_pos[cnew] : a.base[t + 1];
+            }
+        }
+        __syncthreads();
+        if (s_unfinished == 0) break;                 // every thread at its end
+        // C: emit one segment per advanced thread (packed count<<32 | length scan)
+        if (threadIdx.x == 0) s_carry_cnt = 0;
+        __syncthreads();
+        for (int base = 0; base < a.T; base += kWG) {
+            const int t = base + threadIdx.x;
+            int64_t len = 0;
+            if (t < a.T) len = a.nfront[t] - a.front[t];
+            const int64_t packed = len > 0 ? ((int64_t(1) << 32) | len) : 0;
+            int64_t tot;
+            const int64_t ex = block_excl_scan<kWG>(packed, &tot);
+            if (len > 0) {
+                const int64_t s = nseg + s_carry_cnt + (ex >> 32);
+                a.seg_start[s] = a.front[t];
+                a.seg_len[s] = len;
+                a.seg_step[s] = (int32_t)round;
+            }
+            __syncthreads();
+            if (threadIdx.x == 0) s_carry_cnt += tot >> 32;
+            __syncthreads();
+        }
+        const int64_t adv = s_carry_cnt;
+        if (adv == 0) {                               // stalled: cycle
+            if (threadIdx.x == 0) atomicOr(a.err, ERR_KAHN_CYCLE);
+            break;
+        }
+        if (threadIdx.x == 0) a.step_seg[round] = nseg;
+        nseg += adv;
+        // D: advance the fronts
+        for (int t = threadIdx.x; t < a.T; t += kWG) {
+            a.front[t] = a.nfront[t];
+            a.cidx[t] = a.ncidx[t];
+        }
+        round++;
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        a.step_seg[round] = nseg;
+        a.result[0] = round;
+        a.result[1] = nseg;
+    }
+}
+
+// positions in step order: segment of each position by binary search
+__global__ __launch_bounds__(kBS) void k_positions(
+    int64_t n, int64_t nseg, const int64_t *__restrict__ seg_off, const int64_t *__restrict__ seg_start,
+    const int32_t *__restrict__ seg_step, const int32_t *__restrict__ order,
+    const int64_t *__restrict__ dur, const int64_t *__restrict__ gap,
+    const uint16_t *__restrict__ cls, int32_t *__restrict__ pos_node,
+    uint8_t *__restrict__ pos_flags, int64_t *__restrict__ pos_dur,
+    int64_t *__restrict__ pos_gap, uint16_t *__restrict__ pos_cls,
+    int32_t *__restrict__ node_step) {
+    const int64_t q = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (q >= n) return;
+    int64_t lo = 0, hi = nseg - 1;          // last segment with seg_off <= q
+    while (lo < hi) {
+        const int64_t mid = (lo + hi + 1) >> 1;
+        if (seg_off[mid] <= q) lo = mid; else hi = mid - 1;
+    }
+    const int64_t p = seg_start[lo] + (q - seg_off[lo]);
+    const int32_t u = order[p];
+    pos_node[q] = u;
+    pos_flags[q] = (q == seg_off[lo]) ? 1 : 0;
+    pos_dur[q] = dur[u];
+    pos_gap[q] = gap[u];
+    pos_cls[q] = cls ? cls[u] : 0;
+    node_step[u] = seg_step[lo];
+}
+
+__global__ __launch_bounds__(kBS) void k_step_ptr(int64_t nsteps, const int64_t *__restrict__ step_seg,
+                                                  const int64_t *__restrict__ seg_off,
+                                                  int32_t *__restrict__ step_ptr) {
+    const int64_t r = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (r <= nsteps) step_ptr[r] = (int32_t)seg_off[step_seg[r]];
+}
+
+// gathers per position: thread predecessor for run heads + active cross parents
+__global__ __launch_bounds__(kBS) void k_gather_count(int64_t n, const int32_t *__restrict__ pos_node,
+                                                      const uint8_t *__restrict__ pos_flags,
+                                                      const int32_t *__restrict__ prev,
+                                                      const int64_t *__restrict__ xin_ptr,
+                                                      const uint8_t *__restrict__ xin_cls,
+                                                      uint64_t mask, int64_t *__restrict__ cnt) {
+    const int64_t q = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (q >= n) return;
+    const int32_t u = pos_node[q];
+    int64_t c = ((pos_flags[q] & 1) && prev[u] >= 0) ? 1 : 0;
+    for (int64_t k = xin_ptr[u]; k < xin_ptr[u + 1]; k++) c += on(mask, xin_cls[k]);
+    cnt[q] = c;
+}
+
+__global__ __launch_bounds__(kBS) void k_gather_fill(
+    int64_t n, const int32_t *__restrict__ pos_node, const uint8_t *__restrict__ pos_flags,
+    const int32_t *__restrict__ prev, const int64_t *__restrict__ xin_ptr,
+    const int32_t *__restrict__ xin_src, const uint8_t *__restrict__ xin_cls, uint64_t mask,
+    const int64_t *__restrict__ gap, const int64_t *__restrict__ gptr,
+    int32_t *__restrict__ gsrc, int32_t *__restrict__ gpos, uint8_t *__restrict__ gcls,
+    int64_t *__restrict__ ggap) {
+    const int64_t q = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (q >= n) return;
+    const int32_t u = pos_node[q];
+    int64_t o = gptr[q];
+    if ((pos_flags[q] & 1) && prev[u] >= 0) {
+        gsrc[o] = prev[u]; gpos[o] = (int32_t)q; gcls[o] = 255; ggap[o] = gap[prev[u]];
+        o++;
+    }
+    for (int64_t k = xin_ptr[u]; k < xin_ptr[u + 1]; k++) {
+        if (!on(mask, xin_cls[k])) continue;
+        const int32_t s = xin_src[k];
+        gsrc[o] = s; gpos[o] = (int32_t)q; gcls[o] = xin_cls[k]; ggap[o] = gap[s];
+        o++;
+    }
+}
+
+__global__ __launch_bounds__(kBS) void k_step_width(int64_t nsteps, const int32_t *__restrict__ step_ptr,
+                                                    unsigned long long *__restrict__ wmax) {
+    const int64_t r = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    int64_t w = r < nsteps ? (int64_t)(step_ptr[r + 1] - step_ptr[r]) : 0;
+    w = wave_max64(w);
+    if ((threadIdx.x & 63) == 0) atomicMax(wmax, (unsigned long long)w);
+}
+
+// Kahn levels from the phase schedule (one workgroup, phases in order)
+struct LevelArgs {
+    int64_t nsteps;
+    const int32_t *step_ptr;
+    const int32_t *pos_node;
+    const uint8_t *pos_flags;
+    const int32_t *prev;
+    const int64_t *xin_ptr;
+    const int32_t *xin_src;
+    const uint8_t *xin_cls;
+    uint64_t mask;
+    int32_t *level;          // [n] by task
+    unsigned long long *max_level;
+};
+
+__global__ __launch_bounds__(kWG) void k_levels(LevelArgs a) {
+    __shared__ int64_t s_val[kWG];
+    __shared__ uint8_t s_head[kWG];
+    __shared__ int64_t s_tmp[kWG];
+    __shared__ uint8_t s_htmp[kWG];
+    __shared__ int64_t s_carry;
+    int64_t lmax = 0;
+    for (int64_t r = 0; r < a.nsteps; r++) {
+        const int64_t p0 = a.step_ptr[r], p1 = a.step_ptr[r + 1];
+        if (threadIdx.x == 0) s_carry = INT64_MIN / 4;
+        __syncthreads();
+        for (int64_t w0 = p0; w0 < p1; w0 += kWG) {
+            const int64_t q = w0 + threadIdx.x;
+            int64_t x = INT64_MIN / 4;
+            uint8_t h = 1;
+            int32_t u = -1;
+            if (q < p1) {
+                u = a.pos_node[q];
+                h = a.pos_flags[q] & 1;
+                int64_t best = 0;
+                if (h && a.prev[u] >= 0) best = (int64_t)a.level[a.prev[u]] + 1;
+                for (int64_t k = a.xin_ptr[u]; k < a.xin_ptr[u + 1]; k++)
+                    if (on(a.mask, a.xin_cls[k])) {
+                        const int64_t l = (int64_t)a.level[a.xin_src[k]] + 1;
+                        best = l > best ? l : best;
+                    }
+                x = best - q;          // level_q - q is a running max inside a run
+            }
+            if (threadIdx.x == 0 && !h) {   // run continues from the previous window
+                x = x > s_carry ? x : s_carry;
+            }
+            s_val[threadIdx.x] = x;
+            s_head[threadIdx.x] = h;
+            __syncthreads();
+            // segmented inclusive max-scan (Hillis-Steele with head flags)
+            for (int d = 1; d < kWG; d <<= 1) {
+                int64_t v = s_val[threadIdx.x];
+                uint8_t hh = s_head[threadIdx.x];
+                if ((int)threadIdx.x >= d && !hh) {
+                    const int64_t o = s_val[threadIdx.x - d];
+                    v = o > v ? o : v;
+                    hh = s_head[threadIdx.x - d];
+                }
+                s_tmp[threadIdx.x] = v;
+                s_htmp[threadIdx.x] = hh;
+                __syncthreads();
+                s_val[threadIdx.x] = s_tmp[threadIdx.x];
+                s_head[threadIdx.x] = s_htmp[threadIdx.x];
+                __syncthreads();
+            }
+            if (q < p1) {
+                const int64_t lv = s_val[threadIdx.x] + q;
+                a.level[u] = (int32_t)lv;
+                lmax = lv > lmax ? lv : lmax;
+            }
+            __syncthreads();
+            if (threadIdx.x == kWG - 1) s_carry = s_val[kWG - 1];
+            __syncthreads();
+        }
+    }
+    lmax = wave_max64(lmax);
+    if ((threadIdx.x & 63) == 0) atomicMax(a.max_level, (unsigned long long)lmax);
+}
+
+__global__ __launch_bounds__(kBS) void k_level_count(int32_t n, const int32_t *__restrict__ level,
+                                                     int64_t *__restrict__ cnt) {
+    const int64_t u = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (u < n) atomicAdd((unsigned long long *)&cnt[level[u]], 1ull);
+}
+
+__global__ __launch_bounds__(kBS) void k_level_scatter(int32_t n, const int32_t *__restrict__ level,
+                                                       int64_t *__restrict__ fill,
+                                                       const int64_t *__restrict__ dur,
+                                                       const int64_t *__restrict__ gap,
+                                                       const uint16_t *__restrict__ cls,
+                                                       int32_t *__restrict__ pos_node,
+                                                       uint8_t *__restrict__ pos_flags,
+                                                       int64_t *__restrict__ pos_dur,
+                                                       int64_t *__restrict__ pos_gap,
+                                                       uint16_t *__restrict__ pos_cls,
+                                                       int32_t *__restrict__ node_step) {
+    const int64_t u = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (u >= n) return;
+    const int32_t l = level[u];
+    const int64_t q = (int64_t)atomicAdd((unsigned long long *)&fill[l], 1ull);
+    pos_node[q] = (int32_t)u;
+    pos_flags[q] = 1;            // every task is its own run: thread predecessor gathered
+    pos_dur[q] = dur[u];
+    pos_gap[q] = gap[u];
+    pos_cls[q] = cls ? cls[u] : 0;
+    node_step[u] = l;
+}
+
+__global__ __launch_bounds__(kBS) void k_i64_to_i32(int64_t n, const int64_t *__restrict__ in,
+                                                    int32_t *__restrict__ out) {
+    const int64_t i = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (i < n) out[i] = (int32_t)in[i];
+}
+
+}  // namespace
+
+#define CK(x)                                                              \
+    do {                                                                   \
+        hipError_t e_ = (x);                                               \
+        if (e_ != hipSuccess) {                                            \
+            snprintf(msg, msg_len, "%s: %s", #x, hipGetErrorString(e_));   \
+            st = e_ == hipErrorOutOfMemory ? DD_ENOMEM : DD_EHIP;          \
+            goto done;                                                     \
+        }                                                                  \
+    } while (0)
+
+dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sched *sch,
+                          hipStream_t s, char *msg, size_t msg_len) {
+    dd_status st = DD_OK;
+    const int64_t n = g->n;
+    const int32_t T = g->n_threads;
+    const int64_t N1 = n + 1;
+    int64_t *cnt = nullptr, *flag = nullptr, *cidx = nullptr, *rptr = nullptr, *cand_pos = nullptr,
+            *req_ptr = nullptr, *req_gpos = nullptr, *cbase = nullptr, *front = nullptr,
+            *ci = nullptr, *nfront = nullptr, *nci = nullptr, *seg_start = nullptr,
+            *seg_len = nullptr, *seg_off = nullptr, *step_seg = nullptr, *result = nullptr,
+            *gcnt = nullptr, *lvl_cnt = nullptr;
+    int32_t *req_chain = nullptr, *long_list = nullptr, *seg_step = nullptr, *level = nullptr;
+    uint32_t *err = nullptr;
+    unsigned long long *wmax = nullptr;
+    int64_t h_res[2] = {0, 0};
+    int64_t h_C = 0, h_R = 0;
+    uint32_t h_err = 0;
+    unsigned long long h_w = 0;
+    Req rq{g->thread_base, g->order, g->rank, g->thread_id, g->xin_ptr, g->xin_src, g->xin_cls};
+    const int gN = grid_for(n, kBS);
+
+    sch->n = (int32_t)n;
+    sch->mode = mode;
+    sch->mask = mask;
+    CK(dalloc_n(&cnt, N1, s));
+    CK(dalloc_n(&flag, N1, s));
+    CK(dalloc_n(&cidx, N1, s));
+    CK(dalloc_n(&rptr, N1, s));
+    CK(dalloc_n(&err, 1, s));
+    CK(dalloc_n(&result, 4, s));
+    CK(dalloc_n(&wmax, 1, s));
+    CK(hipMemsetAsync(err, 0, sizeof(uint32_t), s));
+    CK(hipMemsetAsync(result, 0, 4 * sizeof(int64_t), s));
+    CK(hipMemsetAsync(wmax, 0, sizeof(unsigned long long), s));
+    if (n > 0) {
+        k_req_count<<<gN, kBS, 0, s>>>((int32_t)n, rq, mask, cnt, flag);
+        CK(hipGetLastError());
+    }
+    CK(scan_exclusive(flag, cidx, n, s));
+    CK(scan_exclusive(cnt, rptr, n, s));
+    CK(hipMemcpyAsync(&h_C, cidx + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+    CK(hipMemcpyAsync(&h_R, rptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+    CK(hipStreamSynchronize(s));
+    CK(dalloc_n(&cand_pos, (size_t)h_C + 1, s));
+    CK(dalloc_n(&req_ptr, (size_t)h_C + 1, s));
+    CK(dalloc_n(&req_chain, (size_t)h_R + 1, s));
+    CK(dalloc_n(&req_gpos, (size_t)h_R + 1, s));
+    CK(dalloc_n(&cbase, (size_t)T + 1, s));
+    CK(dalloc_n(&front, (size_t)T, s));
+    CK(dalloc_n(&ci, (size_t)T, s));
+    CK(dalloc_n(&nfront, (size_t)T, s));
+    CK(dalloc_n(&nci, (size_t)T, s));
+    CK(dalloc_n(&long_list, (size_t)T, s));
+    CK(dalloc_n(&seg_start, N1, s));
+    CK(dalloc_n(&seg_len, N1, s));
+    CK(dalloc_n(&seg_step, N1, s));
+    CK(dalloc_n(&seg_off, N1 + 1, s));
+    CK(dalloc_n(&step_seg, N1 + 1, s));
+    if (n > 0) {
+        k_req_fill<<<gN, kBS, 0, s>>>((int32_t)n, rq, mask, cidx, rptr, cand_pos, req_ptr,
+                                      req_chain, req_gpos);
+        CK(hipGetLastError());
+    }
+    CK(hipMemcpyAsync(req_ptr + h_C, &h_R, sizeof(int64_t), hipMemcpyHostToDevice, s));
+    k_cand_base<<<grid_for((int64_t)T + 1, kBS), kBS, 0, s>>>(T, g->thread_base, cidx, cbase,
+                                                               front, ci);
+    CK(hipGetLastError());
+    {
+        KahnArgs ka{T, n, g->thread_base, cand_pos, cbase, req_ptr, req_chain, req_gpos,
+                    front, ci, nfront, nci, long_list, seg_start, seg_len, seg_step, step_seg,
+                    result, err};
+        k_kahn_rounds<<<1, kWG, 0, s>>>(ka);
+        CK(hipGetLastError());
+    }
+    CK(hipMemcpyAsync(h_res, result, 2 * sizeof(int64_t), hipMemcpyDeviceToHost, s));
+    CK(hipMemcpyAsync(&h_err, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
+    CK(hipStreamSynchronize(s));
+    if (h_err & ERR_KAHN_CYCLE) {
+        snprintf(msg, msg_len, "dependencies plus thread order contain a cycle "
+                               "(Kahn rounds stalled after %lld steps)", (long long)h_res[0]);
+        st = DD_ECYCLE;
+        goto done;
+    }
+    {
+        const int64_t nph = h_res[0], nseg = h_res[1];
+        CK(scan_exclusive(seg_len, seg_off, nseg, s));
+        CK(dalloc_n(&sch->pos_node, N1, s));
+        CK(dalloc_n(&sch->pos_flags, N1, s));
+        CK(dalloc_n(&sch->pos_dur, N1, s));
+        CK(dalloc_n(&sch->pos_gap, N1, s));
+        CK(dalloc_n(&sch->pos_cls, N1, s));
+        CK(dalloc_n(&sch->node_step, N1, s));
+        CK(dalloc_n(&sch->gat_ptr, N1, s));
+        if (n > 0) {
+            k_positions<<<gN, kBS, 0, s>>>(n, nseg, seg_off, seg_start, seg_step, g->order, g->dur,
+                                           g->gap, g->cls, sch->pos_node, sch->pos_flags,
+                                           sch->pos_dur, sch->pos_gap, sch->pos_cls,
+                                           sch->node_step);
+            CK(hipGetLastError());
+        }
+        if (mode == DD_PHASES) {
+            sch->n_steps = nph;
+            sch->n_segments = nseg;
+            CK(dalloc_n(&sch->step_ptr, (size_t)nph + 1, s));
+            k_step_ptr<<<grid_for(nph + 1, kBS), kBS, 0, s>>>(nph, step_seg, seg_off, sch->step_ptr);
+            CK(hipGetLastError());
+        } else {
+            // levels from phases, then tasks sorted by level
+            int32_t *tmp_ptr = nullptr;
+            unsigned long long *lmax = nullptr;
+            unsigned long long h_lmax = 0;
+            CK(dalloc_n(&level, N1, s));
+            CK(dalloc_n(&tmp_ptr, (size_t)nph + 1, s));
+            CK(dalloc_n(&lmax, 1, s));
+            CK(hipMemsetAsync(lmax, 0, sizeof(unsigned long long), s));
+            k_step_ptr<<<grid_for(nph + 1, kBS), kBS, 0, s>>>(nph, step_seg, seg_off, tmp_ptr);
+            LevelArgs la{nph, tmp_ptr, sch->pos_node, sch->pos_flags, g->thread_prev, g->xin_ptr,
+                         g->xin_src, g->xin_cls, mask, level, lmax};
+            k_levels<<<1, kWG, 0, s>>>(la);
+            CK(hipGetLastError());
+            CK(hipMemcpyAsync(&h_lmax, lmax, sizeof(h_lmax), hipMemcpyDeviceToHost, s));
+            CK(hipStreamSynchronize(s));
+            dfree(tmp_ptr, s);
+            dfree(lmax, s);
+            const int64_t nl = n > 0 ? (int64_t)h_lmax + 1 : 0;
+            CK(dalloc_n(&lvl_cnt, (size_t)nl + 1, s));
+            CK(hipMemsetAsync(lvl_cnt, 0, sizeof(int64_t) * ((size_t)nl + 1), s));
+            if (n > 0) {
+                k_level_count<<<gN, kBS, 0, s>>>((int32_t)n, level, lvl_cnt);
+                CK(hipGetLastError());
+            }
+            CK(scan_exclusive(lvl_cnt, lvl_cnt, nl, s));
+            CK(dalloc_n(&sch->step_ptr, (size_t)nl + 1, s));
+            k_i64_to_i32<<<grid_for(nl + 1, kBS), kBS, 0, s>>>(nl + 1, lvl_cnt, sch->step_ptr);
+            CK(hipGetLastError());
+            if (n > 0) {
+                k_level_scatter<<<gN, kBS, 0, s>>>((int32_t)n, level, lvl_cnt, g->dur, g->gap,
+                                                   g->cls, sch->pos_node, sch->pos_flags,
+                                                   sch->pos_dur, sch->pos_gap, sch->pos_cls,
+                                                   sch->node_step);
+                CK(hipGetLastError());
+            }
+            sch->n_steps = nl;
+            sch->n_segments = n;
+        }
+        // gathers
+        CK(dalloc_n(&gcnt, N1, s));
+        if (n > 0) {
+            k_gather_count<<<gN, kBS, 0, s>>>(n, sch->pos_node, sch->pos_flags, g->thread_prev,
+                                              g->xin_ptr, g->xin_cls, mask, gcnt);
+            CK(hipGetLastError());
+        }
+        CK(scan_exclusive(gcnt, sch->gat_ptr, n, s));
+        int64_t h_G = 0;
+        CK(hipMemcpyAsync(&h_G, sch->gat_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+        CK(hipStreamSynchronize(s));
+        sch->n_gathers = h_G;
+        CK(dalloc_n(&sch->gat_src, (size_t)h_G + 1, s));
+        CK(dalloc_n(&sch->gat_pos, (size_t)h_G + 1, s));
+        CK(dalloc_n(&sch->gat_cls, (size_t)h_G + 1, s));
+        CK(dalloc_n(&sch->gat_gap, (size_t)h_G + 1, s));
+        if (n > 0) {
+            k_gather_fill<<<gN, kBS, 0, s>>>(n, sch->pos_node, sch->pos_flags, g->thread_prev,
+                                             g->xin_ptr, g->xin_src, g->xin_cls, mask, g->gap,
+                                             sch->gat_ptr, sch->gat_src, sch->gat_pos,
+                                             sch->gat_cls, sch->gat_gap);
+            CK(hipGetLastError());
+        }
+        k_step_width<<<grid_for(sch->n_steps, kBS), kBS, 0, s>>>(sch->n_steps, sch->step_ptr, wmax);
+        CK(hipGetLastError());
+        CK(hipMemcpyAsync(&h_w, wmax, sizeof(h_w), hipMemcpyDeviceToHost, s));
+        CK(hipStreamSynchronize(s));
+        sch->max_width = (int64_t)h_w;
+    }
+done:
+    dfree(cnt, s); dfree(flag, s); dfree(cidx, s); dfree(rptr, s); dfree(err, s);
+    dfree(result, s); dfree(wmax, s); dfree(cand_pos, s); dfree(req_ptr, s);
+    dfree(req_chain, s); dfree(req_gpos, s); dfree(cbase, s); dfree(front, s); dfree(ci, s);
+    dfree(nfront, s); dfree(nci, s); dfree(long_list, s); dfree(seg_start, s);
+    dfree(seg_len, s); dfree(seg_off, s); dfree(seg_step, s); dfree(step_seg, s);
+    dfree(gcnt, s); dfree(lvl_cnt, s); dfree(level, s);
+    return st;
+}
+
+}  // namespace dd

@@ -312,3 +312,48 @@ def test_all_removed_makespan_zero(oracle_mod):
     vs = H.variants(g, removed=[[0, 1, 2]])
     S, F, ms, _ = oracle_mod.run(g, vs)
     assert ms[0] == 0 and (S[0] == 0).all()
+
+
+# levelization ---------------------------------------------------------------
+def _brute_steps(g, mask):
+    par = {}
+    for u in range(g.n):
+        ps = []
+        for e in range(int(g.in_ptr[u]), int(g.in_ptr[u + 1])):
+            if (mask >> int(g.edge_cls[e])) & 1:
+                s = int(g.in_src[e])
+                ps.append((s, 1 if g.thread_id[s] != g.thread_id[u] else 0))
+        if g.thread_prev[u] >= 0:
+            ps.append((int(g.thread_prev[u]), 0))
+        par[u] = ps
+
+    def walk(u):
+        # all paths ending at u: (edges, cross edges)
+        if not par[u]:
+            yield (0, 0)
+        for p, w in par[u]:
+            for a, b in walk(p):
+                yield (a + 1, b + w)
+    lv, ph = [], []
+    for u in range(g.n):
+        paths = list(walk(u))
+        lv.append(max(a for a, _ in paths))
+        ph.append(max(b for _, b in paths))
+    return lv, ph
+
+
+@pytest.mark.parametrize("seed", range(80))
+def test_levels_and_phases_brute_force(oracle_mod, seed):
+    rng = np.random.default_rng(7000 + seed)
+    g = W.random_graph(rng, int(rng.integers(1, 10)), int(rng.integers(1, 4)),
+                       p_edge=float(rng.uniform(0.1, 0.5)), n_edge_cls=2)
+    mask = int(rng.integers(1, 4))
+    lv, ph = oracle_mod.steps(g, mask)
+    blv, bph = _brute_steps(g, mask)
+    assert list(lv) == blv and list(ph) == bph
+
+
+def test_steps_cycle(oracle_mod):
+    g = H.graph(2, [0, 1], [(0, 1), (1, 0)], [1, 1], [0, 0])
+    with pytest.raises(oracle_mod.OracleError):
+        oracle_mod.steps(g)

@@ -1,0 +1,193 @@
+"""Benchmark: batched what-if simulation on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic input
+already resident in HBM: dd_graph_load (validate, rank thread chains,
+cross-thread edge lists) -> dd_levelize (GPU Kahn phases) ->
+dd_apply_transforms (per-variant tables) -> dd_simulate_batch (every
+variant's start/finish, makespan reduced in the same kernel).
+
+Prints one JSON line.  `value` = task-variant updates per second of the
+whole step (N * V per step).  `roofline` covers the simulation kernel:
+algorithmic bytes of one launch over its average duration (HIP events on the
+launching stream).  `cpu_baseline` times the oracle on the host cores on a
+bounded variant sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def algorithmic_bytes(n, V, n_gathers, n_cls, want_start=False):
+    """Bytes one simulate launch must move at minimum:
+    per (task, variant): 8 B finish (+8 B start) + 1/8 B removal bit;
+    per (gather, variant): 8 B source finish + 1/8 B source removal bit;
+    per task: schedule record (node id 4, duration 8, gap 8, class 2, flags 1,
+    gather offset 8 = 31 B); per gather: source 4, position 4, class 1, gap 8
+    = 17 B; per (class, variant): 16 B scale entry."""
+    per_tv = 8.0 + (8.0 if want_start else 0.0) + 1.0 / 8
+    per_gv = 8.0 + 1.0 / 8
+    return (n * V * per_tv + n_gathers * V * per_gv + n * 31.0 + n_gathers * 17.0
+            + n_cls * V * 16.0)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=5)
+    ap.add_argument("--variants", type=int, default=None)
+    ap.add_argument("--cpu-sample", type=int, default=1024,
+                    help="variants the oracle runs for the CPU baseline (0 = skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the path shards over variants with no exchange "
+              "during simulation, and this build runs on a single MI355X only "
+              "(--gpus %d not supported)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2006_03318_amd import batch, binding as B, workloads as W
+
+    assert torch.cuda.is_available(), "bench needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+
+    t0 = time.time()
+    g, vs = W.config(args.config, variants=args.variants)
+    gen_s = time.time() - t0
+    print("[bench] config %d: %d tasks, %d dependency edges, %d threads, %d variants "
+          "(generated in %.1f s)" % (args.config, g.n, g.n_edges, g.n_threads, vs.n_variants,
+                                     gen_s), file=sys.stderr, flush=True)
+    di = batch.to_device(g, vs, device=dev)
+    outs = []
+    for (v0, v1, *_r) in di.batches:
+        Vb = v1 - v0
+        outs.append((torch.empty((g.n, Vb), dtype=torch.int64, device=dev), None,
+                     torch.empty((Vb,), dtype=torch.int64, device=dev)))
+    torch.cuda.synchronize()
+
+    E = lambda: torch.cuda.Event(enable_timing=True)   # noqa: E731
+    rows = {"load": [], "levelize": [], "transforms": [], "simulate": []}
+    info = {}
+
+    def step(record):
+        ev = [E() for _ in range(2 + 3 * len(di.batches))]
+        ev[0].record(stream)
+        gh = batch.load_graph(di, stream)
+        ev[1].record(stream)
+        k = 2
+        hs = []
+        for bi, (v0, v1, mask, scale, rm, eon) in enumerate(di.batches):
+            sch, nsteps = B.dd_levelize(gh, mask, B.DD_PHASES, stream)
+            ev[k].record(stream)
+            var = B.dd_apply_transforms(gh, v1 - v0, di.n_cls, scale, rm, eon, stream)
+            ev[k + 1].record(stream)
+            fin, st, ms = outs[bi]
+            B.dd_simulate_batch(gh, sch, var, fin, st, ms, stream)
+            ev[k + 2].record(stream)
+            if not info:
+                info.update(B.dd_sched_info(sch))
+            hs.append((sch, var))
+            k += 3
+        for sch, var in hs:
+            B.dd_sched_free(sch)
+            B.dd_variants_free(var)
+        B.dd_graph_free(gh)
+        if record:
+            stream.synchronize()
+            rows["load"].append(ev[0].elapsed_time(ev[1]))
+            k = 2
+            prev = ev[1]
+            lv = tr = sm = 0.0
+            for _ in di.batches:
+                lv += prev.elapsed_time(ev[k])
+                tr += ev[k].elapsed_time(ev[k + 1])
+                sm += ev[k + 1].elapsed_time(ev[k + 2])
+                prev = ev[k + 2]
+                k += 3
+            rows["levelize"].append(lv)
+            rows["transforms"].append(tr)
+            rows["simulate"].append(sm)
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(True)
+        print("[bench] step %d/%d done" % (i + 1, args.steps), file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / args.steps
+    NV = g.n * vs.n_variants
+    value = NV / (ms_per_step / 1e3)
+
+    sim_ms = float(np.mean(rows["simulate"]))
+    nbytes = algorithmic_bytes(g.n, vs.n_variants, info.get("n_gathers", 0), di.n_cls)
+    achieved = nbytes / (sim_ms / 1e3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": "k_simulate", "algorithmic_bytes_per_launch": int(nbytes),
+                "avg_launch_ms": round(sim_ms, 4)}
+
+    # parity sample + CPU baseline: the oracle on the first variants
+    cpu = None
+    parity = None
+    if args.cpu_sample > 0:
+        from oracle import oracle as O
+        O.build(force=False)
+        ns = min(args.cpu_sample, vs.n_variants)
+        cores = max(1, min(len(os.sched_getaffinity(0)), 16))
+        t0 = time.perf_counter()
+        _, _, oms, _ = O.run(g, vs, variants=range(ns), want_start=False, want_finish=False,
+                             workers=cores)
+        cpu_s = time.perf_counter() - t0
+        cpu = {"value": round(g.n * ns / cpu_s, 1), "unit": "node-variant updates/s",
+               "cores": cores, "kind": "oracle",
+               "sample": "first %d of %d variants, all %d tasks (%.1f s wall)"
+                         % (ns, vs.n_variants, g.n, cpu_s)}
+        gms = np.concatenate([m.cpu().numpy() for (_, _, m) in outs])[:ns]
+        parity = bool(np.array_equal(gms, oms))
+
+    out = {
+        "metric": "simulated node-variant updates/sec + achieved HBM GB/s (dd_simulate_batch)",
+        "value": round(value, 1),
+        "unit": "node-variant updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic (seeded trace-shaped task graph, random-variant tables)",
+        "config": {"workload": "config %d: %s, %d tasks x %d variants, %d dependency edges, "
+                               "%d threads" % (args.config, g.name, g.n, vs.n_variants,
+                                               g.n_edges, g.n_threads),
+                   "tasks": g.n, "variants": vs.n_variants, "phases": info.get("n_steps"),
+                   "gathers": info.get("n_gathers")},
+        "breakdown_ms": {k: round(float(np.mean(v)), 3) for k, v in rows.items()},
+        "simulate_only_updates_per_s": round(NV / (sim_ms / 1e3), 1),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "parity_sample_makespans_equal": parity,
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

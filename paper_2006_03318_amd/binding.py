@@ -48,6 +48,10 @@ def lib():
     if not os.path.exists(LIB_PATH):
         raise ImportError("libdd.so not built: run __graft_entry__.build() "
                           "(hipcc --offload-arch=gfx950)")
+    try:        # let torch bring up its HIP runtime first so both share one
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     L = ctypes.CDLL(LIB_PATH)
     sig = {
         "dd_graph_load": (_i32, [_i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,

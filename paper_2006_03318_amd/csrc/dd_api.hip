@@ -85,6 +85,7 @@ void free_sched_arrays(dd_sched *x) {
     dd::dfree(x->pos_dur, s); dd::dfree(x->pos_gap, s); dd::dfree(x->pos_cls, s);
     dd::dfree(x->gat_ptr, s); dd::dfree(x->gat_src, s); dd::dfree(x->gat_pos, s);
     dd::dfree(x->gat_cls, s); dd::dfree(x->gat_gap, s); dd::dfree(x->node_step, s);
+    dd::dfree(x->gat_spos, s); dd::dfree(x->rec, s);
 }
 
 }  // namespace

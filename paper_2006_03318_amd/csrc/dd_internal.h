@@ -40,6 +40,20 @@ struct alignas(16) ScaleEntry {
     uint32_t shift;
 };
 
+// One schedule position as the simulation reads it: the task, its
+// duration and gap, and up to two of its gathers inline (source task, the
+// source's schedule position, class and gap).  Gathers beyond two stay in
+// the gather arrays starting at `ovf`.
+struct alignas(16) Rec {
+    int64_t dur, gap, g0_gap, g1_gap;
+    int32_t node, g0_src, g1_src, g0_spos, g1_spos;
+    uint16_t cls;
+    uint8_t g0_cls, g1_cls;
+    uint32_t flags;   // bit0: first task of a thread run; bits 8..31: gathers beyond two
+    int32_t ovf;
+};
+static_assert(sizeof(Rec) == 64, "record size");
+
 // Statistics reduced on the device while loading (hi/lo split sums cannot
 // overflow for n < 2^31 values below 2^62).
 struct LoadStats {
@@ -88,7 +102,9 @@ struct dd_sched {
     int32_t *gat_pos = nullptr;   // position it feeds
     uint8_t *gat_cls = nullptr;   // edge class; 255 = always present (thread order)
     int64_t *gat_gap = nullptr;   // gap of the source task
+    int32_t *gat_spos = nullptr;  // schedule position of the source task
     int32_t *node_step = nullptr; // [n]
+    dd::Rec *rec = nullptr;       // [n] per position
 };
 
 struct dd_variants {

@@ -316,6 +316,45 @@ __global__ __launch_bounds__(kBS) void k_gather_fill(
     }
 }
 
+__global__ __launch_bounds__(kBS) void k_inverse(int64_t n, const int32_t *__restrict__ pos_node,
+                                                 int32_t *__restrict__ pos_of) {
+    const int64_t q = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (q < n) pos_of[pos_node[q]] = (int32_t)q;
+}
+
+__global__ __launch_bounds__(kBS) void k_gather_spos(int64_t G, const int32_t *__restrict__ gsrc,
+                                                     const int32_t *__restrict__ pos_of,
+                                                     int32_t *__restrict__ gspos) {
+    const int64_t e = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (e < G) gspos[e] = pos_of[gsrc[e]];
+}
+
+// the per-position record the simulation streams through LDS
+__global__ __launch_bounds__(kBS) void k_records(
+    int64_t n, const int32_t *__restrict__ pos_node, const uint8_t *__restrict__ pos_flags,
+    const int64_t *__restrict__ pos_dur, const int64_t *__restrict__ pos_gap,
+    const uint16_t *__restrict__ pos_cls, const int64_t *__restrict__ gptr,
+    const int32_t *__restrict__ gsrc, const int32_t *__restrict__ gspos,
+    const uint8_t *__restrict__ gcls, const int64_t *__restrict__ ggap, Rec *__restrict__ rec) {
+    const int64_t q = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (q >= n) return;
+    Rec r;
+    r.dur = pos_dur[q];
+    r.gap = pos_gap[q];
+    r.node = pos_node[q];
+    r.cls = pos_cls[q];
+    const int64_t e0 = gptr[q], e1 = gptr[q + 1];
+    const int64_t ng = e1 - e0;
+    r.g0_src = -1; r.g1_src = -1; r.g0_spos = 0; r.g1_spos = 0;
+    r.g0_gap = 0; r.g1_gap = 0; r.g0_cls = 0; r.g1_cls = 0;
+    if (ng > 0) { r.g0_src = gsrc[e0]; r.g0_spos = gspos[e0]; r.g0_cls = gcls[e0]; r.g0_gap = ggap[e0]; }
+    if (ng > 1) { r.g1_src = gsrc[e0 + 1]; r.g1_spos = gspos[e0 + 1]; r.g1_cls = gcls[e0 + 1]; r.g1_gap = ggap[e0 + 1]; }
+    const int64_t extra = ng > 2 ? ng - 2 : 0;
+    r.flags = (uint32_t)(pos_flags[q] & 1) | ((uint32_t)extra << 8);
+    r.ovf = (int32_t)(e0 + 2);
+    rec[q] = r;
+}
+
 __global__ __launch_bounds__(kBS) void k_step_width(int64_t nsteps, const int32_t *__restrict__ step_ptr,
                                                     unsigned long long *__restrict__ wmax) {
     const int64_t r = (int64_t)blockIdx.x * kBS + threadIdx.x;
@@ -617,6 +656,23 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
                                              sch->gat_ptr, sch->gat_src, sch->gat_pos,
                                              sch->gat_cls, sch->gat_gap);
             CK(hipGetLastError());
+        }
+        {
+            int32_t *pos_of = nullptr;
+            CK(dalloc_n(&pos_of, N1, s));
+            CK(dalloc_n(&sch->gat_spos, (size_t)h_G + 1, s));
+            CK(dalloc_n(&sch->rec, N1, s));
+            if (n > 0) {
+                k_inverse<<<gN, kBS, 0, s>>>(n, sch->pos_node, pos_of);
+                if (h_G > 0)
+                    k_gather_spos<<<grid_for(h_G, kBS), kBS, 0, s>>>(h_G, sch->gat_src, pos_of,
+                                                                    sch->gat_spos);
+                k_records<<<gN, kBS, 0, s>>>(n, sch->pos_node, sch->pos_flags, sch->pos_dur,
+                                             sch->pos_gap, sch->pos_cls, sch->gat_ptr, sch->gat_src,
+                                             sch->gat_spos, sch->gat_cls, sch->gat_gap, sch->rec);
+                CK(hipGetLastError());
+            }
+            dfree(pos_of, s);
         }
         k_step_width<<<grid_for(sch->n_steps, kBS), kBS, 0, s>>>(sch->n_steps, sch->step_ptr, wmax);
         CK(hipGetLastError());

@@ -9,8 +9,8 @@
  * iteration time.  Here thousands of transformed variants of one graph are
  * simulated in one batch on the GPU.
  *
- * Semantics (the simulation of Sec. 3.1, Algorithm 1, "Daydream's Simulation
- * Algorithm"; task fields of Sec. 3.2.1; dependency types of Sec. 3.2.2):
+ * Semantics (the simulation of Sec. 4.1, Algorithm 1, "Daydream's Simulation
+ * Algorithm"; task fields of Sec. 4.2.1; dependency types of Sec. 4.2.2):
  *   every task u has an execution thread (a CPU thread, a GPU stream or a
  *   communication channel), a duration d_u and a gap g_u (CPU time between
  *   the end of u and the next task on its thread), all int64 nanoseconds.
@@ -22,9 +22,9 @@
  *   which is what Algorithm 1 computes: every child's start is raised to the
  *   parent's start + duration + gap, and tasks on one thread run in their
  *   recorded order (that order does not change between executions,
- *   Sec. 3.2.2).
+ *   Sec. 4.2.2).
  *
- * Transformations per variant (Sec. 3.4, graph-transformation primitives):
+ * Transformations per variant (Sec. 4.4, graph-transformation primitives):
  *   shrink/scale: task of class c in variant v gets duration
  *                 floor(d * p / q) with (p, q) = scale[c][v];
  *   Remove:       a removed task gets duration 0 and gap 0, which is the
@@ -90,8 +90,8 @@ typedef struct { int32_t p, q; } dd_ratio;
                          contiguous run of each thread's tasks */
 
 /*
- * dd_graph_load -- the task graph G(V, E) of Sec. 3.2 (tasks, Sec. 3.2.1;
- * dependencies, Sec. 3.2.2).
+ * dd_graph_load -- the task graph G(V, E) of Sec. 4.2 (tasks, Sec. 4.2.1;
+ * dependencies, Sec. 4.2.2).
  *   n            number of tasks.
  *   n_threads    number of execution threads; thread ids are 0..n_threads-1.
  *   in_ptr       int64 [n+1], CSR offsets of dependency in-edges per task;
@@ -131,7 +131,7 @@ dd_status dd_levelize(const dd_graph *g, uint64_t active_edge_classes, int32_t m
                       void *stream, dd_sched **out, int64_t *n_steps_out);
 
 /*
- * dd_apply_transforms -- per-variant transform tables (Sec. 3.4 primitives).
+ * dd_apply_transforms -- per-variant transform tables (Sec. 4.4 primitives).
  *   n_variants   V >= 1.
  *   n_cls        rows of `scale`; must exceed every node_cls of the graph.
  *   scale        dd_ratio [n_cls][V]; NULL = all 1/1.

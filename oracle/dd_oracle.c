@@ -3,23 +3,23 @@
  *
  * A plain, slow CPU reference for the batched what-if simulation.  For each
  * requested variant it
- *   1. applies the graph transformations of Sec. 3.4: the shrink/scale
+ *   1. applies the graph transformations of Sec. 4.4: the shrink/scale
  *      primitive (duration * p / q, floored to whole nanoseconds) and the
  *      Remove primitive; edges whose class is switched off in the variant
  *      are absent;
- *   2. runs the simulation of Sec. 3.1, Algorithm 1, step by step: reference
+ *   2. runs the simulation of Sec. 4.1, Algorithm 1, step by step: reference
  *      counts over every task's parents, a frontier F of ready tasks,
- *      schedule(F) picking the task with the earliest start (Sec. 3.4,
+ *      schedule(F) picking the task with the earliest start (Sec. 4.4,
  *      "Schedule"), per-thread progress P[t], start = max(P[t], start),
  *      P[t] = start + duration + gap, and every child's start raised to the
  *      parent's start + duration + gap.
- * Parents are the dependency edges of Sec. 3.2.2 given in the input plus
+ * Parents are the dependency edges of Sec. 4.2.2 given in the input plus
  * the order of consecutive tasks on one execution thread (also a dependency
- * type of Sec. 3.2.2).
+ * type of Sec. 4.2.2).
  *
  * Removal has two readings, both implemented so tests can check that they
  * agree: mode 0 keeps a removed task with duration and gap 0 (a
- * pass-through); mode 1 unlinks it (Sec. 3.4, Insert/Remove: the task is
+ * pass-through); mode 1 unlinks it (Sec. 4.4, Insert/Remove: the task is
  * taken out of its thread's list, and each of its predecessors is linked to
  * each of its successors).
  *
@@ -467,7 +467,7 @@ int ddo_run(const ddo_graph *g, const ddo_variants *vs,
 /* ------------------------------------------------------------------ */
 /* Topological steps of the graph restricted to the edge classes in `mask`
  * (thread order always present), by Kahn's algorithm (the reference counts
- * and frontier of Sec. 3.1, Algorithm 1, popped first-in first-out):
+ * and frontier of Sec. 4.1, Algorithm 1, popped first-in first-out):
  *   level[u] = longest path to u counted in edges (Kahn level);
  *   phase[u] = longest path to u where a dependency between two different
  *              threads counts 1 and thread order (or a dependency inside

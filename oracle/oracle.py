@@ -1,8 +1,8 @@
 """The oracle: TEST INFRASTRUCTURE ONLY.
 
 ctypes wrapper over dd_oracle.c, a plain CPU implementation of the paper's
-simulation algorithm (Sec. 3.1, Algorithm 1) applied per variant after the
-shrink/scale and Remove transformations (Sec. 3.4).  Only tests/, the smoke
+simulation algorithm (Sec. 4.1, Algorithm 1) applied per variant after the
+shrink/scale and Remove transformations (Sec. 4.4).  Only tests/, the smoke
 check and the benchmark's CPU-baseline leg may import this module.  It
 shares no code with the GPU path.
 """

@@ -1,8 +1,8 @@
 // Graph load: validation, thread-chain ranking, cross-thread edge lists,
 // plus the prefix-sum utility used across the library.
 //
-// The task graph is the one of Sec. 3.2: tasks with an execution thread,
-// duration and gap (Sec. 3.2.1) and the dependency types of Sec. 3.2.2.
+// The task graph is the one of Sec. 4.2: tasks with an execution thread,
+// duration and gap (Sec. 4.2.1) and the dependency types of Sec. 4.2.2.
 // Consecutive tasks on one thread are ordered (a dependency type itself);
 // the chain of each thread is ranked here by pointer jumping so that every
 // later kernel can address "position p on thread t".  A dependency between

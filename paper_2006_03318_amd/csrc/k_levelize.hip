@@ -1,9 +1,9 @@
 // Levelization on the GPU: Kahn's algorithm over the task graph (the
-// reference counts and ready frontier of Sec. 3.1, Algorithm 1), taken one
+// reference counts and ready frontier of Sec. 4.1, Algorithm 1), taken one
 // whole frontier per round.
 //
 // Phases.  Because tasks on one thread run in their recorded order
-// (Sec. 3.2.2), the graph is a set of thread chains plus cross-thread
+// (Sec. 4.2.2), the graph is a set of thread chains plus cross-thread
 // dependencies.  A round advances the front of every thread past all tasks
 // whose cross-thread parents lie behind the fronts of their own threads at
 // the start of the round; the tasks passed in round r form phase r, one

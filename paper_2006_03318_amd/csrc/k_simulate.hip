@@ -1,8 +1,8 @@
 // Batched simulation: every variant of the transformed graph at once (the
 // hot path).
 //
-// What is computed (Sec. 3.1, Algorithm 1, with the transformations of
-// Sec. 3.4 applied per variant): for each task u in topological order and
+// What is computed (Sec. 4.1, Algorithm 1, with the transformations of
+// Sec. 4.4 applied per variant): for each task u in topological order and
 // each variant v,
 //     d' = removed ? 0 : floor(d * p / q),   g' = removed ? 0 : g
 //     start  = max(0, release of every parent present in v)

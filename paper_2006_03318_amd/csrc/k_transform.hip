@@ -1,5 +1,5 @@
-// Per-(class, variant) shrink/scale table (Sec. 3.4, "shrink/scale"
-// primitive; the AMP recipe of Sec. 4.1 divides durations by 3 or 2).
+// Per-(class, variant) shrink/scale table (Sec. 4.4, "shrink/scale"
+// primitive; the AMP recipe of Sec. 5.1 divides durations by 3 or 2).
 //
 // A scaled duration is floor(d * p / q) in integer nanoseconds.  To keep the
 // simulation kernel free of 64-bit division, each (p, q) becomes a

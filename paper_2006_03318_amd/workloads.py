@@ -11,8 +11,8 @@ and the GPU path read the same objects.
 Shapes follow the paper's description of training traces: one or two CPU
 threads issuing every kernel through a launch call, one main compute stream,
 a memcpy stream, an optional auxiliary stream joined through events, and a
-communication channel for gradient all-reduces (Sec. 2 "Key Ideas",
-Sec. 3.2.1 task types, Sec. 3.2.2 dependency types).  Durations follow the
+communication channel for gradient all-reduces (Sec. 3 ("Key Ideas"),
+Sec. 4.2.1 task types, Sec. 4.2.2 dependency types).  Durations follow the
 recipe stated in the design notes: kernels lognormal(median, sigma=1),
 CPU launch calls U[5,15] us, CPU gaps U[0,3] us, device and communication
 gaps 0, all int64 ns.
@@ -158,7 +158,7 @@ class _Builder:
     def launch(self, cpu: int, stream: int, kind: int, layer: int,
                cls_override: int = -1) -> Tuple[int, int]:
         """A CPU launch call followed by the device task it issues
-        (correlation dependency, Sec. 3.2.2)."""
+        (correlation dependency, Sec. 4.2.2)."""
         l = self.task(cpu, K_LAUNCH, layer)
         k = self.task(stream, kind, layer, launch_of=l, cls_override=cls_override)
         self.edge(l, k)
@@ -296,7 +296,7 @@ def _transformer_iteration(n_layers=24, n_wu=554, comm=False, bucket_bytes=25 <<
     n_wu element-wise weight-update kernels.  With comm=True, one all-reduce
     per gradient bucket is issued on its own channel after the last backward
     kernel of its bucket; the first weight-update kernel waits for all of
-    them (Sec. 3.2.1 communication tasks)."""
+    them (Sec. 4.2.1 communication tasks)."""
     b = _Builder(4)
     _, mc = b.launch(CPU, MEMCPY_S, K_MEMCPY, -1)
     ks = []

@@ -1,16 +1,16 @@
 """Pins of the oracle against what the paper and the mathematics fix.
 
-The oracle runs the event-driven simulation of Sec. 3.1 (Algorithm 1).  It
+The oracle runs the event-driven simulation of Sec. 4.1 (Algorithm 1).  It
 is checked here against things that are not the oracle:
   * brute force over every path of tiny random graphs (the start of a task is
     the latest release over all chains of parents; Algorithm 1 adds
     duration + gap along every dependency it follows);
   * closed forms (one thread; a CPU thread launching onto one stream);
-  * the hand-worked rounding table for the shrink/scale primitive (Sec. 3.4);
+  * the hand-worked rounding table for the shrink/scale primitive (Sec. 4.4);
   * invariants (serialization lower bound, monotonicity, 1-Lipschitz);
-  * agreement of two readings of Remove (Sec. 3.4) and of three tie rules of
+  * agreement of two readings of Remove (Sec. 4.4) and of three tie rules of
     schedule(), which the per-thread trace order makes irrelevant
-    (Sec. 3.2.2: the order on a thread does not change between executions).
+    (Sec. 4.2.2: the order on a thread does not change between executions).
 """
 import os
 

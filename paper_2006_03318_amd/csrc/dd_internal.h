@@ -41,18 +41,24 @@ struct alignas(16) ScaleEntry {
 };
 
 // One schedule position as the simulation reads it: the task, its
-// duration and gap, and up to two of its gathers inline (source task, the
-// source's schedule position, class and gap).  Gathers beyond two stay in
-// the gather arrays starting at `ovf`.
+// duration and gap, its thread, and up to two of its gathers inline (source
+// task, the source's schedule position, class; the gap of the first).
+// Gathers beyond two stay in the gather arrays starting at `ovf`.
 struct alignas(16) Rec {
-    int64_t dur, gap, g0_gap, g1_gap;
-    int32_t node, g0_src, g1_src, g0_spos, g1_spos;
+    int64_t dur, gap, g0_gap;
+    int32_t node, g0_src, g1_src, g0_spos, g1_spos, thread;
     uint16_t cls;
     uint8_t g0_cls, g1_cls;
-    uint32_t flags;   // bit0: first task of a thread run; bits 8..31: gathers beyond two
+    uint32_t flags;   // bit0: first task of a thread run; bit1: last task of a run;
+                      // bits 8..31: gathers beyond two
     int32_t ovf;
+    int32_t pad;
 };
 static_assert(sizeof(Rec) == 64, "record size");
+
+// Graphs with at most this many threads keep each thread's latest release in
+// LDS during the simulation instead of gathering the previous task of a run.
+constexpr int kMaxCarryThreads = 64;
 
 // Statistics reduced on the device while loading (hi/lo split sums cannot
 // overflow for n < 2^31 values below 2^62).
@@ -105,6 +111,7 @@ struct dd_sched {
     int32_t *gat_spos = nullptr;  // schedule position of the source task
     int32_t *node_step = nullptr; // [n]
     dd::Rec *rec = nullptr;       // [n] per position
+    bool thread_carry = false;    // thread predecessors come from per-thread carries
 };
 
 struct dd_variants {

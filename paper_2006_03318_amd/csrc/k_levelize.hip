@@ -284,11 +284,12 @@ __global__ __launch_bounds__(kBS) void k_gather_count(int64_t n, const int32_t *
                                                       const int32_t *__restrict__ prev,
                                                       const int64_t *__restrict__ xin_ptr,
                                                       const uint8_t *__restrict__ xin_cls,
-                                                      uint64_t mask, int64_t *__restrict__ cnt) {
+                                                      uint64_t mask, bool with_prev,
+                                                      int64_t *__restrict__ cnt) {
     const int64_t q = (int64_t)blockIdx.x * kBS + threadIdx.x;
     if (q >= n) return;
     const int32_t u = pos_node[q];
-    int64_t c = ((pos_flags[q] & 1) && prev[u] >= 0) ? 1 : 0;
+    int64_t c = (with_prev && (pos_flags[q] & 1) && prev[u] >= 0) ? 1 : 0;
     for (int64_t k = xin_ptr[u]; k < xin_ptr[u + 1]; k++) c += on(mask, xin_cls[k]);
     cnt[q] = c;
 }
@@ -297,14 +298,14 @@ __global__ __launch_bounds__(kBS) void k_gather_fill(
     int64_t n, const int32_t *__restrict__ pos_node, const uint8_t *__restrict__ pos_flags,
     const int32_t *__restrict__ prev, const int64_t *__restrict__ xin_ptr,
     const int32_t *__restrict__ xin_src, const uint8_t *__restrict__ xin_cls, uint64_t mask,
-    const int64_t *__restrict__ gap, const int64_t *__restrict__ gptr,
+    bool with_prev, const int64_t *__restrict__ gap, const int64_t *__restrict__ gptr,
     int32_t *__restrict__ gsrc, int32_t *__restrict__ gpos, uint8_t *__restrict__ gcls,
     int64_t *__restrict__ ggap) {
     const int64_t q = (int64_t)blockIdx.x * kBS + threadIdx.x;
     if (q >= n) return;
     const int32_t u = pos_node[q];
     int64_t o = gptr[q];
-    if ((pos_flags[q] & 1) && prev[u] >= 0) {
+    if (with_prev && (pos_flags[q] & 1) && prev[u] >= 0) {
         gsrc[o] = prev[u]; gpos[o] = (int32_t)q; gcls[o] = 255; ggap[o] = gap[prev[u]];
         o++;
     }
@@ -331,7 +332,8 @@ __global__ __launch_bounds__(kBS) void k_gather_spos(int64_t G, const int32_t *_
 
 // the per-position record the simulation streams through LDS
 __global__ __launch_bounds__(kBS) void k_records(
-    int64_t n, const int32_t *__restrict__ pos_node, const uint8_t *__restrict__ pos_flags,
+    int64_t n, const int32_t *__restrict__ tid, const int32_t *__restrict__ pos_node,
+    const uint8_t *__restrict__ pos_flags,
     const int64_t *__restrict__ pos_dur, const int64_t *__restrict__ pos_gap,
     const uint16_t *__restrict__ pos_cls, const int64_t *__restrict__ gptr,
     const int32_t *__restrict__ gsrc, const int32_t *__restrict__ gspos,
@@ -342,15 +344,19 @@ __global__ __launch_bounds__(kBS) void k_records(
     r.dur = pos_dur[q];
     r.gap = pos_gap[q];
     r.node = pos_node[q];
+    r.thread = tid[r.node];
     r.cls = pos_cls[q];
+    r.pad = 0;
     const int64_t e0 = gptr[q], e1 = gptr[q + 1];
     const int64_t ng = e1 - e0;
     r.g0_src = -1; r.g1_src = -1; r.g0_spos = 0; r.g1_spos = 0;
-    r.g0_gap = 0; r.g1_gap = 0; r.g0_cls = 0; r.g1_cls = 0;
+    r.g0_gap = 0; r.g0_cls = 0; r.g1_cls = 0;
     if (ng > 0) { r.g0_src = gsrc[e0]; r.g0_spos = gspos[e0]; r.g0_cls = gcls[e0]; r.g0_gap = ggap[e0]; }
-    if (ng > 1) { r.g1_src = gsrc[e0 + 1]; r.g1_spos = gspos[e0 + 1]; r.g1_cls = gcls[e0 + 1]; r.g1_gap = ggap[e0 + 1]; }
+    if (ng > 1) { r.g1_src = gsrc[e0 + 1]; r.g1_spos = gspos[e0 + 1]; r.g1_cls = gcls[e0 + 1]; }
     const int64_t extra = ng > 2 ? ng - 2 : 0;
-    r.flags = (uint32_t)(pos_flags[q] & 1) | ((uint32_t)extra << 8);
+    // last task of a run: the next position starts a run (or the schedule ends)
+    const bool last = (q + 1 == n) || (pos_flags[q + 1] & 1);
+    r.flags = (uint32_t)(pos_flags[q] & 1) | (last ? 2u : 0u) | ((uint32_t)extra << 8);
     r.ovf = (int32_t)(e0 + 2);
     rec[q] = r;
 }
@@ -513,6 +519,7 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
     sch->n = (int32_t)n;
     sch->mode = mode;
     sch->mask = mask;
+    sch->thread_carry = T <= kMaxCarryThreads;
     CK(dalloc_n(&cnt, N1, s));
     CK(dalloc_n(&flag, N1, s));
     CK(dalloc_n(&cidx, N1, s));
@@ -638,7 +645,8 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
         CK(dalloc_n(&gcnt, N1, s));
         if (n > 0) {
             k_gather_count<<<gN, kBS, 0, s>>>(n, sch->pos_node, sch->pos_flags, g->thread_prev,
-                                              g->xin_ptr, g->xin_cls, mask, gcnt);
+                                              g->xin_ptr, g->xin_cls, mask, !sch->thread_carry,
+                                              gcnt);
             CK(hipGetLastError());
         }
         CK(scan_exclusive(gcnt, sch->gat_ptr, n, s));
@@ -652,7 +660,8 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
         CK(dalloc_n(&sch->gat_gap, (size_t)h_G + 1, s));
         if (n > 0) {
             k_gather_fill<<<gN, kBS, 0, s>>>(n, sch->pos_node, sch->pos_flags, g->thread_prev,
-                                             g->xin_ptr, g->xin_src, g->xin_cls, mask, g->gap,
+                                             g->xin_ptr, g->xin_src, g->xin_cls, mask,
+                                             !sch->thread_carry, g->gap,
                                              sch->gat_ptr, sch->gat_src, sch->gat_pos,
                                              sch->gat_cls, sch->gat_gap);
             CK(hipGetLastError());
@@ -667,7 +676,7 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
                 if (h_G > 0)
                     k_gather_spos<<<grid_for(h_G, kBS), kBS, 0, s>>>(h_G, sch->gat_src, pos_of,
                                                                     sch->gat_spos);
-                k_records<<<gN, kBS, 0, s>>>(n, sch->pos_node, sch->pos_flags, sch->pos_dur,
+                k_records<<<gN, kBS, 0, s>>>(n, g->thread_id, sch->pos_node, sch->pos_flags, sch->pos_dur,
                                              sch->pos_gap, sch->pos_cls, sch->gat_ptr, sch->gat_src,
                                              sch->gat_spos, sch->gat_cls, sch->gat_gap, sch->rec);
                 CK(hipGetLastError());

@@ -6,6 +6,7 @@ import numpy as np
 import pytest
 
 from oracle import oracle as O
+from paper_2006_03318_amd import batch as BT
 from paper_2006_03318_amd import binding as B
 from paper_2006_03318_amd import workloads as W
 from tests import helpers as H
@@ -81,6 +82,32 @@ def test_every_variant_width(vs_width, monkeypatch):
     g = W.random_graph(rng, 500, 3, p_edge=0.01, n_edge_cls=2, max_dur=1000)
     vs = W.random_variants(rng, g, 19, p_remove=0.3)
     _check(g, vs, B.DD_PHASES, "width%d-random" % vs_width)
+
+
+@pytest.mark.parametrize("vs_width", [1, 2, 4, 8, 16])
+def test_outputs_prefilled_with_sentinel(vs_width, monkeypatch):
+    """Output buffers start full of a huge sentinel: a read of finish before
+    its task is written, or any stale read, shows up as a wrong value.  Odd
+    and even variant counts cover both lane layouts of every width."""
+    import torch
+    require_gpu()
+    monkeypatch.setenv("DD_VS", str(vs_width))
+    sent = 1 << 61
+    for V in (37, 38):
+        g, vs = W.config(1, variants=V)
+        di = BT.to_device(g, vs)
+        outs = [(torch.full((g.n, v1 - v0), sent, dtype=torch.int64, device="cuda"),
+                 torch.full((g.n, v1 - v0), sent, dtype=torch.int64, device="cuda"),
+                 torch.full((v1 - v0,), sent, dtype=torch.int64, device="cuda"))
+                for (v0, v1, *_r) in di.batches]
+        say("parity sentinel width%d V=%d" % (vs_width, V))
+        res = BT.simulate(di, want_start=True, outputs=outs)
+        torch.cuda.synchronize()
+        oS, oF, oM, _ = O.run(g, vs)
+        for v0, v1, f, s_, m in res:
+            assert_equal_arrays("sentinel makespan", m.cpu().numpy(), oM[v0:v1])
+            assert_equal_arrays("sentinel finish", f.cpu().numpy().T, oF[v0:v1])
+            assert_equal_arrays("sentinel start", s_.cpu().numpy().T, oS[v0:v1])
 
 
 def test_empty_graph():

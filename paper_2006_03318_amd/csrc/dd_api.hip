@@ -310,7 +310,12 @@ dd_status dd_apply_transforms(const dd_graph *g, int32_t n_variants, int32_t n_c
     TRY(hipStreamSynchronize(s), "sync");
     TRY(hipMemcpyAsync(x->edge_on, h_on, sizeof(uint64_t) * (size_t)n_variants, hipMemcpyHostToDevice, s), "copy edge_on");
     x->used_mask = 0;
-    for (int32_t v = 0; v < n_variants; v++) x->used_mask |= h_on[v];
+    x->all_mask = ~0ull;
+    for (int32_t v = 0; v < n_variants; v++) {
+        x->used_mask |= h_on[v];
+        x->all_mask &= h_on[v];
+    }
+    x->any_magic = h_err[1] != 0;
     if (h_err[0]) { st = map_err_bits(h_err[0]); goto fail_out; }
     {
         uint64_t pmax, rbits;

@@ -41,20 +41,20 @@ struct alignas(16) ScaleEntry {
 };
 
 // One schedule position as the simulation reads it: the task, its
-// duration and gap, its thread, and up to two of its gathers inline (source
-// task, the source's schedule position, class; the gap of the first).
-// Gathers beyond two stay in the gather arrays starting at `ovf`.
+// duration, gap and class, and up to two of its gathers inline (source task,
+// the source's schedule position, edge class).  Gathers beyond two stay in
+// the gather arrays (gat_ptr[q] + 2 onwards).
 struct alignas(16) Rec {
-    int64_t dur, gap, g0_gap;
-    int32_t node, g0_src, g1_src, g0_spos, g1_spos, thread;
-    uint16_t cls;
-    uint8_t g0_cls, g1_cls;
+    int64_t dur, gap;
+    int32_t node, g0_src, g1_src, g0_spos;
+    int32_t g1_spos;
+    uint32_t cls;     // bits 0..15 task class, 16..23 / 24..31 edge class of gather 0 / 1
     uint32_t flags;   // bit0: first task of a thread run; bit1: last task of a run;
-                      // bits 8..31: gathers beyond two
-    int32_t ovf;
+                      // bits 2..7: thread (graphs with at most 64 threads);
+                      // bits 8..31: gathers beyond two (saturating)
     int32_t pad;
 };
-static_assert(sizeof(Rec) == 64, "record size");
+static_assert(sizeof(Rec) == 48, "record size");
 
 // Graphs with at most this many threads keep each thread's latest release in
 // LDS during the simulation instead of gathering the previous task of a run.
@@ -118,6 +118,8 @@ struct dd_variants {
     uint64_t graph_id = 0;
     int32_t n = 0, V = 0, W = 0, n_cls = 0;
     uint64_t used_mask = 0;       // OR of edge_on over all variants
+    uint64_t all_mask = 0;        // AND of edge_on over all variants
+    bool any_magic = false;       // some scale has q not a power of two
     hipStream_t stream = nullptr;
     dd::ScaleEntry *table = nullptr;  // [n_cls][V]
     uint32_t *rm_bits = nullptr;      // [n][W]

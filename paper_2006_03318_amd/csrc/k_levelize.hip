@@ -337,27 +337,28 @@ __global__ __launch_bounds__(kBS) void k_records(
     const int64_t *__restrict__ pos_dur, const int64_t *__restrict__ pos_gap,
     const uint16_t *__restrict__ pos_cls, const int64_t *__restrict__ gptr,
     const int32_t *__restrict__ gsrc, const int32_t *__restrict__ gspos,
-    const uint8_t *__restrict__ gcls, const int64_t *__restrict__ ggap, Rec *__restrict__ rec) {
+    const uint8_t *__restrict__ gcls, Rec *__restrict__ rec) {
     const int64_t q = (int64_t)blockIdx.x * kBS + threadIdx.x;
     if (q >= n) return;
     Rec r;
     r.dur = pos_dur[q];
     r.gap = pos_gap[q];
     r.node = pos_node[q];
-    r.thread = tid[r.node];
-    r.cls = pos_cls[q];
-    r.pad = 0;
+    const int32_t t = tid[r.node];
     const int64_t e0 = gptr[q], e1 = gptr[q + 1];
     const int64_t ng = e1 - e0;
+    uint32_t c0 = 0, c1 = 0;
     r.g0_src = -1; r.g1_src = -1; r.g0_spos = 0; r.g1_spos = 0;
-    r.g0_gap = 0; r.g0_cls = 0; r.g1_cls = 0;
-    if (ng > 0) { r.g0_src = gsrc[e0]; r.g0_spos = gspos[e0]; r.g0_cls = gcls[e0]; r.g0_gap = ggap[e0]; }
-    if (ng > 1) { r.g1_src = gsrc[e0 + 1]; r.g1_spos = gspos[e0 + 1]; r.g1_cls = gcls[e0 + 1]; }
-    const int64_t extra = ng > 2 ? ng - 2 : 0;
+    if (ng > 0) { r.g0_src = gsrc[e0]; r.g0_spos = gspos[e0]; c0 = gcls[e0]; }
+    if (ng > 1) { r.g1_src = gsrc[e0 + 1]; r.g1_spos = gspos[e0 + 1]; c1 = gcls[e0 + 1]; }
+    r.cls = (uint32_t)pos_cls[q] | (c0 << 16) | (c1 << 24);
+    int64_t extra = ng > 2 ? ng - 2 : 0;   // count saturates; the gather pointers are exact
+    if (extra > 0xFFFFFF) extra = 0xFFFFFF;
     // last task of a run: the next position starts a run (or the schedule ends)
     const bool last = (q + 1 == n) || (pos_flags[q + 1] & 1);
-    r.flags = (uint32_t)(pos_flags[q] & 1) | (last ? 2u : 0u) | ((uint32_t)extra << 8);
-    r.ovf = (int32_t)(e0 + 2);
+    r.flags = (uint32_t)(pos_flags[q] & 1) | (last ? 2u : 0u) |
+              ((uint32_t)(t < kMaxCarryThreads ? t : 0) << 2) | ((uint32_t)extra << 8);
+    r.pad = 0;
     rec[q] = r;
 }
 
@@ -678,7 +679,7 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
                                                                     sch->gat_spos);
                 k_records<<<gN, kBS, 0, s>>>(n, g->thread_id, sch->pos_node, sch->pos_flags, sch->pos_dur,
                                              sch->pos_gap, sch->pos_cls, sch->gat_ptr, sch->gat_src,
-                                             sch->gat_spos, sch->gat_cls, sch->gat_gap, sch->rec);
+                                             sch->gat_spos, sch->gat_cls, sch->rec);
                 CK(hipGetLastError());
             }
             dfree(pos_of, s);

@@ -52,6 +52,7 @@ __device__ __forceinline__ int64_t scaled(int64_t d, const ScaleEntry &se) {
 __device__ __forceinline__ int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
 
 struct PipeArgs {
+    const int64_t *gat_ptr;       // [n+1] gathers of each position
     const int32_t *gat_src;       // gathers beyond two per position
     const int32_t *gat_spos;
     const uint8_t *gat_cls;
@@ -84,12 +85,17 @@ __device__ __forceinline__ void store_vals(gi64 *o, const Vals<2> &v) {
     *(gi64x2 *)o = t;
 }
 
+// per-lane values indexed by variant: vector types stay in registers where
+// a conditional read of an array element could turn into a pointer select
+template <int N> struct I64V { typedef long long T __attribute__((ext_vector_type(N))); };
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
 template <int K, int VPL>
 struct Dyn {                      // per-lane loads for the next round
     uint32_t rmw[K];              // removal word of the task
     Vals<VPL> f0[K], f1[K];       // finish of old gather sources
     uint32_t r0w[K], r1w[K];      // removal words of those sources
-    int64_t g1gap[K];             // gap of the second source
+    int64_t g0gap[K], g1gap[K];   // gaps of those sources
 };
 
 __device__ __forceinline__ bool cls_on(uint64_t eon, uint8_t c) {
@@ -141,8 +147,13 @@ __device__ __forceinline__ void wave_scan(int64_t &a, int64_t &b, int &h) {
 // Idle lanes keep issuing the same prefetch loads (clamped addresses) and
 // stores (to a dummy target), so the count of memory operations in flight
 // is the same on every path and the wait for the next round's data never
-// includes this round's stores.
-template <int LPS, int VPL, int K, bool TLDS, bool START>
+// includes this round's stores.  Waves whose slots all lie past the end of
+// a round skip the arithmetic (rounds at the end of a phase are ragged).
+//
+// UNI: every variant of the launch enables every edge class that the
+// schedule's gathers use, every scale is a power of two and every duration
+// is below 2^32 (one 32x32 multiply and a shift per scaled duration).
+template <int LPS, int VPL, int K, bool TLDS, bool START, bool UNI>
 __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ round_r0,
                                                   const int32_t *__restrict__ round_rn,
                                                   const int64_t *__restrict__ n_rounds,
@@ -151,9 +162,15 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
     constexpr int NS = kNT / LPS;
     constexpr int RP = NS * K;
     constexpr int NE = NS * VS;           // slot summaries (= kNT * VPL)
-    static_assert(RP <= kNT, "one record per thread and round");
+    constexpr int RW = RP * 3;            // 16-byte words of one ring buffer
+    constexpr int PF = (RW + kNT - 1) / kNT;
+    static_assert(sizeof(Rec) == 48, "record layout");
+    static_assert(RP <= kNT, "positions per round");
+    static_assert(PF <= 3, "record prefetch words per lane");
     static_assert(NE / 64 <= 16, "chunk totals");
-    __shared__ Rec sRec[2][RP];
+    static_assert(!UNI || TLDS, "uniform path keeps the table in LDS");
+    // records of rounds k, k+1 (read) and k+2 (being filled): a ring of three
+    __shared__ uint4 sRec[3][RW];
     __shared__ int64_t sR[RP * VS];
     __shared__ int64_t sA[NE], sB[NE];
     __shared__ uint8_t sH[NE];
@@ -188,6 +205,10 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
     const bool tcar = a.thread_carry != 0;
 
     if (tid == 0) sFlags = 0;
+    {   // the record ring starts zeroed (no stale fields past a round's end)
+        uint4 *z = &sRec[0][0];
+        for (int i = tid; i < 3 * RW; i += kNT) z[i] = make_uint4(0u, 0u, 0u, 0u);
+    }
     __syncthreads();
     bool any_magic = false;
     if (TLDS) {
@@ -201,10 +222,6 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         }
     }
     for (int i = tid; i < kMaxCarryThreads * VS; i += kNT) sTC[i] = 0;
-    {   // the record ring starts zeroed (no stale fields past a round's end)
-        uint4 *z = reinterpret_cast<uint4 *>(&sRec[0][0]);
-        for (int i = tid; i < 2 * RP * 4; i += kNT) z[i] = make_uint4(0u, 0u, 0u, 0u);
-    }
     if (tid < VS) {
         sMs[tid] = 0;
         // per-variant values read inside the loop live in LDS: a register
@@ -212,11 +229,11 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         sEon[tid] = a.edge_on[v0 + tid < a.V ? v0 + tid : 0];
     }
     if (any_magic) atomicOr(&sFlags, 1);
-    __syncthreads();
     for (int rr = 0; rr < 2; rr++) {          // prologue: records of rounds 0 and 1
         if (rr < nr) {
             const int r0 = round_r0[rr], rn = round_rn[rr];
-            for (int i = tid; i < rn; i += kNT) sRec[rr][i] = rec[r0 + i];
+            const uint4 *src = reinterpret_cast<const uint4 *>(rec + r0);
+            for (int i = tid; i < rn * 3; i += kNT) sRec[rr][i] = src[i];
         }
     }
     __syncthreads();
@@ -225,29 +242,30 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
     uint64_t eall = ~0ull;
 #pragma unroll
     for (int o = 0; o < VS; o++) eall &= sEon[o];
-    const bool all_on = (eall & a.cls_mask) == a.cls_mask;
-    const bool shift_only = TLDS && !(sFlags & 1);
+    const bool all_on = UNI || (eall & a.cls_mask) == a.cls_mask;
+    const bool shift_only = UNI || (TLDS && !(sFlags & 1));
 
-    // loads of round kk (records in sRec[kk & 1]); a gather is old when its
-    // source position precedes prev_r0 (its round finished two rounds ago)
-    auto issue = [&](int64_t kk, int prev_r0, Dyn<K, VPL> &d) {
+    // loads of round kk (records in ring buffer b); a gather is old when its
+    // source position precedes prev_r0 (its round has ended before round kk-1)
+    auto issue = [&](int64_t kk, int b, int prev_r0, Dyn<K, VPL> &d) {
         const int rn = round_rn[kk];
-        const Rec *R = sRec[kk & 1];
+        const Rec *R = reinterpret_cast<const Rec *>(sRec[b]);
 #pragma unroll
         for (int i = 0; i < K; i++) {
             const int q = slot * K + i;
             const bool ok = q < rn;
             const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
-            const int4 w1 = r4[1];   // g0_gap (2 words), node, g0_src
-            const int4 w2 = r4[2];   // g1_src, g0_spos, g1_spos, thread
-            const int32_t node = ok ? w1.z : 0;
-            const bool n0 = ok && w1.w >= 0 && w2.y < prev_r0;
-            const bool n1 = ok && w2.x >= 0 && w2.z < prev_r0;
-            const int64_t a0 = n0 ? w1.w : 0, a1 = n1 ? w2.x : 0;
+            const int4 w1 = r4[1];   // node, g0_src, g1_src, g0_spos
+            const int p1 = r4[2].x;  // g1_spos
+            const int32_t node = ok ? w1.x : 0;
+            const bool n0 = ok && w1.y >= 0 && w1.w < prev_r0;
+            const bool n1 = ok && w1.z >= 0 && p1 < prev_r0;
+            const int64_t a0 = n0 ? w1.y : 0, a1 = n1 ? w1.z : 0;
             d.rmw[i] = a.rm[(int64_t)node * W + vw];
             if (__any(n0)) {
                 d.f0[i] = *reinterpret_cast<const Vals<VPL> *>(a.finish + a0 * V + vvf);
                 d.r0w[i] = a.rm[a0 * W + vw];
+                d.g0gap[i] = a.gap[a0];
             }
             if (__any(n1)) {
                 d.f1[i] = *reinterpret_cast<const Vals<VPL> *>(a.finish + a1 * V + vvf);
@@ -257,15 +275,14 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         }
     };
     Dyn<K, VPL> D;
-    if (nr > 0) issue(0, 0, D);
+    if (nr > 0) issue(0, 0, 0, D);
 
-    int64_t carry[VPL], ms[VPL];
-#pragma unroll
-    for (int j = 0; j < VPL; j++) { carry[j] = 0; ms[j] = 0; }
+    typename I64V<VPL>::T carry = 0, ms = 0;
     int prev_r0 = 0;
+    int b0 = 0, b1 = 1, b2 = 2;               // ring buffers of rounds k, k+1, k+2
     for (int64_t k = 0; k < nr; k++) {
         const int r0 = round_r0[k], rn = round_rn[k];
-        const Rec *R = sRec[k & 1];
+        const Rec *R = reinterpret_cast<const Rec *>(sRec[b0]);
         uint64_t eon[VPL];
 #pragma unroll
         for (int j = 0; j < VPL; j++) eon[j] = sEon[o0 + j];
@@ -273,14 +290,17 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         // whole round to arrive (records of k+1 are in LDS since round k-1)
         Dyn<K, VPL> DN;
         const int64_t k1 = k + 1 < nr ? k + 1 : k;
-        issue(k1, r0, DN);
+        issue(k1, k + 1 < nr ? b1 : b0, r0, DN);
         // records of round k+2: global -> registers now, -> LDS at the round's end
         const int64_t k2 = k + 2 < nr ? k + 2 : k;
-        const int r0b = round_r0[k2];
-        const int nxt_rn = k + 2 < nr ? round_rn[k2] : 0;
-        const uint4 *nsrc = reinterpret_cast<const uint4 *>(rec + r0b + (tid < nxt_rn ? tid : 0));
-        const uint4 nx0 = nsrc[0], nx1 = nsrc[1], nx2 = nsrc[2], nx3 = nsrc[3];
+        const int nxt_w = k + 2 < nr ? round_rn[k2] * 3 : 0;
+        const u32x4 *nsrc = reinterpret_cast<const u32x4 *>(rec + round_r0[k2]);
+        u32x4 nx0, nx1, nx2;
+        nx0 = nsrc[tid < nxt_w ? tid : 0];
+        if (PF > 1) nx1 = nsrc[tid + kNT < nxt_w ? tid + kNT : 0];
+        if (PF > 2) nx2 = nsrc[tid + 2 * kNT < nxt_w ? tid + 2 * kNT : 0];
 
+        const bool wact = __any(slot * K < rn);  // some position of this wave is live
         // walk: local max-plus recurrence over this slot's K positions
         int64_t Fl[K][VPL], Dp[K][VPL], Dd[K][VPL];
         int32_t U[K];
@@ -291,103 +311,106 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
 #pragma unroll
         for (int j = 0; j < VPL; j++) rmk[j] = 0;
         bool hh = false;
+        if (wact) {
 #pragma unroll
-        for (int i = 0; i < K; i++) {
-            const int q = slot * K + i;
-            const bool ok = q < rn;
-            const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
-            const int4 w0 = r4[0], w1 = r4[1], w2 = r4[2], w3 = r4[3];
-            const int64_t dur = ((int64_t)(uint32_t)w0.y << 32) | (uint32_t)w0.x;
-            const int64_t gap = ((int64_t)(uint32_t)w0.w << 32) | (uint32_t)w0.z;
-            const int64_t g0gap = ((int64_t)(uint32_t)w1.y << 32) | (uint32_t)w1.x;
-            const int32_t node = w1.z, s0 = w1.w, s1 = w2.x, p0 = w2.y, p1 = w2.z;
-            // positions past the round's end hold stale or unwritten LDS:
-            // nothing read from them may form an address
-            const int32_t thr = ok ? w2.w : 0;
-            const uint32_t cl = (uint32_t)w3.x;
-            const int cls = ok ? (int)(cl & 0xffff) : 0;
-            const uint8_t c0 = (cl >> 16) & 0xff, c1 = cl >> 24;
-            const uint32_t flags = (uint32_t)w3.y;
-            const int32_t ovf = w3.z;
-            const bool head = ok && (flags & 1u);
-            U[i] = node;
-            const bool old0 = p0 < prev_r0, old1 = p1 < prev_r0;
-            int i0 = p0 - prev_r0, i1 = p1 - prev_r0;
-            i0 = i0 < 0 ? 0 : (i0 >= RP ? RP - 1 : i0);
-            i1 = i1 < 0 ? 0 : (i1 >= RP ? RP - 1 : i1);
-            const bool has1 = ok && s1 >= 0;
-            const bool any1 = __any(has1);
-            const uint32_t extra = ok ? (flags >> 8) : 0u;
-            const int tcx = (tcar && (uint32_t)thr < (uint32_t)kMaxCarryThreads) ? thr * VS : 0;
+            for (int i = 0; i < K; i++) {
+                const int q = slot * K + i;
+                const bool ok = q < rn;
+                const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
+                const int4 w0 = r4[0], w1 = r4[1], w2 = r4[2];
+                const int64_t dur = ((int64_t)(uint32_t)w0.y << 32) | (uint32_t)w0.x;
+                const int64_t gap = ((int64_t)(uint32_t)w0.w << 32) | (uint32_t)w0.z;
+                const int32_t node = w1.x, s0 = w1.y, s1 = w1.z, p0 = w1.w, p1 = w2.x;
+                // positions past the round's end hold stale LDS: nothing read
+                // from them may form an address
+                const uint32_t cl = (uint32_t)w2.y;
+                const int cls = ok ? (int)(cl & 0xffff) : 0;
+                const uint8_t c0 = (cl >> 16) & 0xff, c1 = cl >> 24;
+                const uint32_t flags = ok ? (uint32_t)w2.z : 0u;
+                const bool head = flags & 1u;
+                U[i] = node;
+                const bool old0 = p0 < prev_r0, old1 = p1 < prev_r0;
+                int i0 = p0 - prev_r0, i1 = p1 - prev_r0;
+                i0 = i0 < 0 ? 0 : (i0 >= RP ? RP - 1 : i0);
+                i1 = i1 < 0 ? 0 : (i1 >= RP ? RP - 1 : i1);
+                const bool has0 = ok && s0 >= 0;
+                const bool has1 = ok && s1 >= 0;
+                const bool any1 = __any(has1);
+                const uint32_t extra = flags >> 8;
+                const int tcx = ((flags >> 2) & 63u) * VS + o0;
 #pragma unroll
-            for (int j = 0; j < VPL; j++) {
-                const uint32_t bit = vsh + j;
-                const bool rmv = (D.rmw[i] >> bit) & 1u;
-                int64_t X = 0;
-                {
-                    const int64_t ro = D.f0[i].x[j] + (((D.r0w[i] >> bit) & 1u) ? 0 : g0gap);
-                    const int64_t rn0 = sR[i0 * VS + o0 + j];
-                    const int64_t rel = old0 ? ro : rn0;
-                    const bool on = ok && s0 >= 0 && (all_on || cls_on(eon[j], c0));
-                    X = on ? max64(X, rel) : X;
-                }
-                if (any1) {
-                    const int64_t ro = D.f1[i].x[j] + (((D.r1w[i] >> bit) & 1u) ? 0 : D.g1gap[i]);
-                    const int64_t rn1 = sR[i1 * VS + o0 + j];
-                    const int64_t rel = old1 ? ro : rn1;
-                    const bool on = has1 && (all_on || cls_on(eon[j], c1));
-                    X = on ? max64(X, rel) : X;
-                }
-                if (tcar) {                                    // previous task of the thread
-                    const int64_t tc = sTC[tcx + o0 + j];
-                    X = head ? max64(X, tc) : X;
-                }
-                if (extra) {                                   // rare: wide fan-in
-                    for (uint32_t e2 = 0; e2 < extra; e2++) {
-                        const int64_t e = (int64_t)ovf + e2;
-                        const uint8_t c = a.gat_cls[e];
-                        if (!cls_on(eon[j], c)) continue;
-                        const int32_t sp = a.gat_spos[e];
-                        int64_t rel;
-                        if (sp < prev_r0) {
-                            const int64_t sx = a.gat_src[e];
-                            const bool rs = (a.rm[sx * W + vw] >> bit) & 1u;
-                            rel = a.finish[sx * V + vvf + j] + (rs ? 0 : a.gat_gap[e]);
-                        } else {
-                            rel = sR[(sp - prev_r0) * VS + o0 + j];
+                for (int j = 0; j < VPL; j++) {
+                    const uint32_t bit = vsh + j;
+                    const bool rmv = (D.rmw[i] >> bit) & 1u;
+                    int64_t X;
+                    {
+                        const int64_t ro = D.f0[i].x[j] + (((D.r0w[i] >> bit) & 1u) ? 0 : D.g0gap[i]);
+                        const int64_t rn0 = sR[i0 * VS + o0 + j];
+                        const int64_t rel = old0 ? ro : rn0;
+                        const bool on = has0 && (all_on || cls_on(eon[j], c0));
+                        X = on ? rel : 0;
+                    }
+                    if (any1) {
+                        const int64_t ro = D.f1[i].x[j] + (((D.r1w[i] >> bit) & 1u) ? 0 : D.g1gap[i]);
+                        const int64_t rn1 = sR[i1 * VS + o0 + j];
+                        const int64_t rel = old1 ? ro : rn1;
+                        const bool on = has1 && (all_on || cls_on(eon[j], c1));
+                        X = on ? max64(X, rel) : X;
+                    }
+                    if (tcar) {                                // previous task of the thread
+                        const int64_t tc = sTC[tcx + j];
+                        X = head ? max64(X, tc) : X;
+                    }
+                    if (extra) {                               // rare: wide fan-in
+                        const int64_t e1 = a.gat_ptr[r0 + q + 1];
+                        for (int64_t e = a.gat_ptr[r0 + q] + 2; e < e1; e++) {
+                            const uint8_t c = a.gat_cls[e];
+                            if (!cls_on(eon[j], c)) continue;
+                            const int32_t sp = a.gat_spos[e];
+                            int64_t rel;
+                            if (sp < prev_r0) {
+                                const int64_t sx = a.gat_src[e];
+                                const bool rs = (a.rm[sx * W + vw] >> bit) & 1u;
+                                rel = a.finish[sx * V + vvf + j] + (rs ? 0 : a.gat_gap[e]);
+                            } else {
+                                rel = sR[(sp - prev_r0) * VS + o0 + j];
+                            }
+                            X = max64(X, rel);
                         }
-                        X = max64(X, rel);
                     }
-                }
-                const bool live = ok && !rmv;
-                int64_t dp;
-                if (TLDS) {
-                    const uint64_t te = sT[cls * VS + o0 + j];
-                    if (shift_only) {
-                        dp = (int64_t)(((uint64_t)dur * (uint32_t)te) >> ((uint32_t)(te >> 32) & 0xff));
+                    const bool live = ok && !rmv;
+                    int64_t dp;
+                    if (UNI) {
+                        const uint64_t te = sT[cls * VS + o0 + j];
+                        dp = (int64_t)(((uint64_t)(uint32_t)dur * (uint32_t)te) >> ((uint32_t)(te >> 32) & 0xff));
+                    } else if (TLDS) {
+                        const uint64_t te = sT[cls * VS + o0 + j];
+                        if (shift_only) {
+                            dp = (int64_t)(((uint64_t)dur * (uint32_t)te) >> ((uint32_t)(te >> 32) & 0xff));
+                        } else {
+                            dp = scaled8(dur, te, a.table, (int64_t)cls * V + vvf + j);
+                        }
                     } else {
-                        dp = scaled8(dur, te, a.table, (int64_t)cls * V + vvf + j);
+                        dp = scaled(dur, a.table[(int64_t)cls * V + vvf + j]);
                     }
-                } else {
-                    dp = scaled(dur, a.table[(int64_t)cls * V + vvf + j]);
+                    dp = live ? dp : 0;
+                    const int64_t gp = live ? gap : 0;
+                    A[j] = head ? 0 : A[j];
+                    B[j] = head ? 0 : B[j];
+                    const int64_t F = max64(B[j], X) + dp;
+                    Dp[i][j] = A[j] + dp;
+                    A[j] += dp + gp;
+                    B[j] = F + gp;
+                    Fl[i][j] = F;
+                    if (START) Dd[i][j] = dp;
+                    if (rmv) rmk[j] |= 1u << i;
                 }
-                dp = live ? dp : 0;
-                const int64_t gp = live ? gap : 0;
-                A[j] = head ? 0 : A[j];
-                B[j] = head ? 0 : B[j];
-                const int64_t S = max64(B[j], X);
-                const int64_t F = S + dp;
-                Dp[i][j] = A[j] + dp;
-                A[j] += dp + gp;
-                B[j] = F + gp;
-                Fl[i][j] = F;
-                Dd[i][j] = dp;
-                if (rmv) rmk[j] |= 1u << i;
+                hh = hh || head;
+                if (!hh) before |= 1u << i;
             }
-            hh = hh || head;
-            if (!hh) before |= 1u << i;
         }
-        // slot summaries (variant-major); slot 0 absorbs the carry
+        // slot summaries (variant-major); slot 0 absorbs the carry; slots of
+        // idle waves are the identity (0, 0)
 #pragma unroll
         for (int j = 0; j < VPL; j++) {
             const int e = (o0 + j) * NS + slot;
@@ -398,14 +421,21 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         }
         __syncthreads();                                     // B1
         // inclusive scan of slot summaries per variant: DPP within the wave,
-        // then earlier 64-slot chunks of the same variant
+        // then earlier 64-slot chunks of the same variant; chunks whose
+        // slots all lie past the round's end are skipped
+        const int ls = (rn - 1) / K;                         // last live slot
         int64_t xa[VPL], xb[VPL];
         int xh[VPL];
+        bool cact[VPL];
 #pragma unroll
         for (int j = 0; j < VPL; j++) {
             const int e = tid + j * kNT;
-            xa[j] = sA[e]; xb[j] = sB[e]; xh[j] = sH[e];
-            wave_scan(xa[j], xb[j], xh[j]);
+            cact[j] = __any((e % NS) <= ls);
+            xa[j] = 0; xb[j] = 0; xh[j] = 1;
+            if (cact[j]) {
+                xa[j] = sA[e]; xb[j] = sB[e]; xh[j] = sH[e];
+                wave_scan(xa[j], xb[j], xh[j]);
+            }
         }
         if (NS > 64) {
 #pragma unroll
@@ -419,7 +449,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
                 const int e = tid + j * kNT;
                 const int chunk = (e % NS) >> 6;
                 const int first = (e / NS) * (NS >> 6);
-                if (chunk > 0 && !xh[j]) {
+                if (cact[j] && chunk > 0 && !xh[j]) {
                     int64_t pa = sTA[first], pb = sTB[first];
                     int ph = sTH[first];
                     for (int c = 1; c < chunk; c++) {
@@ -433,32 +463,35 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
             }
         }
 #pragma unroll
-        for (int j = 0; j < VPL; j++) sB[tid + j * kNT] = xb[j];
+        for (int j = 0; j < VPL; j++)
+            if (cact[j]) sB[tid + j * kNT] = xb[j];
         __syncthreads();                                     // B2
         // finalize: carry-in, results, stores, releases for the next round
-        int64_t cin[VPL];
-#pragma unroll
-        for (int j = 0; j < VPL; j++)
-            cin[j] = slot == 0 ? carry[j] : sB[(o0 + j) * NS + slot - 1];
 #pragma unroll
         for (int i = 0; i < K; i++) {
             const int q = slot * K + i;
             const bool ok = q < rn;
-            const int64_t gap = R[q].gap;
-            const uint32_t flags = R[q].flags;
-            const int32_t thr = R[q].thread;
-            const bool last = ok && tcar && (flags & 2u) && (uint32_t)thr < (uint32_t)kMaxCarryThreads;
             Vals<VPL> fv, sv;
 #pragma unroll
-            for (int j = 0; j < VPL; j++) {
-                const int64_t F = ((before >> i) & 1u) ? max64(cin[j] + Dp[i][j], Fl[i][j]) : Fl[i][j];
-                const bool rmv = (rmk[j] >> i) & 1u;
-                const int64_t Rv = F + (rmv ? 0 : gap);
-                if (ok) sR[q * VS + o0 + j] = Rv;
-                if (last) sTC[thr * VS + o0 + j] = Rv;
-                fv.x[j] = F;
-                sv.x[j] = F - Dd[i][j];
-                if (ok && lok && !rmv) ms[j] = max64(ms[j], F);
+            for (int j = 0; j < VPL; j++) { fv.x[j] = 0; sv.x[j] = 0; }
+            if (wact) {
+                const int4 w0 = reinterpret_cast<const int4 *>(&R[q])[0];
+                const int64_t gap = ((int64_t)(uint32_t)w0.w << 32) | (uint32_t)w0.z;
+                const uint32_t flags = ok ? R[q].flags : 0u;
+                const bool last = tcar && (flags & 2u);
+                const int tcx = ((flags >> 2) & 63u) * VS + o0;
+#pragma unroll
+                for (int j = 0; j < VPL; j++) {
+                    const int64_t cin = slot == 0 ? carry[j] : sB[(o0 + j) * NS + slot - 1];
+                    const int64_t F = ((before >> i) & 1u) ? max64(cin + Dp[i][j], Fl[i][j]) : Fl[i][j];
+                    const bool rmv = (rmk[j] >> i) & 1u;
+                    const int64_t Rv = F + (rmv ? 0 : gap);
+                    if (ok) sR[q * VS + o0 + j] = Rv;
+                    if (last) sTC[tcx + j] = Rv;
+                    fv.x[j] = F;
+                    if (START) sv.x[j] = F - Dd[i][j];
+                    if (ok && lok && !rmv) ms[j] = max64(ms[j], F);
+                }
             }
             const bool st = ok && lok;
             gi64 *o = st ? (gi64 *)(a.finish + ((int64_t)U[i] * V + vf)) : dummy;
@@ -471,18 +504,19 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
             }
         }
 #pragma unroll
-        for (int j = 0; j < VPL; j++) carry[j] = sB[(o0 + j) * NS + NS - 1];
+        for (int j = 0; j < VPL; j++) carry[j] = sB[(o0 + j) * NS + ls];
+        // round k+2 goes into the buffer that round k-1 used: every wave
+        // finished reading it before the previous round's last barrier
+        {
+            u32x4 *dst = reinterpret_cast<u32x4 *>(sRec[b2]);
+            if (tid < nxt_w) dst[tid] = nx0;
+            if (PF > 1 && tid + kNT < nxt_w) dst[tid + kNT] = nx1;
+            if (PF > 2 && tid + 2 * kNT < nxt_w) dst[tid + 2 * kNT] = nx2;
+        }
         prev_r0 = r0;
         D = DN;
-        // record tid may belong to a slot of another wave, which reads it in
-        // its finalize: refill the slot of round k only after every wave is
-        // past that point, and publish it before the next round's issue
+        const int bt = b0; b0 = b1; b1 = b2; b2 = bt;
         __syncthreads();                                     // B3
-        if (tid < nxt_rn) {
-            uint4 *dst = reinterpret_cast<uint4 *>(&sRec[k & 1][tid]);
-            dst[0] = nx0; dst[1] = nx1; dst[2] = nx2; dst[3] = nx3;
-        }
-        __syncthreads();                                     // B4
     }
 #pragma unroll
     for (int j = 0; j < VPL; j++) atomicMax(&sMs[o0 + j], (unsigned long long)ms[j]);
@@ -509,6 +543,12 @@ __global__ __launch_bounds__(256) void k_round_fill(int64_t nsteps, const int32_
     }
 }
 
+template <int LPS, int VPL, int K, bool TLDS, bool START, bool UNI>
+void launch_one(int grid, hipStream_t s, const int32_t *r0, const int32_t *rn,
+                const int64_t *nrp, const Rec *rec, const PipeArgs &args) {
+    k_sim_pipe<LPS, VPL, K, TLDS, START, UNI><<<grid, kNT, 0, s>>>(r0, rn, nrp, rec, args);
+}
+
 template <int LPS, int VPL, int K>
 hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants *var,
                        int64_t *finish, int64_t *start, int64_t *makespan, hipStream_t s) {
@@ -527,21 +567,25 @@ hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants
     e = scan_exclusive(cnt, cnt, ns, s);
     if (e == hipSuccess && ns > 0)
         k_round_fill<<<grid_for(ns, 256), 256, 0, s>>>(ns, sch->step_ptr, cnt, RP, r0, rn);
-    PipeArgs args{sch->gat_src, sch->gat_spos, sch->gat_cls, sch->gat_gap, g->gap, var->table,
-                  var->n_cls, var->rm_bits, var->edge_on, sch->mask & g->cross_mask,
+    const uint64_t cls_mask = sch->mask & g->cross_mask;
+    PipeArgs args{sch->gat_ptr, sch->gat_src, sch->gat_spos, sch->gat_cls, sch->gat_gap, g->gap,
+                  var->table, var->n_cls, var->rm_bits, var->edge_on, cls_mask,
                   sch->thread_carry ? 1 : 0, var->V, var->W, finish, start, makespan, dummy};
     const int grid = (var->V + VS - 1) / VS;
     const int64_t *nrp = cnt + ns;
     const bool tl = (int64_t)var->n_cls * VS <= kTabLds;
+    // uniform: every gather class on in every variant, shift-only scales,
+    // durations below 2^32
+    const bool uni = tl && (var->all_mask & cls_mask) == cls_mask && !var->any_magic &&
+                     g->dmax < (int64_t(1) << 32);
+    const Rec *rc = sch->rec;
     if (e == hipSuccess) {
-        if (tl && start)
-            k_sim_pipe<LPS, VPL, K, true, true><<<grid, kNT, 0, s>>>(r0, rn, nrp, sch->rec, args);
-        else if (tl)
-            k_sim_pipe<LPS, VPL, K, true, false><<<grid, kNT, 0, s>>>(r0, rn, nrp, sch->rec, args);
-        else if (start)
-            k_sim_pipe<LPS, VPL, K, false, true><<<grid, kNT, 0, s>>>(r0, rn, nrp, sch->rec, args);
-        else
-            k_sim_pipe<LPS, VPL, K, false, false><<<grid, kNT, 0, s>>>(r0, rn, nrp, sch->rec, args);
+        if (uni && start) launch_one<LPS, VPL, K, true, true, true>(grid, s, r0, rn, nrp, rc, args);
+        else if (uni) launch_one<LPS, VPL, K, true, false, true>(grid, s, r0, rn, nrp, rc, args);
+        else if (tl && start) launch_one<LPS, VPL, K, true, true, false>(grid, s, r0, rn, nrp, rc, args);
+        else if (tl) launch_one<LPS, VPL, K, true, false, false>(grid, s, r0, rn, nrp, rc, args);
+        else if (start) launch_one<LPS, VPL, K, false, true, false>(grid, s, r0, rn, nrp, rc, args);
+        else launch_one<LPS, VPL, K, false, false, false>(grid, s, r0, rn, nrp, rc, args);
         e = hipGetLastError();
     }
     dfree(cnt, s); dfree(r0, s); dfree(rn, s); dfree(dummy, s);

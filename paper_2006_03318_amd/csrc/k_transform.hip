@@ -29,7 +29,7 @@ __global__ __launch_bounds__(kBS) void k_scale_table(const dd_ratio *__restrict_
                                                      unsigned long long *__restrict__ pmax,
                                                      unsigned long long *__restrict__ rmax_bits) {
     const int64_t i = (int64_t)blockIdx.x * kBS + threadIdx.x;
-    uint32_t e = 0;
+    uint32_t e = 0, mg = 0;
     int64_t pm = 0;
     int64_t rb = 0;
     if (i < count) {
@@ -55,6 +55,7 @@ __global__ __launch_bounds__(kBS) void k_scale_table(const dd_ratio *__restrict_
                 const uint64_t d0 = t / uq;
                 se.magic = ((d1 << 32) | d0) + 1;  // q is not a power of two: remainder != 0
                 se.shift = l - 2;
+                mg = 1;
             }
             pm = p;
             const double ratio = (double)p / (double)q;
@@ -64,9 +65,13 @@ __global__ __launch_bounds__(kBS) void k_scale_table(const dd_ratio *__restrict_
     }
     pm = wave_max64(pm);
     rb = wave_max64(rb);
-    for (int o = 32; o > 0; o >>= 1) e |= (uint32_t)__shfl_xor((int)e, o, 64);
+    for (int o = 32; o > 0; o >>= 1) {
+        e |= (uint32_t)__shfl_xor((int)e, o, 64);
+        mg |= (uint32_t)__shfl_xor((int)mg, o, 64);
+    }
     if ((threadIdx.x & 63) == 0) {
         if (e) atomicOr(err, e);
+        if (mg) atomicOr(err + 1, mg);
         atomicMax(pmax, (unsigned long long)pm);
         atomicMax(rmax_bits, (unsigned long long)rb);
     }
@@ -76,7 +81,8 @@ __global__ __launch_bounds__(kBS) void k_scale_table(const dd_ratio *__restrict_
 
 hipError_t launch_build_scale_table(const dd_ratio *scale_dev, int32_t n_cls, int32_t V,
                                     ScaleEntry *table, uint32_t *err, hipStream_t s) {
-    // err[0] = error bits, err[1..2] = pmax, err[3..4] = max ratio bits (caller-zeroed)
+    // err[0] = error bits, err[1] = some q is not a power of two, err[2..3] = pmax,
+    // err[4..5] = max ratio bits (caller-zeroed)
     const int64_t count = (int64_t)n_cls * V;
     unsigned long long *pmax = reinterpret_cast<unsigned long long *>(err + 2);
     unsigned long long *rmax = reinterpret_cast<unsigned long long *>(err + 4);

@@ -87,17 +87,19 @@ hipError_t scan_exclusive(const int64_t *in, int64_t *out, int64_t n, hipStream_
 namespace {
 constexpr int kBS = 256;
 
+constexpr int kValBlocks = 1024;   // grid-stride blocks: one set of atomics per block
+
 __global__ __launch_bounds__(kBS) void k_validate_nodes(
     int32_t n, int32_t T, const int32_t *__restrict__ prev, const int32_t *__restrict__ tid,
     const int64_t *__restrict__ dur, const int64_t *__restrict__ gap,
     const uint16_t *__restrict__ cls, const int64_t *__restrict__ in_ptr,
     int32_t *__restrict__ succ, int32_t *__restrict__ heads, uint32_t *__restrict__ err,
     LoadStats *__restrict__ st) {
-    const int64_t u = (int64_t)blockIdx.x * kBS + threadIdx.x;
     uint32_t e = 0;
-    int64_t d = 0, g = 0;
-    uint32_t c = 0;
-    if (u < n) {
+    // sums split at bit 32 so that no partial sum can overflow
+    int64_t dhi = 0, dlo = 0, ghi = 0, glo = 0, dm = 0, cm = 0;
+    for (int64_t u = (int64_t)blockIdx.x * kBS + threadIdx.x; u < n;
+         u += (int64_t)gridDim.x * kBS) {
         const int32_t t = tid[u];
         const bool t_ok = t >= 0 && t < T;
         if (!t_ok) e |= ERR_THREAD_RANGE;
@@ -110,29 +112,45 @@ __global__ __launch_bounds__(kBS) void k_validate_nodes(
         } else if (t_ok) {
             if (atomicAdd(&heads[t], 1) != 0) e |= ERR_HEADS;
         }
-        d = dur[u];
-        g = gap[u];
+        int64_t d = dur[u], g = gap[u];
         if (d < 0 || g < 0) e |= ERR_NEG_TIME;
         if (d >= kTimeLimit || g >= kTimeLimit) e |= ERR_BIG_TIME;
         if (d < 0 || d >= kTimeLimit) d = 0;
         if (g < 0 || g >= kTimeLimit) g = 0;
         if (in_ptr[u + 1] < in_ptr[u]) e |= ERR_PTR_ORDER;
-        c = cls ? cls[u] : 0;
+        const int64_t c = cls ? cls[u] : 0;
+        dhi += d >> 32; dlo += d & 0xffffffffll;
+        ghi += g >> 32; glo += g & 0xffffffffll;
+        dm = d > dm ? d : dm;
+        cm = c > cm ? c : cm;
     }
-    // reduce statistics per wave, one atomic per wave
-    int64_t dhi = wave_sum64(d >> 32), dlo = wave_sum64(d & 0xffffffffll);
-    int64_t ghi = wave_sum64(g >> 32), glo = wave_sum64(g & 0xffffffffll);
-    int64_t dm = wave_max64(d), cm = wave_max64((int64_t)c);
-    uint32_t eo = e;
-    for (int o = 32; o > 0; o >>= 1) eo |= (uint32_t)__shfl_xor((int)eo, o, 64);
+    // wave reduction, then the block's waves through LDS, one atomic set per block
+    dhi = wave_sum64(dhi); dlo = wave_sum64(dlo);
+    ghi = wave_sum64(ghi); glo = wave_sum64(glo);
+    dm = wave_max64(dm); cm = wave_max64(cm);
+    for (int o = 32; o > 0; o >>= 1) e |= (uint32_t)__shfl_xor((int)e, o, 64);
+    constexpr int NW = kBS / 64;
+    __shared__ int64_t red[7][NW];
+    const int w = threadIdx.x >> 6;
     if ((threadIdx.x & 63) == 0) {
+        red[0][w] = dhi; red[1][w] = dlo; red[2][w] = ghi; red[3][w] = glo;
+        red[4][w] = dm; red[5][w] = cm; red[6][w] = e;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int i = 1; i < NW; i++) {
+            dhi += red[0][i]; dlo += red[1][i]; ghi += red[2][i]; glo += red[3][i];
+            dm = red[4][i] > dm ? red[4][i] : dm;
+            cm = red[5][i] > cm ? red[5][i] : cm;
+            e |= (uint32_t)red[6][i];
+        }
         atomicAdd(&st->dsum_hi, (unsigned long long)dhi);
         atomicAdd(&st->dsum_lo, (unsigned long long)dlo);
         atomicAdd(&st->gsum_hi, (unsigned long long)ghi);
         atomicAdd(&st->gsum_lo, (unsigned long long)glo);
         atomicMax(&st->dmax, (unsigned long long)dm);
         atomicMax(&st->cls_max, (unsigned long long)cm);
-        if (eo) atomicOr(err, eo);
+        if (e) atomicOr(err, e);
     }
 }
 
@@ -260,7 +278,9 @@ __global__ __launch_bounds__(kBS) void k_cross_fill(
 
 hipError_t launch_validate_nodes(const dd_graph *g, const int64_t *in_ptr, int32_t *succ,
                                  int32_t *heads, uint32_t *err, LoadStats *st, hipStream_t s) {
-    k_validate_nodes<<<grid_for(g->n, kBS), kBS, 0, s>>>(g->n, g->n_threads, g->thread_prev,
+    int blocks = grid_for(g->n, kBS);
+    if (blocks > kValBlocks) blocks = kValBlocks;
+    k_validate_nodes<<<blocks, kBS, 0, s>>>(g->n, g->n_threads, g->thread_prev,
                                                          g->thread_id, g->dur, g->gap, g->cls,
                                                          in_ptr, succ, heads, err, st);
     return hipGetLastError();

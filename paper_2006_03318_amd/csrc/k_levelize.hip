@@ -59,6 +59,14 @@ __global__ __launch_bounds__(kBS) void k_req_count(int32_t n, Req r, uint64_t ma
     flag[p] = c > 0;
 }
 
+// A candidate packed for the windowed rounds: its order position and its
+// first two requirements (parent position in order space, parent thread);
+// meta = thread of req 0 | thread of req 1 << 8 | requirement count << 16.
+struct alignas(16) CandEnt {
+    int32_t pos, g0, g1;
+    uint32_t meta;
+};
+
 // candidates (positions with a cross-thread parent) and their requirements
 __global__ __launch_bounds__(kBS) void k_req_fill(int32_t n, Req r, uint64_t mask,
                                                   const int64_t *__restrict__ cidx,
@@ -66,7 +74,8 @@ __global__ __launch_bounds__(kBS) void k_req_fill(int32_t n, Req r, uint64_t mas
                                                   int64_t *__restrict__ cand_pos,
                                                   int64_t *__restrict__ req_ptr,
                                                   int32_t *__restrict__ req_chain,
-                                                  int64_t *__restrict__ req_gpos) {
+                                                  int64_t *__restrict__ req_gpos,
+                                                  CandEnt *__restrict__ pent) {
     const int64_t p = (int64_t)blockIdx.x * kBS + threadIdx.x;
     if (p >= n) return;
     if (cidx[p + 1] == cidx[p]) return;
@@ -75,14 +84,22 @@ __global__ __launch_bounds__(kBS) void k_req_fill(int32_t n, Req r, uint64_t mas
     int64_t o = rptr_by_pos[p];
     req_ptr[i] = o;
     const int32_t u = r.order[p];
+    CandEnt ce{(int32_t)p, 0, 0, 0u};
+    uint32_t nr = 0;
     for (int64_t k = r.xin_ptr[u]; k < r.xin_ptr[u + 1]; k++) {
         if (!on(mask, r.xin_cls[k])) continue;
         const int32_t s = r.xin_src[k];
         const int32_t ts = r.tid[s];
+        const int64_t gp = r.base[ts] + r.rank[s];
         req_chain[o] = ts;
-        req_gpos[o] = r.base[ts] + r.rank[s];
+        req_gpos[o] = gp;
+        if (nr == 0) { ce.g0 = (int32_t)gp; ce.meta |= (uint32_t)ts & 0xff; }
+        if (nr == 1) { ce.g1 = (int32_t)gp; ce.meta |= ((uint32_t)ts & 0xff) << 8; }
+        nr++;
         o++;
     }
+    ce.meta |= (nr < 0xffff ? nr : 0xffffu) << 16;
+    if (pent) pent[i] = ce;
 }
 
 __global__ __launch_bounds__(kBS) void k_cand_base(int32_t T, const int64_t *__restrict__ base,
@@ -237,6 +254,185 @@ __global__ __launch_bounds__(kWG) void k_kahn_rounds(KahnArgs a) {
         }
         round++;
         __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        a.step_seg[round] = nseg;
+        a.result[0] = round;
+        a.result[1] = nseg;
+    }
+}
+
+// Windowed rounds for graphs with at most kWinT threads: the same rounds as
+// above, with each thread's next candidates staged in LDS (one wave per
+// thread) so that a round reads no global memory except to refill a window
+// that is less than half full, to test a candidate beyond its window, or for
+// a requirement past the first two of a candidate.
+constexpr int kWinT = 16;
+constexpr int kWinEnt = 6144;           // LDS candidate entries shared by all threads
+constexpr int kRefill = 8;              // window entries loaded per lane at once
+constexpr int kFar = 16;                // candidates per lane and step past the window
+constexpr int kNear = 1;                // candidates per lane and step inside the window
+
+struct WinArgs {
+    int32_t T, wlog;                    // window of 2^wlog entries per thread
+    const int64_t *base;                // [T+1]
+    const int64_t *cbase;               // [T+1]
+    const CandEnt *pent;                // [C]
+    const int64_t *req_ptr;             // [C+1]
+    const int32_t *req_chain;
+    const int64_t *req_gpos;
+    int64_t *seg_start, *seg_len;       // [n]
+    int32_t *seg_step;                  // [n]
+    int64_t *step_seg;                  // [n+1]
+    int64_t *result;                    // [0] steps, [1] segments
+    uint32_t *err;
+};
+
+__device__ __forceinline__ bool win_blocked(const WinArgs &a, const CandEnt &e, int64_t j,
+                                            const int32_t *front) {
+    const uint32_t nr = e.meta >> 16;
+    if (e.g0 >= front[e.meta & 0xff]) return true;
+    if (nr > 1 && e.g1 >= front[(e.meta >> 8) & 0xff]) return true;
+    if (nr > 2) {
+        for (int64_t k = a.req_ptr[j] + 2; k < a.req_ptr[j + 1]; k++)
+            if (a.req_gpos[k] >= front[a.req_chain[k]]) return true;
+    }
+    return false;
+}
+
+__global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
+    __shared__ CandEnt s_win[kWinEnt + 64];
+    __shared__ int32_t s_front[kWinT], s_nfront[kWinT], s_end[kWinT];
+    __shared__ int32_t s_ci[kWinT], s_nci[kWinT], s_ce[kWinT], s_wend[kWinT];
+    __shared__ int s_stop;
+    const int lane = threadIdx.x & 63;
+    const int t = threadIdx.x >> 6;               // one wave per thread of the graph
+    const int W = 1 << a.wlog;
+    const bool mine = t < a.T;
+    CandEnt *win = s_win + (mine ? t : 0) * W;
+    if (threadIdx.x < a.T) {
+        const int u = threadIdx.x;
+        s_front[u] = (int32_t)a.base[u];
+        s_end[u] = (int32_t)a.base[u + 1];
+        s_ci[u] = (int32_t)a.cbase[u];
+        s_ce[u] = (int32_t)a.cbase[u + 1];
+        s_wend[u] = (int32_t)a.cbase[u];
+    }
+    if (threadIdx.x == 0) s_stop = 0;
+    __syncthreads();
+    int64_t nseg = 0, round = 0;
+    for (;;) {
+        // refill this thread's window when less than half of it lies ahead:
+        // all loads of a refill are in flight together (one memory latency)
+        if (mine) {
+            const int ci = s_ci[t], ce = s_ce[t], wend = s_wend[t];
+            if (wend < ce && wend - ci < (W >> 1)) {
+                const int nend = ci + W < ce ? ci + W : ce;
+                const int from = wend > ci ? wend : ci;     // entries behind ci are spent
+                for (int j0 = from; j0 < nend; j0 += kRefill * 64) {
+                    CandEnt v[kRefill];
+#pragma unroll
+                    for (int r = 0; r < kRefill; r++) {
+                        const int j = j0 + r * 64 + lane;
+                        v[r] = a.pent[j < nend ? j : from];
+                    }
+#pragma unroll
+                    for (int r = 0; r < kRefill; r++) {   // past the end: a spare slot
+                        const int j = j0 + r * 64 + lane;
+                        CandEnt *dst = j < nend ? &win[j & (W - 1)] : &s_win[kWinEnt + lane];
+                        *dst = v[r];
+                    }
+                }
+                if (lane == 0) s_wend[t] = nend;
+            }
+        }
+        // A: advance each thread's front past its ready candidates
+        if (mine) {
+            const int f = s_front[t], end = s_end[t], ce = s_ce[t], wend = s_wend[t];
+            int ci = s_ci[t];
+            int cnew = ce;
+            if (f < end) {
+                for (;;) {
+                    if (ci >= ce) { cnew = ce; break; }
+                    if (ci < wend) {
+                        // kNear x 64 candidates from the LDS window, the reads
+                        // of all of them in flight together
+                        const int lim = wend < ce ? wend : ce;
+                        bool bl[kNear];
+#pragma unroll
+                        for (int r = 0; r < kNear; r++) {
+                            const int j = ci + r * 64 + lane;
+                            const CandEnt e = win[j & (W - 1)];
+                            bl[r] = j < lim && win_blocked(a, e, j, s_front);
+                        }
+                        bool hit = false;
+#pragma unroll
+                        for (int r = 0; r < kNear; r++) {
+                            const unsigned long long bal = __ballot(bl[r]);
+                            if (bal && !hit) { cnew = ci + r * 64 + __ffsll((long long)bal) - 1; hit = true; }
+                        }
+                        if (hit) break;
+                        ci = ci + kNear * 64 < lim ? ci + kNear * 64 : lim;
+                    } else {
+                        // past the window (a long ready run): kFar x 64
+                        // candidates from global memory, all loads in flight
+                        CandEnt e[kFar];
+#pragma unroll
+                        for (int r = 0; r < kFar; r++) {
+                            const int j = ci + r * 64 + lane;
+                            e[r] = a.pent[j < ce ? j : ce - 1];
+                        }
+                        bool hit = false;
+#pragma unroll
+                        for (int r = 0; r < kFar; r++) {
+                            const int j = ci + r * 64 + lane;
+                            const bool b = j < ce && win_blocked(a, e[r], j, s_front);
+                            const unsigned long long bal = __ballot(b);
+                            if (bal && !hit) { cnew = ci + r * 64 + __ffsll((long long)bal) - 1; hit = true; }
+                        }
+                        if (hit) break;
+                        ci += kFar * 64;
+                    }
+                }
+            } else {
+                cnew = ci;
+            }
+            if (lane == 0) {
+                s_nci[t] = cnew;
+                s_nfront[t] = f >= end ? f
+                              : (cnew < ce ? (cnew < wend ? win[cnew & (W - 1)].pos : a.pent[cnew].pos)
+                                           : end);
+            }
+        }
+        __syncthreads();
+        // C + D (wave 0): emit one segment per advanced thread, move the fronts
+        if (t == 0) {
+            int len = 0, unfinished = 0;
+            if (lane < a.T) {
+                len = s_nfront[lane] - s_front[lane];
+                unfinished = s_front[lane] < s_end[lane];
+            }
+            const unsigned long long adv = __ballot(len > 0);
+            const bool any_left = __ballot(unfinished) != 0;
+            if (!any_left) {
+                if (lane == 0) s_stop = 1;
+            } else if (adv == 0) {
+                if (lane == 0) { s_stop = 1; atomicOr(a.err, ERR_KAHN_CYCLE); }
+            } else {
+                if (len > 0) {
+                    const int64_t sidx = nseg + __popcll(adv & ((1ull << lane) - 1));
+                    a.seg_start[sidx] = s_front[lane];
+                    a.seg_len[sidx] = len;
+                    a.seg_step[sidx] = (int32_t)round;
+                }
+                if (lane == 0) a.step_seg[round] = nseg;
+                if (lane < a.T) { s_front[lane] = s_nfront[lane]; s_ci[lane] = s_nci[lane]; }
+                nseg += __popcll(adv);
+                round++;
+            }
+        }
+        __syncthreads();
+        if (s_stop) break;
     }
     if (threadIdx.x == 0) {
         a.step_seg[round] = nseg;
@@ -508,6 +704,8 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
             *seg_len = nullptr, *seg_off = nullptr, *step_seg = nullptr, *result = nullptr,
             *gcnt = nullptr, *lvl_cnt = nullptr;
     int32_t *req_chain = nullptr, *long_list = nullptr, *seg_step = nullptr, *level = nullptr;
+    CandEnt *pent = nullptr;
+    const bool windowed = T <= kWinT;
     uint32_t *err = nullptr;
     unsigned long long *wmax = nullptr;
     int64_t h_res[2] = {0, 0};
@@ -544,6 +742,7 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
     CK(dalloc_n(&req_ptr, (size_t)h_C + 1, s));
     CK(dalloc_n(&req_chain, (size_t)h_R + 1, s));
     CK(dalloc_n(&req_gpos, (size_t)h_R + 1, s));
+    if (windowed) CK(dalloc_n(&pent, (size_t)h_C + 1, s));
     CK(dalloc_n(&cbase, (size_t)T + 1, s));
     CK(dalloc_n(&front, (size_t)T, s));
     CK(dalloc_n(&ci, (size_t)T, s));
@@ -557,14 +756,21 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
     CK(dalloc_n(&step_seg, N1 + 1, s));
     if (n > 0) {
         k_req_fill<<<gN, kBS, 0, s>>>((int32_t)n, rq, mask, cidx, rptr, cand_pos, req_ptr,
-                                      req_chain, req_gpos);
+                                      req_chain, req_gpos, pent);
         CK(hipGetLastError());
     }
     CK(hipMemcpyAsync(req_ptr + h_C, &h_R, sizeof(int64_t), hipMemcpyHostToDevice, s));
     k_cand_base<<<grid_for((int64_t)T + 1, kBS), kBS, 0, s>>>(T, g->thread_base, cidx, cbase,
                                                                front, ci);
     CK(hipGetLastError());
-    {
+    if (windowed) {
+        int wlog = 6;                                  // 2^wlog entries per thread
+        while ((int64_t)T << (wlog + 1) <= kWinEnt) wlog++;
+        WinArgs wa{T, wlog, g->thread_base, cbase, pent, req_ptr, req_chain, req_gpos,
+                   seg_start, seg_len, seg_step, step_seg, result, err};
+        k_kahn_win<<<1, kWG, 0, s>>>(wa);
+        CK(hipGetLastError());
+    } else {
         KahnArgs ka{T, n, g->thread_base, cand_pos, cbase, req_ptr, req_chain, req_gpos,
                     front, ci, nfront, nci, long_list, seg_start, seg_len, seg_step, step_seg,
                     result, err};
@@ -696,7 +902,7 @@ done:
     dfree(req_chain, s); dfree(req_gpos, s); dfree(cbase, s); dfree(front, s); dfree(ci, s);
     dfree(nfront, s); dfree(nci, s); dfree(long_list, s); dfree(seg_start, s);
     dfree(seg_len, s); dfree(seg_off, s); dfree(seg_step, s); dfree(step_seg, s);
-    dfree(gcnt, s); dfree(lvl_cnt, s); dfree(level, s);
+    dfree(gcnt, s); dfree(lvl_cnt, s); dfree(level, s); dfree(pent, s);
     return st;
 }
 

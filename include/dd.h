@@ -47,7 +47,11 @@
  *     caller; the library never frees them.
  *   - Handles are owned by the library until the matching *_free.  A handle
  *     keeps device memory, released on the stream it was created on, which
- *     must stay valid until the handle is freed.
+ *     must stay valid until the handle is freed.  Released device memory
+ *     stays in a cache of the library, kept per device and stream, and is
+ *     handed out again to later calls on that same stream (stream order
+ *     makes the reuse safe); it returns to the device when an allocation
+ *     would otherwise fail, or at process exit.
  *   - `stream` is a hipStream_t (NULL = default stream).  Work is
  *     stream-ordered.  Input validation is synchronous: load, levelize and
  *     apply_transforms wait for their own device checks before returning.

@@ -2,7 +2,10 @@
 // order in which the device passes of each call run.
 
 #include <atomic>
+#include <map>
 #include <math.h>
+#include <mutex>
+#include <unordered_map>
 #include <stdarg.h>
 #include <stdio.h>
 #include <stdlib.h>
@@ -26,20 +29,6 @@ dd_status fail(dd_status s, const char *fmt, ...) {
 dd_status hip_fail(hipError_t e, const char *what) {
     return fail(e == hipErrorOutOfMemory ? DD_ENOMEM : DD_EHIP, "%s: %s", what,
                 hipGetErrorString(e));
-}
-
-void configure_pool_once() {
-    static std::atomic<uint64_t> done_mask{0};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev >= 64) return;
-    const uint64_t bit = 1ull << dev;
-    if (done_mask.load() & bit) return;
-    hipMemPool_t pool;
-    if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
-        uint64_t thr = UINT64_MAX;   // keep freed blocks cached for the next call
-        (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &thr);
-    }
-    done_mask.fetch_or(bit);
 }
 
 dd_status map_err_bits(uint32_t e) {
@@ -92,15 +81,81 @@ void free_sched_arrays(dd_sched *x) {
 
 namespace dd {
 
+// Device memory cache.  Released blocks wait in a free list keyed by
+// (device, stream) and serve later requests on that stream only: work on
+// one stream runs in order, so a block released there can be handed out
+// again at once.  A cached block serves a request of up to its size and at
+// least half of it.  New blocks come from hipMalloc; when that fails, every
+// cached block of the device is returned and the allocation retried.
+namespace {
+
+struct CacheKey {
+    int dev;
+    hipStream_t s;
+    bool operator<(const CacheKey &o) const { return dev != o.dev ? dev < o.dev : s < o.s; }
+};
+struct LiveBlock {
+    size_t bytes;
+    int dev;
+};
+
+std::mutex g_mu;
+std::map<CacheKey, std::multimap<size_t, void *>> g_free;
+std::unordered_map<void *, LiveBlock> g_live;
+
+void release_cached(int dev) {   // caller holds g_mu; dev is the current device
+    (void)hipDeviceSynchronize();  // work queued before a release may still read a block
+    for (auto it = g_free.begin(); it != g_free.end();) {
+        if (it->first.dev == dev) {
+            for (auto &b : it->second) (void)hipFree(b.second);
+            it = g_free.erase(it);
+        } else {
+            ++it;
+        }
+    }
+}
+
+}  // namespace
+
 hipError_t dalloc(void **p, size_t bytes, hipStream_t s) {
-    configure_pool_once();
     *p = nullptr;
-    if (bytes == 0) bytes = 16;
-    return hipMallocAsync(p, bytes, s);
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    bytes = (bytes + 511) & ~(size_t)511;
+    if (bytes == 0) bytes = 512;
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto fit = g_free.find(CacheKey{dev, s});
+    if (fit != g_free.end()) {
+        auto it = fit->second.lower_bound(bytes);
+        if (it != fit->second.end() && it->first / 2 <= bytes) {
+            *p = it->second;
+            g_live[*p] = LiveBlock{it->first, dev};
+            fit->second.erase(it);
+            return hipSuccess;
+        }
+    }
+    e = hipMalloc(p, bytes);
+    if (e == hipErrorOutOfMemory) {
+        (void)hipGetLastError();
+        release_cached(dev);
+        e = hipMalloc(p, bytes);
+    }
+    if (e != hipSuccess) {
+        *p = nullptr;
+        return e;
+    }
+    g_live[*p] = LiveBlock{bytes, dev};
+    return hipSuccess;
 }
 
 void dfree(void *p, hipStream_t s) {
-    if (p) (void)hipFreeAsync(p, s);
+    if (!p) return;
+    std::lock_guard<std::mutex> lk(g_mu);
+    auto it = g_live.find(p);
+    if (it == g_live.end()) return;
+    g_free[CacheKey{it->second.dev, s}].emplace(it->second.bytes, p);
+    g_live.erase(it);
 }
 
 }  // namespace dd

@@ -70,6 +70,7 @@ struct PipeArgs {
 };
 
 constexpr int kTabLds = 4096;     // scale entries kept in LDS (8 B each)
+constexpr int kSmall = 64;        // rounds of at most this many positions: one wave per variant
 typedef __attribute__((address_space(1))) int64_t gi64;   // global-memory int64
 
 // VPL consecutive int64 of one task row (one load or store per lane)
@@ -90,12 +91,16 @@ __device__ __forceinline__ void store_vals(gi64 *o, const Vals<2> &v) {
 template <int N> struct I64V { typedef long long T __attribute__((ext_vector_type(N))); };
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
+// Loads prefetched a round ahead: the task's removal word and, for the first
+// gather when its source finished two or more rounds earlier, the source's
+// finish, removal word and gap.  A second gather (rare: a task waiting on
+// two other threads) loads its old source when the round needs it.
 template <int K, int VPL>
-struct Dyn {                      // per-lane loads for the next round
+struct Dyn {
     uint32_t rmw[K];              // removal word of the task
-    Vals<VPL> f0[K], f1[K];       // finish of old gather sources
-    uint32_t r0w[K], r1w[K];      // removal words of those sources
-    int64_t g0gap[K], g1gap[K];   // gaps of those sources
+    Vals<VPL> f0[K];              // finish of the first gather's source
+    uint32_t r0w[K];              // removal word of that source
+    int64_t g0gap[K];             // gap of that source
 };
 
 __device__ __forceinline__ bool cls_on(uint64_t eon, uint8_t c) {
@@ -169,6 +174,11 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
     static_assert(PF <= 3, "record prefetch words per lane");
     static_assert(NE / 64 <= 16, "chunk totals");
     static_assert(!UNI || TLDS, "uniform path keeps the table in LDS");
+    // small rounds (at most 64 positions): wave w alone handles variants
+    // w, w + 8, ... for every position of the round (one per lane), so the
+    // round needs no slot scan across waves and only the ring barrier
+    constexpr int PS = (VS + 7) / 8;      // variants per wave in a small round
+    static_assert(PS <= K && PS <= 2, "load slots for small rounds");
     // records of rounds k, k+1 (read) and k+2 (being filled): a ring of three
     __shared__ uint4 sRec[3][RW];
     __shared__ int64_t sR[RP * VS];
@@ -179,11 +189,13 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
     __shared__ uint64_t sT[TLDS ? kTabLds : 1];
     __shared__ int64_t sTC[kMaxCarryThreads * VS];
     __shared__ unsigned long long sMs[VS];
+    __shared__ int64_t sCarry[VS];        // release at the end of a big round
     __shared__ uint64_t sEon[VS];
     __shared__ int sFlags;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
+    const int wv = tid >> 6;
     const int lis = tid % LPS;
     const int slot = tid / LPS;
     const int nwg = gridDim.x;
@@ -201,7 +213,8 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
     const int64_t V = a.V, W = a.W;
     const int64_t nr = *n_rounds;
     const int o0 = lis * VPL;                 // variant offset inside the workgroup
-    gi64 *const dummy = (gi64 *)(a.dummy + tid * VPL);
+    // stores that must not land go to one 16-byte spot per wave (one line)
+    gi64 *const dummy = (gi64 *)(a.dummy + (tid >> 6) * 2);
     const bool tcar = a.thread_carry != 0;
 
     if (tid == 0) sFlags = 0;
@@ -245,39 +258,80 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
     const bool all_on = UNI || (eall & a.cls_mask) == a.cls_mask;
     const bool shift_only = UNI || (TLDS && !(sFlags & 1));
 
+    // positions per slot in a round of rn positions: small rounds spread
+    // over all waves, one position per slot, instead of filling the first
+    // wave with K positions per slot
+    auto per_slot = [&](int rn) { return rn <= NS ? 1 : (rn + NS - 1) / NS; };
+
     // loads of round kk (records in ring buffer b); a gather is old when its
     // source position precedes prev_r0 (its round has ended before round kk-1)
     auto issue = [&](int64_t kk, int b, int prev_r0, Dyn<K, VPL> &d) {
         const int rn = round_rn[kk];
+        const int ke = per_slot(rn);
         const Rec *R = reinterpret_cast<const Rec *>(sRec[b]);
+        if (rn <= kSmall) {
+            // small layout: position = lane; slot jj of the load registers
+            // holds variant w + 8 jj of this wave (K loads of the removal
+            // word either way, so that both layouts issue alike)
+            const int q = lane;
+            const bool ok = q < rn;
+            const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
+            const int4 w1 = r4[1];
+            const int p1 = r4[2].x;
+            const int32_t node = ok ? w1.x : 0;
+            const bool n0 = ok && w1.y >= 0 && w1.w < prev_r0;
+            const int64_t a0 = n0 ? w1.y : 0;
+            (void)p1;
+#pragma unroll
+            for (int jj = 0; jj < K; jj++) {
+                const int os = wv + 8 * jj;
+                const bool vv = jj < PS && os < VS && v0 + os < a.V;
+                const int64_t vs_ = vv ? v0 + os : 0;
+                const int64_t vwj = vs_ >> 5;
+                d.rmw[jj] = a.rm[(int64_t)(vv ? node : 0) * W + vwj];
+                if (jj < PS) {
+                    if (__any(n0 && vv)) {
+                        d.f0[jj].x[0] = a.finish[a0 * V + vs_];
+                        d.r0w[jj] = a.rm[a0 * W + vwj];
+                        d.g0gap[jj] = a.gap[a0];
+                    }
+                }
+            }
+            return;
+        }
 #pragma unroll
         for (int i = 0; i < K; i++) {
-            const int q = slot * K + i;
-            const bool ok = q < rn;
+            const int q = slot * ke + i;
+            const bool ok = i < ke && q < rn;
             const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
             const int4 w1 = r4[1];   // node, g0_src, g1_src, g0_spos
             const int p1 = r4[2].x;  // g1_spos
             const int32_t node = ok ? w1.x : 0;
             const bool n0 = ok && w1.y >= 0 && w1.w < prev_r0;
-            const bool n1 = ok && w1.z >= 0 && p1 < prev_r0;
-            const int64_t a0 = n0 ? w1.y : 0, a1 = n1 ? w1.z : 0;
+            const int64_t a0 = n0 ? w1.y : 0;
+            (void)p1;
             d.rmw[i] = a.rm[(int64_t)node * W + vw];
             if (__any(n0)) {
                 d.f0[i] = *reinterpret_cast<const Vals<VPL> *>(a.finish + a0 * V + vvf);
                 d.r0w[i] = a.rm[a0 * W + vw];
                 d.g0gap[i] = a.gap[a0];
             }
-            if (__any(n1)) {
-                d.f1[i] = *reinterpret_cast<const Vals<VPL> *>(a.finish + a1 * V + vvf);
-                d.r1w[i] = a.rm[a1 * W + vw];
-                d.g1gap[i] = a.gap[a1];
-            }
         }
     };
     Dyn<K, VPL> D;
     if (nr > 0) issue(0, 0, 0, D);
+    // Consume the first round's loads here: the loop's registers then hold
+    // no load in flight on entry, and the wait-count bookkeeping does not
+    // make every round's walk wait for part of the next round's loads.
+#pragma unroll
+    for (int i = 0; i < K; i++) {
+        asm volatile("" ::"v"(D.rmw[i]), "v"(D.r0w[i]), "v"(D.g0gap[i]));
+#pragma unroll
+        for (int j = 0; j < VPL; j++) asm volatile("" ::"v"(D.f0[i].x[j]));
+    }
 
     typename I64V<VPL>::T carry = 0, ms = 0;
+    int64_t msS0 = 0, msS1 = 0;               // small rounds: variants w and w + 8
     int prev_r0 = 0;
     int b0 = 0, b1 = 1, b2 = 2;               // ring buffers of rounds k, k+1, k+2
     for (int64_t k = 0; k < nr; k++) {
@@ -300,7 +354,125 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         if (PF > 1) nx1 = nsrc[tid + kNT < nxt_w ? tid + kNT : 0];
         if (PF > 2) nx2 = nsrc[tid + 2 * kNT < nxt_w ? tid + 2 * kNT : 0];
 
-        const bool wact = __any(slot * K < rn);  // some position of this wave is live
+        if (rn <= kSmall) {
+            // ---- small round: one position per lane, variants per wave ----
+            const int q = lane;
+            const bool ok = q < rn;
+            const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
+            const int4 w0 = r4[0], w1 = r4[1], w2 = r4[2];
+            const int64_t dur = ((int64_t)(uint32_t)w0.y << 32) | (uint32_t)w0.x;
+            const int64_t gap = ((int64_t)(uint32_t)w0.w << 32) | (uint32_t)w0.z;
+            const int32_t node = w1.x, s0 = w1.y, s1 = w1.z, p0 = w1.w, p1 = w2.x;
+            const uint32_t cl = (uint32_t)w2.y;
+            const int cls = ok ? (int)(cl & 0xffff) : 0;
+            const uint8_t c0 = (cl >> 16) & 0xff, c1 = cl >> 24;
+            const uint32_t flags = ok ? (uint32_t)w2.z : 0u;
+            const bool head = flags & 1u;
+            const bool old0 = p0 < prev_r0, old1 = p1 < prev_r0;
+            int i0 = p0 - prev_r0, i1 = p1 - prev_r0;
+            i0 = i0 < 0 ? 0 : (i0 >= RP ? RP - 1 : i0);
+            i1 = i1 < 0 ? 0 : (i1 >= RP ? RP - 1 : i1);
+            const bool has0 = ok && s0 >= 0;
+            const bool has1 = ok && s1 >= 0;
+            const bool any1 = __any(has1);
+            const uint32_t extra = flags >> 8;
+            const int tcx = ((flags >> 2) & 63u) * VS;
+#pragma unroll
+            for (int jj = 0; jj < K; jj++) {
+                const int os = wv + 8 * jj;
+                const bool vw_ok = jj < PS && os < VS && v0 + os < a.V;   // wave-uniform
+                const int64_t vs_ = vw_ok ? v0 + os : 0;
+                int64_t F = 0, S = 0;
+                bool st = false;
+                if (vw_ok) {
+                    const uint32_t bit = (uint32_t)(vs_ & 31);
+                    const int64_t vwj = vs_ >> 5;
+                    const uint64_t eo = sEon[os];
+                    const bool rmv = (D.rmw[jj] >> bit) & 1u;
+                    int64_t X;
+                    {
+                        const int64_t ro = D.f0[jj].x[0] + (((D.r0w[jj] >> bit) & 1u) ? 0 : D.g0gap[jj]);
+                        const int64_t rel = old0 ? ro : sR[i0 * VS + os];
+                        const bool on = has0 && (all_on || cls_on(eo, c0));
+                        X = on ? rel : 0;
+                    }
+                    if (any1) {
+                        int64_t ro = 0;
+                        if (__any(has1 && old1)) {       // rare: loaded on demand
+                            const int64_t a1 = has1 && old1 ? s1 : 0;
+                            const bool r1 = (a.rm[a1 * W + vwj] >> bit) & 1u;
+                            ro = a.finish[a1 * V + vs_] + (r1 ? 0 : a.gap[a1]);
+                        }
+                        const int64_t rel = old1 ? ro : sR[i1 * VS + os];
+                        const bool on = has1 && (all_on || cls_on(eo, c1));
+                        X = on ? max64(X, rel) : X;
+                    }
+                    if (tcar) X = head ? max64(X, sTC[tcx + os]) : X;
+                    if (extra) {
+                        const int64_t e1 = a.gat_ptr[r0 + q + 1];
+                        for (int64_t e = a.gat_ptr[r0 + q] + 2; e < e1; e++) {
+                            const uint8_t c = a.gat_cls[e];
+                            if (!cls_on(eo, c)) continue;
+                            const int32_t sp = a.gat_spos[e];
+                            int64_t rel;
+                            if (sp < prev_r0) {
+                                const int64_t sx = a.gat_src[e];
+                                const bool rs = (a.rm[sx * W + vwj] >> bit) & 1u;
+                                rel = a.finish[sx * V + vs_] + (rs ? 0 : a.gat_gap[e]);
+                            } else {
+                                rel = sR[(sp - prev_r0) * VS + os];
+                            }
+                            X = max64(X, rel);
+                        }
+                    }
+                    int64_t dp;
+                    if (UNI) {
+                        const uint64_t te = sT[cls * VS + os];
+                        dp = (int64_t)(((uint64_t)(uint32_t)dur * (uint32_t)te) >> ((uint32_t)(te >> 32) & 0xff));
+                    } else if (TLDS) {
+                        const uint64_t te = sT[cls * VS + os];
+                        if (shift_only) {
+                            dp = (int64_t)(((uint64_t)dur * (uint32_t)te) >> ((uint32_t)(te >> 32) & 0xff));
+                        } else {
+                            dp = scaled8(dur, te, a.table, (int64_t)cls * V + vs_);
+                        }
+                    } else {
+                        dp = scaled(dur, a.table[(int64_t)cls * V + vs_]);
+                    }
+                    const bool live = ok && !rmv;
+                    dp = live ? dp : 0;
+                    const int64_t gp = live ? gap : 0;
+                    // one position per lane: c -> max(c + A, B); the round's
+                    // first position closes the segment (carry folded in)
+                    int64_t sa = ok ? dp + gp : 0;
+                    int64_t sb = ok ? X + dp + gp : 0;
+                    int sh = ok && (head || q == 0);
+                    if (q == 0 && ok && !head) sb = max64(sCarry[os] + sa, sb);
+                    wave_scan(sa, sb, sh);
+                    const int64_t Rv = sb;
+                    F = Rv - gp;
+                    S = F - dp;
+                    if (ok) sR[q * VS + os] = Rv;
+                    if (ok && tcar && (flags & 2u)) sTC[tcx + os] = Rv;
+                    if (ok && !rmv) {
+                        if (jj == 0) msS0 = max64(msS0, F);
+                        else msS1 = max64(msS1, F);
+                    }
+                    st = ok;
+                }
+                gi64 *o = st ? (gi64 *)(a.finish + ((int64_t)node * V + vs_)) : dummy;
+                asm volatile("" : "+v"(o));  // one store per slot in either layout
+                *o = F;
+                if (START) {
+                    gi64 *os2 = st ? (gi64 *)(a.start + ((int64_t)node * V + vs_)) : dummy;
+                    asm volatile("" : "+v"(os2));
+                    *os2 = S;
+                }
+            }
+        } else {
+        // ---- big round: slots of consecutive positions across all waves ----
+        const int ke = per_slot(rn);              // positions per slot this round
+        const bool wact = __any(slot * ke < rn);  // some position of this wave is live
         // walk: local max-plus recurrence over this slot's K positions
         int64_t Fl[K][VPL], Dp[K][VPL], Dd[K][VPL];
         int32_t U[K];
@@ -314,7 +486,8 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         if (wact) {
 #pragma unroll
             for (int i = 0; i < K; i++) {
-                const int q = slot * K + i;
+                if (i >= ke) break;
+                const int q = slot * ke + i;
                 const bool ok = q < rn;
                 const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
                 const int4 w0 = r4[0], w1 = r4[1], w2 = r4[2];
@@ -351,7 +524,12 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
                         X = on ? rel : 0;
                     }
                     if (any1) {
-                        const int64_t ro = D.f1[i].x[j] + (((D.r1w[i] >> bit) & 1u) ? 0 : D.g1gap[i]);
+                        int64_t ro = 0;
+                        if (__any(has1 && old1)) {       // rare: loaded on demand
+                            const int64_t a1 = has1 && old1 ? s1 : 0;
+                            const bool r1 = (a.rm[a1 * W + vw] >> bit) & 1u;
+                            ro = a.finish[a1 * V + vvf + j] + (r1 ? 0 : a.gap[a1]);
+                        }
                         const int64_t rn1 = sR[i1 * VS + o0 + j];
                         const int64_t rel = old1 ? ro : rn1;
                         const bool on = has1 && (all_on || cls_on(eon[j], c1));
@@ -423,7 +601,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         // inclusive scan of slot summaries per variant: DPP within the wave,
         // then earlier 64-slot chunks of the same variant; chunks whose
         // slots all lie past the round's end are skipped
-        const int ls = (rn - 1) / K;                         // last live slot
+        const int ls = (rn - 1) / ke;                        // last live slot
         int64_t xa[VPL], xb[VPL];
         int xh[VPL];
         bool cact[VPL];
@@ -469,8 +647,8 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         // finalize: carry-in, results, stores, releases for the next round
 #pragma unroll
         for (int i = 0; i < K; i++) {
-            const int q = slot * K + i;
-            const bool ok = q < rn;
+            const int q = slot * ke + i;
+            const bool ok = i < ke && q < rn;
             Vals<VPL> fv, sv;
 #pragma unroll
             for (int j = 0; j < VPL; j++) { fv.x[j] = 0; sv.x[j] = 0; }
@@ -505,6 +683,11 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         }
 #pragma unroll
         for (int j = 0; j < VPL; j++) carry[j] = sB[(o0 + j) * NS + ls];
+        if (slot == 0) {
+#pragma unroll
+            for (int j = 0; j < VPL; j++) sCarry[o0 + j] = carry[j];
+        }
+        }   // big round
         // round k+2 goes into the buffer that round k-1 used: every wave
         // finished reading it before the previous round's last barrier
         {
@@ -520,6 +703,8 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
     }
 #pragma unroll
     for (int j = 0; j < VPL; j++) atomicMax(&sMs[o0 + j], (unsigned long long)ms[j]);
+    if (wv < VS) atomicMax(&sMs[wv], (unsigned long long)msS0);
+    if (PS > 1 && wv + 8 < VS) atomicMax(&sMs[wv + 8], (unsigned long long)msS1);
     __syncthreads();
     if (tid < VS && v0 + tid < a.V) a.makespan[v0 + tid] = (int64_t)sMs[tid];
 }

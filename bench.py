@@ -41,6 +41,37 @@ def algorithmic_bytes(n, V, n_gathers, n_cls, want_start=False):
             + n_cls * V * 16.0)
 
 
+def kernel_source_digest():
+    """sha256 over the sources the simulation kernel is compiled from."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("k_simulate.hip", "dd_internal.h", "dd_common.cuh"):
+        with open(os.path.join(ROOT, "paper_2006_03318_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(config, n, V):
+    """HBM bytes per launch from the committed counter summary of this
+    workload (FETCH_SIZE + WRITE_SIZE, each scaled by the plain copy's), or
+    None when there is none or the kernel's sources changed since."""
+    path = os.path.join(ROOT, "profiles", "k_sim_pipe_transformer_x32_counters.md")
+    if config != 5 or not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        if line.startswith("traffic_bytes_per_launch:"):
+            for tok in line.split()[1:]:
+                k, _, v = tok.partition("=")
+                fields[k] = v
+            break
+    if fields.get("source_sha256") != kernel_source_digest():
+        return None
+    if fields.get("tasks") != str(n) or fields.get("variants") != str(V):
+        return None
+    return int(fields["bytes"])
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -50,17 +81,30 @@ def main():
     ap.add_argument("--variants", type=int, default=None)
     ap.add_argument("--cpu-sample", type=int, default=1024,
                     help="variants the oracle runs for the CPU baseline (0 = skip)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only copy MIB MiB device to device three times: the plain copy "
+                         "whose byte counters scale the simulation kernel's")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU: the path shards over variants with no exchange "
-              "during simulation, and this build runs on a single MI355X only "
-              "(--gpus %d not supported)" % args.gpus, file=sys.stderr)
+        print("bench.py measures one GPU: the simulation shards over variants with no "
+              "exchange between shards, and runs on more than one GPU are not part of "
+              "this benchmark (--gpus %d not supported)" % args.gpus, file=sys.stderr)
         sys.exit(2)
 
     import torch
     from paper_2006_03318_amd import batch, binding as B, workloads as W
 
     assert torch.cuda.is_available(), "bench needs a GPU"
+    if args.copy_calibration > 0:
+        nb = args.copy_calibration << 20
+        src = torch.ones(nb // 8, dtype=torch.int64, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": nb, "copy_bytes_written": nb, "copies": 3}))
+        return
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
@@ -68,8 +112,8 @@ def main():
     t0 = time.time()
     g, vs = W.config(args.config, variants=args.variants)
     gen_s = time.time() - t0
-    print("[bench] config %d: %d tasks, %d dependency edges, %d threads, %d variants "
-          "(generated in %.1f s)" % (args.config, g.n, g.n_edges, g.n_threads, vs.n_variants,
+    print("[bench] %s: %d tasks, %d dependency edges, %d threads, %d variants "
+          "(generated in %.1f s)" % (g.name, g.n, g.n_edges, g.n_threads, vs.n_variants,
                                      gen_s), file=sys.stderr, flush=True)
     di = batch.to_device(g, vs, device=dev)
     outs = []
@@ -139,8 +183,9 @@ def main():
     nbytes = algorithmic_bytes(g.n, vs.n_variants, info.get("n_gathers", 0), di.n_cls)
     achieved = nbytes / (sim_ms / 1e3) / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                "kernel": "k_simulate", "algorithmic_bytes_per_launch": int(nbytes),
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": measured_traffic(args.config, g.n, vs.n_variants),
+                "kernel": "k_sim_pipe", "algorithmic_bytes_per_launch": int(nbytes),
                 "avg_launch_ms": round(sim_ms, 4)}
 
     # parity sample + CPU baseline: the oracle on the first variants
@@ -175,9 +220,9 @@ def main():
         "vs_baseline": None,
         "dtype": "int64",
         "data": "synthetic (seeded trace-shaped task graph, random-variant tables)",
-        "config": {"workload": "config %d: %s, %d tasks x %d variants, %d dependency edges, "
-                               "%d threads" % (args.config, g.name, g.n, vs.n_variants,
-                                               g.n_edges, g.n_threads),
+        "config": {"workload": "%s sweep: %d tasks x %d variants, %d dependency edges, "
+                               "%d threads" % (g.name, g.n, vs.n_variants, g.n_edges,
+                                               g.n_threads),
                    "tasks": g.n, "variants": vs.n_variants, "phases": info.get("n_steps"),
                    "gathers": info.get("n_gathers")},
         "breakdown_ms": {k: round(float(np.mean(v)), 3) for k, v in rows.items()},

@@ -290,7 +290,7 @@ def _cnn_iteration(n_layers=20) -> _Template:
 
 def _transformer_iteration(n_layers=24, n_wu=554, comm=False, bucket_bytes=25 << 20,
                            layer_grad_bytes=None):
-    """Transformer encoder iteration (Sec. 4 workloads; BERT-like): per layer
+    """Transformer encoder iteration (BERT-like, as in the evaluation of Sec. 6.1): per layer
     40 fwd kernels (8 GEMM-like) with one fork/join group of 8 aux-stream
     kernels joined back through events, 80 bwd kernels (16 GEMM-like) and
     n_wu element-wise weight-update kernels.  With comm=True, one all-reduce

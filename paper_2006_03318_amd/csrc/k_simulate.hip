@@ -340,11 +340,13 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         uint64_t eon[VPL];
 #pragma unroll
         for (int j = 0; j < VPL; j++) eon[j] = sEon[o0 + j];
-        // next round's loads, issued before this round's walk so they have a
-        // whole round to arrive (records of k+1 are in LDS since round k-1)
+        // next round's loads (records of k+1 are in LDS since round k-1): a
+        // small round issues them first; a big round after its walk, so the
+        // walk does not queue behind them and the two register sets are
+        // never live together
         Dyn<K, VPL> DN;
         const int64_t k1 = k + 1 < nr ? k + 1 : k;
-        issue(k1, k + 1 < nr ? b1 : b0, r0, DN);
+        const int bN = k + 1 < nr ? b1 : b0;
         // records of round k+2: global -> registers now, -> LDS at the round's end
         const int64_t k2 = k + 2 < nr ? k + 2 : k;
         const int nxt_w = k + 2 < nr ? round_rn[k2] * 3 : 0;
@@ -356,6 +358,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
 
         if (rn <= kSmall) {
             // ---- small round: one position per lane, variants per wave ----
+            issue(k1, bN, r0, DN);
             const int q = lane;
             const bool ok = q < rn;
             const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
@@ -598,6 +601,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
             sH[e] = hh || slot == 0;
         }
         __syncthreads();                                     // B1
+        issue(k1, bN, r0, DN);
         // inclusive scan of slot summaries per variant: DPP within the wave,
         // then earlier 64-slot chunks of the same variant; chunks whose
         // slots all lie past the round's end are skipped

@@ -274,6 +274,7 @@ dd_status dd_graph_load(int32_t n, int32_t n_threads, const int64_t *in_ptr, con
         g->gsum = gs >= ((__int128)1 << 62) ? ((int64_t)1 << 62) : (int64_t)gs;
     }
     g->dmax = (int64_t)hs.dmax;
+    g->gmax = (int64_t)hs.gmax;
     g->max_cls = (int32_t)hs.cls_max;
     g->cross_mask = hs.cross_mask;
     if (g->dsum + (__int128)g->gsum >= ((__int128)1 << 62)) {

@@ -52,7 +52,7 @@ struct alignas(16) Rec {
     uint32_t flags;   // bit0: first task of a thread run; bit1: last task of a run;
                       // bits 2..7: thread (graphs with at most 64 threads);
                       // bits 8..31: gathers beyond two (saturating)
-    int32_t pad;
+    uint32_t g0_gap32;  // gap of gather 0's source, low 32 bits (whole when gaps < 2^32)
 };
 static_assert(sizeof(Rec) == 48, "record size");
 
@@ -64,7 +64,7 @@ constexpr int kMaxCarryThreads = 64;
 // overflow for n < 2^31 values below 2^62).
 struct LoadStats {
     unsigned long long dsum_hi, dsum_lo, gsum_hi, gsum_lo;
-    unsigned long long dmax, cls_max, cross_mask, pad;
+    unsigned long long dmax, cls_max, cross_mask, gmax;
 };
 
 }  // namespace dd
@@ -76,7 +76,7 @@ struct dd_graph {
     hipStream_t stream = nullptr;
     uint64_t id = 0;
     // statistics (host)
-    int64_t dmax = 0, gsum = 0;
+    int64_t dmax = 0, gmax = 0, gsum = 0;
     __int128 dsum = 0;
     int32_t max_cls = 0;
     uint64_t cross_mask = 0;      // edge classes present among cross-thread edges

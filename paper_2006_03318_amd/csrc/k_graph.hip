@@ -97,7 +97,7 @@ __global__ __launch_bounds__(kBS) void k_validate_nodes(
     LoadStats *__restrict__ st) {
     uint32_t e = 0;
     // sums split at bit 32 so that no partial sum can overflow
-    int64_t dhi = 0, dlo = 0, ghi = 0, glo = 0, dm = 0, cm = 0;
+    int64_t dhi = 0, dlo = 0, ghi = 0, glo = 0, dm = 0, gm = 0, cm = 0;
     for (int64_t u = (int64_t)blockIdx.x * kBS + threadIdx.x; u < n;
          u += (int64_t)gridDim.x * kBS) {
         const int32_t t = tid[u];
@@ -122,19 +122,20 @@ __global__ __launch_bounds__(kBS) void k_validate_nodes(
         dhi += d >> 32; dlo += d & 0xffffffffll;
         ghi += g >> 32; glo += g & 0xffffffffll;
         dm = d > dm ? d : dm;
+        gm = g > gm ? g : gm;
         cm = c > cm ? c : cm;
     }
     // wave reduction, then the block's waves through LDS, one atomic set per block
     dhi = wave_sum64(dhi); dlo = wave_sum64(dlo);
     ghi = wave_sum64(ghi); glo = wave_sum64(glo);
-    dm = wave_max64(dm); cm = wave_max64(cm);
+    dm = wave_max64(dm); gm = wave_max64(gm); cm = wave_max64(cm);
     for (int o = 32; o > 0; o >>= 1) e |= (uint32_t)__shfl_xor((int)e, o, 64);
     constexpr int NW = kBS / 64;
-    __shared__ int64_t red[7][NW];
+    __shared__ int64_t red[8][NW];
     const int w = threadIdx.x >> 6;
     if ((threadIdx.x & 63) == 0) {
         red[0][w] = dhi; red[1][w] = dlo; red[2][w] = ghi; red[3][w] = glo;
-        red[4][w] = dm; red[5][w] = cm; red[6][w] = e;
+        red[4][w] = dm; red[5][w] = cm; red[6][w] = e; red[7][w] = gm;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -143,12 +144,14 @@ __global__ __launch_bounds__(kBS) void k_validate_nodes(
             dm = red[4][i] > dm ? red[4][i] : dm;
             cm = red[5][i] > cm ? red[5][i] : cm;
             e |= (uint32_t)red[6][i];
+            gm = red[7][i] > gm ? red[7][i] : gm;
         }
         atomicAdd(&st->dsum_hi, (unsigned long long)dhi);
         atomicAdd(&st->dsum_lo, (unsigned long long)dlo);
         atomicAdd(&st->gsum_hi, (unsigned long long)ghi);
         atomicAdd(&st->gsum_lo, (unsigned long long)glo);
         atomicMax(&st->dmax, (unsigned long long)dm);
+        atomicMax(&st->gmax, (unsigned long long)gm);
         atomicMax(&st->cls_max, (unsigned long long)cm);
         if (e) atomicOr(err, e);
     }

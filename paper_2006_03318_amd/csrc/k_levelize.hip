@@ -533,7 +533,7 @@ __global__ __launch_bounds__(kBS) void k_records(
     const int64_t *__restrict__ pos_dur, const int64_t *__restrict__ pos_gap,
     const uint16_t *__restrict__ pos_cls, const int64_t *__restrict__ gptr,
     const int32_t *__restrict__ gsrc, const int32_t *__restrict__ gspos,
-    const uint8_t *__restrict__ gcls, Rec *__restrict__ rec) {
+    const uint8_t *__restrict__ gcls, const int64_t *__restrict__ ggap, Rec *__restrict__ rec) {
     const int64_t q = (int64_t)blockIdx.x * kBS + threadIdx.x;
     if (q >= n) return;
     Rec r;
@@ -545,7 +545,11 @@ __global__ __launch_bounds__(kBS) void k_records(
     const int64_t ng = e1 - e0;
     uint32_t c0 = 0, c1 = 0;
     r.g0_src = -1; r.g1_src = -1; r.g0_spos = 0; r.g1_spos = 0;
-    if (ng > 0) { r.g0_src = gsrc[e0]; r.g0_spos = gspos[e0]; c0 = gcls[e0]; }
+    r.g0_gap32 = 0;
+    if (ng > 0) {
+        r.g0_src = gsrc[e0]; r.g0_spos = gspos[e0]; c0 = gcls[e0];
+        r.g0_gap32 = (uint32_t)ggap[e0];
+    }
     if (ng > 1) { r.g1_src = gsrc[e0 + 1]; r.g1_spos = gspos[e0 + 1]; c1 = gcls[e0 + 1]; }
     r.cls = (uint32_t)pos_cls[q] | (c0 << 16) | (c1 << 24);
     int64_t extra = ng > 2 ? ng - 2 : 0;   // count saturates; the gather pointers are exact
@@ -554,7 +558,6 @@ __global__ __launch_bounds__(kBS) void k_records(
     const bool last = (q + 1 == n) || (pos_flags[q + 1] & 1);
     r.flags = (uint32_t)(pos_flags[q] & 1) | (last ? 2u : 0u) |
               ((uint32_t)(t < kMaxCarryThreads ? t : 0) << 2) | ((uint32_t)extra << 8);
-    r.pad = 0;
     rec[q] = r;
 }
 
@@ -885,7 +888,7 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
                                                                     sch->gat_spos);
                 k_records<<<gN, kBS, 0, s>>>(n, g->thread_id, sch->pos_node, sch->pos_flags, sch->pos_dur,
                                              sch->pos_gap, sch->pos_cls, sch->gat_ptr, sch->gat_src,
-                                             sch->gat_spos, sch->gat_cls, sch->rec);
+                                             sch->gat_spos, sch->gat_cls, sch->gat_gap, sch->rec);
                 CK(hipGetLastError());
             }
             dfree(pos_of, s);

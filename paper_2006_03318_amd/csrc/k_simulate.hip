@@ -157,7 +157,8 @@ __device__ __forceinline__ void wave_scan(int64_t &a, int64_t &b, int &h) {
 //
 // UNI: every variant of the launch enables every edge class that the
 // schedule's gathers use, every scale is a power of two and every duration
-// is below 2^32 (one 32x32 multiply and a shift per scaled duration).
+// and gap is below 2^32 (one 32x32 multiply and a shift per scaled
+// duration; a gather source's gap comes from the record).
 template <int LPS, int VPL, int K, bool TLDS, bool START, bool UNI>
 __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ round_r0,
                                                   const int32_t *__restrict__ round_rn,
@@ -288,14 +289,24 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
                 const bool vv = jj < PS && os < VS && v0 + os < a.V;
                 const int64_t vs_ = vv ? v0 + os : 0;
                 const int64_t vwj = vs_ >> 5;
-                d.rmw[jj] = a.rm[(int64_t)(vv ? node : 0) * W + vwj];
+                // every field is written on every path: stores that differ
+                // between paths get merged through a selected address, which
+                // would keep the whole struct in scratch
+                const uint32_t rw = a.rm[(int64_t)(vv ? node : 0) * W + vwj];
+                Vals<VPL> f{};
+                uint32_t r0 = 0;
+                int64_t gg = 0;
                 if (jj < PS) {
                     if (__any(n0 && vv)) {
-                        d.f0[jj].x[0] = a.finish[a0 * V + vs_];
-                        d.r0w[jj] = a.rm[a0 * W + vwj];
-                        d.g0gap[jj] = a.gap[a0];
+                        f.x[0] = a.finish[a0 * V + vs_];
+                        r0 = a.rm[a0 * W + vwj];
+                        if (!UNI) gg = a.gap[a0];
                     }
                 }
+                d.rmw[jj] = rw;
+                d.f0[jj] = f;
+                d.r0w[jj] = r0;
+                d.g0gap[jj] = gg;
             }
             return;
         }
@@ -310,12 +321,19 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
             const bool n0 = ok && w1.y >= 0 && w1.w < prev_r0;
             const int64_t a0 = n0 ? w1.y : 0;
             (void)p1;
-            d.rmw[i] = a.rm[(int64_t)node * W + vw];
+            const uint32_t rw = a.rm[(int64_t)node * W + vw];
+            Vals<VPL> f{};
+            uint32_t r0 = 0;
+            int64_t gg = 0;
             if (__any(n0)) {
-                d.f0[i] = *reinterpret_cast<const Vals<VPL> *>(a.finish + a0 * V + vvf);
-                d.r0w[i] = a.rm[a0 * W + vw];
-                d.g0gap[i] = a.gap[a0];
+                f = *reinterpret_cast<const Vals<VPL> *>(a.finish + a0 * V + vvf);
+                r0 = a.rm[a0 * W + vw];
+                if (!UNI) gg = a.gap[a0];
             }
+            d.rmw[i] = rw;
+            d.f0[i] = f;
+            d.r0w[i] = r0;
+            d.g0gap[i] = gg;
         }
     };
     Dyn<K, VPL> D;
@@ -325,7 +343,8 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
     // make every round's walk wait for part of the next round's loads.
 #pragma unroll
     for (int i = 0; i < K; i++) {
-        asm volatile("" ::"v"(D.rmw[i]), "v"(D.r0w[i]), "v"(D.g0gap[i]));
+        asm volatile("" ::"v"(D.rmw[i]), "v"(D.r0w[i]));
+        if (!UNI) asm volatile("" ::"v"(D.g0gap[i]));
 #pragma unroll
         for (int j = 0; j < VPL; j++) asm volatile("" ::"v"(D.f0[i].x[j]));
     }
@@ -358,7 +377,8 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
 
         if (rn <= kSmall) {
             // ---- small round: one position per lane, variants per wave ----
-            issue(k1, bN, r0, DN);
+            Dyn<K, VPL> DNs;
+            issue(k1, bN, r0, DNs);
             const int q = lane;
             const bool ok = q < rn;
             const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
@@ -394,7 +414,8 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
                     const bool rmv = (D.rmw[jj] >> bit) & 1u;
                     int64_t X;
                     {
-                        const int64_t ro = D.f0[jj].x[0] + (((D.r0w[jj] >> bit) & 1u) ? 0 : D.g0gap[jj]);
+                        const int64_t g0g = UNI ? (int64_t)(uint32_t)w2.w : D.g0gap[jj];
+                        const int64_t ro = D.f0[jj].x[0] + (((D.r0w[jj] >> bit) & 1u) ? 0 : g0g);
                         const int64_t rel = old0 ? ro : sR[i0 * VS + os];
                         const bool on = has0 && (all_on || cls_on(eo, c0));
                         X = on ? rel : 0;
@@ -472,6 +493,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
                     *os2 = S;
                 }
             }
+            DN = DNs;
         } else {
         // ---- big round: slots of consecutive positions across all waves ----
         const int ke = per_slot(rn);              // positions per slot this round
@@ -520,7 +542,8 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
                     const bool rmv = (D.rmw[i] >> bit) & 1u;
                     int64_t X;
                     {
-                        const int64_t ro = D.f0[i].x[j] + (((D.r0w[i] >> bit) & 1u) ? 0 : D.g0gap[i]);
+                        const int64_t g0g = UNI ? (int64_t)(uint32_t)w2.w : D.g0gap[i];
+                        const int64_t ro = D.f0[i].x[j] + (((D.r0w[i] >> bit) & 1u) ? 0 : g0g);
                         const int64_t rn0 = sR[i0 * VS + o0 + j];
                         const int64_t rel = old0 ? ro : rn0;
                         const bool on = has0 && (all_on || cls_on(eon[j], c0));
@@ -601,7 +624,8 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
             sH[e] = hh || slot == 0;
         }
         __syncthreads();                                     // B1
-        issue(k1, bN, r0, DN);
+        Dyn<K, VPL> DNb;
+        issue(k1, bN, r0, DNb);
         // inclusive scan of slot summaries per variant: DPP within the wave,
         // then earlier 64-slot chunks of the same variant; chunks whose
         // slots all lie past the round's end are skipped
@@ -691,6 +715,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
 #pragma unroll
             for (int j = 0; j < VPL; j++) sCarry[o0 + j] = carry[j];
         }
+        DN = DNb;
         }   // big round
         // round k+2 goes into the buffer that round k-1 used: every wave
         // finished reading it before the previous round's last barrier
@@ -764,9 +789,9 @@ hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants
     const int64_t *nrp = cnt + ns;
     const bool tl = (int64_t)var->n_cls * VS <= kTabLds;
     // uniform: every gather class on in every variant, shift-only scales,
-    // durations below 2^32
+    // durations and gaps below 2^32 (a source's gap then rides in its record)
     const bool uni = tl && (var->all_mask & cls_mask) == cls_mask && !var->any_magic &&
-                     g->dmax < (int64_t(1) << 32);
+                     g->dmax < (int64_t(1) << 32) && g->gmax < (int64_t(1) << 32);
     const Rec *rc = sch->rec;
     if (e == hipSuccess) {
         if (uni && start) launch_one<LPS, VPL, K, true, true, true>(grid, s, r0, rn, nrp, rc, args);

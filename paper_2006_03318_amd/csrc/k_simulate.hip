@@ -533,15 +533,18 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
                 i1 = i1 < 0 ? 0 : (i1 >= RP ? RP - 1 : i1);
                 const bool has0 = ok && s0 >= 0;
                 const bool has1 = ok && s1 >= 0;
+                // wave-uniform skips: chain phases have few gathers and heads
+                const bool any0 = __any(has0);
                 const bool any1 = __any(has1);
+                const bool anyh = __any(head);
                 const uint32_t extra = flags >> 8;
                 const int tcx = ((flags >> 2) & 63u) * VS + o0;
 #pragma unroll
                 for (int j = 0; j < VPL; j++) {
                     const uint32_t bit = vsh + j;
                     const bool rmv = (D.rmw[i] >> bit) & 1u;
-                    int64_t X;
-                    {
+                    int64_t X = 0;
+                    if (any0) {
                         const int64_t g0g = UNI ? (int64_t)(uint32_t)w2.w : D.g0gap[i];
                         const int64_t ro = D.f0[i].x[j] + (((D.r0w[i] >> bit) & 1u) ? 0 : g0g);
                         const int64_t rn0 = sR[i0 * VS + o0 + j];
@@ -561,7 +564,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
                         const bool on = has1 && (all_on || cls_on(eon[j], c1));
                         X = on ? max64(X, rel) : X;
                     }
-                    if (tcar) {                                // previous task of the thread
+                    if (tcar && anyh) {                        // previous task of the thread
                         const int64_t tc = sTC[tcx + j];
                         X = head ? max64(X, tc) : X;
                     }
@@ -599,8 +602,10 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
                     }
                     dp = live ? dp : 0;
                     const int64_t gp = live ? gap : 0;
-                    A[j] = head ? 0 : A[j];
-                    B[j] = head ? 0 : B[j];
+                    if (anyh) {
+                        A[j] = head ? 0 : A[j];
+                        B[j] = head ? 0 : B[j];
+                    }
                     const int64_t F = max64(B[j], X) + dp;
                     Dp[i][j] = A[j] + dp;
                     A[j] += dp + gp;

@@ -263,8 +263,9 @@ __global__ __launch_bounds__(kWG) void k_kahn_rounds(KahnArgs a) {
 }
 
 // Windowed rounds for graphs with at most kWinT threads: the same rounds as
-// above, with each thread's next candidates staged in LDS (one wave per
-// thread) so that a round reads no global memory except to refill a window
+// above, with each thread's next candidates staged in LDS (a wave per thread,
+// waves taking threads w, w + waves, ...) so that a round reads no global
+// memory except to refill a window
 // that is less than half full, to test a candidate beyond its window, or for
 // a requirement past the first two of a candidate.
 constexpr int kWinT = 16;
@@ -306,10 +307,9 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
     __shared__ int32_t s_ci[kWinT], s_nci[kWinT], s_ce[kWinT], s_wend[kWinT];
     __shared__ int s_stop;
     const int lane = threadIdx.x & 63;
-    const int t = threadIdx.x >> 6;               // one wave per thread of the graph
+    const int wave = threadIdx.x >> 6;
+    const int nw = blockDim.x >> 6;               // waves; wave w takes threads w, w + nw, ...
     const int W = 1 << a.wlog;
-    const bool mine = t < a.T;
-    CandEnt *win = s_win + (mine ? t : 0) * W;
     if (threadIdx.x < a.T) {
         const int u = threadIdx.x;
         s_front[u] = (int32_t)a.base[u];
@@ -324,7 +324,8 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
     for (;;) {
         // refill this thread's window when less than half of it lies ahead:
         // all loads of a refill are in flight together (one memory latency)
-        if (mine) {
+        for (int t = wave; t < a.T; t += nw) {
+            CandEnt *win = s_win + t * W;
             const int ci = s_ci[t], ce = s_ce[t], wend = s_wend[t];
             if (wend < ce && wend - ci < (W >> 1)) {
                 const int nend = ci + W < ce ? ci + W : ce;
@@ -347,7 +348,8 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
             }
         }
         // A: advance each thread's front past its ready candidates
-        if (mine) {
+        for (int t = wave; t < a.T; t += nw) {
+            CandEnt *win = s_win + t * W;
             const int f = s_front[t], end = s_end[t], ce = s_ce[t], wend = s_wend[t];
             int ci = s_ci[t];
             int cnew = ce;
@@ -406,7 +408,7 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
         }
         __syncthreads();
         // C + D (wave 0): emit one segment per advanced thread, move the fronts
-        if (t == 0) {
+        if (wave == 0) {
             int len = 0, unfinished = 0;
             if (lane < a.T) {
                 len = s_nfront[lane] - s_front[lane];

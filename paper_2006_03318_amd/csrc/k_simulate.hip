@@ -37,6 +37,8 @@
 
 #include <stdlib.h>
 
+#include <type_traits>
+
 namespace dd {
 namespace {
 
@@ -61,6 +63,9 @@ struct PipeArgs {
     const ScaleEntry *table;      // [n_cls][V]
     int32_t n_cls;
     const uint32_t *rm;           // [n][W]
+    const void *rmp;              // [workgroups][n] removal bits of the workgroup's variants
+                                  // per schedule position (u8 for VS <= 8, else u16)
+    int64_t npos;                 // positions (= tasks)
     const uint64_t *edge_on;      // [V]
     uint64_t cls_mask;            // edge classes present in the schedule's gathers
     int32_t thread_carry;         // previous task of a run comes from LDS carries
@@ -91,13 +96,12 @@ __device__ __forceinline__ void store_vals(gi64 *o, const Vals<2> &v) {
 template <int N> struct I64V { typedef long long T __attribute__((ext_vector_type(N))); };
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// Loads prefetched a round ahead: the task's removal word and, for the first
-// gather when its source finished two or more rounds earlier, the source's
-// finish, removal word and gap.  A second gather (rare: a task waiting on
+// Loads prefetched a round ahead: for the first gather when its source
+// finished two or more rounds earlier, the source's finish, removal word and
+// gap.  (The task's own removal bits come with the records.)  A second gather (rare: a task waiting on
 // two other threads) loads its old source when the round needs it.
 template <int K, int VPL>
 struct Dyn {
-    uint32_t rmw[K];              // removal word of the task
     Vals<VPL> f0[K];              // finish of the first gather's source
     uint32_t r0w[K];              // removal word of that source
     int64_t g0gap[K];             // gap of that source
@@ -180,8 +184,12 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
     // round needs no slot scan across waves and only the ring barrier
     constexpr int PS = (VS + 7) / 8;      // variants per wave in a small round
     static_assert(PS <= K && PS <= 2, "load slots for small rounds");
-    // records of rounds k, k+1 (read) and k+2 (being filled): a ring of three
+    // records of rounds k, k+1 (read) and k+2 (being filled): a ring of three;
+    // beside them the removal bits of the workgroup's variants per position
+    typedef typename std::conditional<(VS <= 8), uint8_t, uint16_t>::type RmT;
+    static_assert(VS <= 16, "removal bits per position");
     __shared__ uint4 sRec[3][RW];
+    __shared__ RmT sRm[3][RP];
     __shared__ int64_t sR[RP * VS];
     __shared__ int64_t sA[NE], sB[NE];
     __shared__ uint8_t sH[NE];
@@ -217,6 +225,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
     // stores that must not land go to one 16-byte spot per wave (one line)
     gi64 *const dummy = (gi64 *)(a.dummy + (tid >> 6) * 2);
     const bool tcar = a.thread_carry != 0;
+    const RmT *const rmrow = reinterpret_cast<const RmT *>(a.rmp) + (int64_t)wg * a.npos;
 
     if (tid == 0) sFlags = 0;
     {   // the record ring starts zeroed (no stale fields past a round's end)
@@ -248,6 +257,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
             const int r0 = round_r0[rr], rn = round_rn[rr];
             const uint4 *src = reinterpret_cast<const uint4 *>(rec + r0);
             for (int i = tid; i < rn * 3; i += kNT) sRec[rr][i] = src[i];
+            for (int i = tid; i < rn; i += kNT) sRm[rr][i] = rmrow[r0 + i];
         }
     }
     __syncthreads();
@@ -279,7 +289,6 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
             const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
             const int4 w1 = r4[1];
             const int p1 = r4[2].x;
-            const int32_t node = ok ? w1.x : 0;
             const bool n0 = ok && w1.y >= 0 && w1.w < prev_r0;
             const int64_t a0 = n0 ? w1.y : 0;
             (void)p1;
@@ -292,7 +301,6 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
                 // every field is written on every path: stores that differ
                 // between paths get merged through a selected address, which
                 // would keep the whole struct in scratch
-                const uint32_t rw = a.rm[(int64_t)(vv ? node : 0) * W + vwj];
                 Vals<VPL> f{};
                 uint32_t r0 = 0;
                 int64_t gg = 0;
@@ -303,7 +311,6 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
                         if (!UNI) gg = a.gap[a0];
                     }
                 }
-                d.rmw[jj] = rw;
                 d.f0[jj] = f;
                 d.r0w[jj] = r0;
                 d.g0gap[jj] = gg;
@@ -317,11 +324,9 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
             const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
             const int4 w1 = r4[1];   // node, g0_src, g1_src, g0_spos
             const int p1 = r4[2].x;  // g1_spos
-            const int32_t node = ok ? w1.x : 0;
             const bool n0 = ok && w1.y >= 0 && w1.w < prev_r0;
             const int64_t a0 = n0 ? w1.y : 0;
             (void)p1;
-            const uint32_t rw = a.rm[(int64_t)node * W + vw];
             Vals<VPL> f{};
             uint32_t r0 = 0;
             int64_t gg = 0;
@@ -330,7 +335,6 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
                 r0 = a.rm[a0 * W + vw];
                 if (!UNI) gg = a.gap[a0];
             }
-            d.rmw[i] = rw;
             d.f0[i] = f;
             d.r0w[i] = r0;
             d.g0gap[i] = gg;
@@ -343,7 +347,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
     // make every round's walk wait for part of the next round's loads.
 #pragma unroll
     for (int i = 0; i < K; i++) {
-        asm volatile("" ::"v"(D.rmw[i]), "v"(D.r0w[i]));
+        asm volatile("" ::"v"(D.r0w[i]));
         if (!UNI) asm volatile("" ::"v"(D.g0gap[i]));
 #pragma unroll
         for (int j = 0; j < VPL; j++) asm volatile("" ::"v"(D.f0[i].x[j]));
@@ -372,6 +376,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         const u32x4 *nsrc = reinterpret_cast<const u32x4 *>(rec + round_r0[k2]);
         u32x4 nx0, nx1, nx2;
         nx0 = nsrc[tid < nxt_w ? tid : 0];
+        const RmT nrm = rmrow[round_r0[k2] + (tid < nxt_w / 3 ? tid : 0)];
         if (PF > 1) nx1 = nsrc[tid + kNT < nxt_w ? tid + kNT : 0];
         if (PF > 2) nx2 = nsrc[tid + 2 * kNT < nxt_w ? tid + 2 * kNT : 0];
 
@@ -390,6 +395,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
             const int cls = ok ? (int)(cl & 0xffff) : 0;
             const uint8_t c0 = (cl >> 16) & 0xff, c1 = cl >> 24;
             const uint32_t flags = ok ? (uint32_t)w2.z : 0u;
+            const uint32_t rb = ok ? (uint32_t)sRm[b0][q] : 0u;   // removal bits of the task
             const bool head = flags & 1u;
             const bool old0 = p0 < prev_r0, old1 = p1 < prev_r0;
             int i0 = p0 - prev_r0, i1 = p1 - prev_r0;
@@ -411,7 +417,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
                     const uint32_t bit = (uint32_t)(vs_ & 31);
                     const int64_t vwj = vs_ >> 5;
                     const uint64_t eo = sEon[os];
-                    const bool rmv = (D.rmw[jj] >> bit) & 1u;
+                    const bool rmv = (rb >> os) & 1u;
                     int64_t X;
                     {
                         const int64_t g0g = UNI ? (int64_t)(uint32_t)w2.w : D.g0gap[jj];
@@ -525,6 +531,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
                 const int cls = ok ? (int)(cl & 0xffff) : 0;
                 const uint8_t c0 = (cl >> 16) & 0xff, c1 = cl >> 24;
                 const uint32_t flags = ok ? (uint32_t)w2.z : 0u;
+                const uint32_t rb = ok ? (uint32_t)sRm[b0][q] : 0u;   // removal bits of the task
                 const bool head = flags & 1u;
                 U[i] = node;
                 const bool old0 = p0 < prev_r0, old1 = p1 < prev_r0;
@@ -542,7 +549,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
 #pragma unroll
                 for (int j = 0; j < VPL; j++) {
                     const uint32_t bit = vsh + j;
-                    const bool rmv = (D.rmw[i] >> bit) & 1u;
+                    const bool rmv = (rb >> (o0 + j)) & 1u;
                     int64_t X = 0;
                     if (any0) {
                         const int64_t g0g = UNI ? (int64_t)(uint32_t)w2.w : D.g0gap[i];
@@ -727,6 +734,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         {
             u32x4 *dst = reinterpret_cast<u32x4 *>(sRec[b2]);
             if (tid < nxt_w) dst[tid] = nx0;
+            if (tid < nxt_w / 3) sRm[b2][tid] = nrm;
             if (PF > 1 && tid + kNT < nxt_w) dst[tid + kNT] = nx1;
             if (PF > 2 && tid + 2 * kNT < nxt_w) dst[tid + 2 * kNT] = nx2;
         }
@@ -741,6 +749,41 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
     if (PS > 1 && wv + 8 < VS) atomicMax(&sMs[wv + 8], (unsigned long long)msS1);
     __syncthreads();
     if (tid < VS && v0 + tid < a.V) a.makespan[v0 + tid] = (int64_t)sMs[tid];
+}
+
+// Removal bits per schedule position for each workgroup's VS variants:
+// rmp[g][q] = bits g*VS .. g*VS+VS-1 of task pos_node[q]'s removal row.
+// A block transposes a tile of 64 positions x 64 words through LDS, so both
+// the row reads and the per-workgroup writes are contiguous.
+template <int VS, typename RmT>
+__global__ __launch_bounds__(256) void k_rm_pos(int64_t n, int32_t W, int32_t nwg,
+                                                const int32_t *__restrict__ pos_node,
+                                                const uint32_t *__restrict__ rm,
+                                                RmT *__restrict__ rmp) {
+    __shared__ uint32_t tile[64][65];
+    const int64_t q0 = (int64_t)blockIdx.x * 64;
+    const int w0 = blockIdx.y * 64;
+    for (int i = threadIdx.x; i < 64 * 64; i += 256) {
+        const int pl = i >> 6, wl = i & 63;
+        const int64_t q = q0 + pl;
+        const int w = w0 + wl;
+        uint32_t v = 0;
+        if (q < n && w < W) v = rm[(int64_t)pos_node[q] * W + w];
+        tile[pl][wl] = v;
+    }
+    __syncthreads();
+    const int g0 = (int)((int64_t)w0 * 32 / VS);
+    int64_t g1 = (int64_t)(w0 + 64) * 32 / VS;
+    if (g1 > nwg) g1 = nwg;
+    constexpr uint32_t mask = VS >= 32 ? ~0u : ((1u << VS) - 1u);
+    for (int64_t i = threadIdx.x; i < (g1 - g0) * 64; i += 256) {
+        const int g = g0 + (int)(i >> 6);
+        const int pl = (int)(i & 63);
+        const int64_t q = q0 + pl;
+        if (q >= n) continue;
+        const int bitpos = g * VS;
+        rmp[(int64_t)g * n + q] = (RmT)((tile[pl][bitpos / 32 - w0] >> (bitpos % 32)) & mask);
+    }
 }
 
 __global__ __launch_bounds__(256) void k_round_count(int64_t nsteps, const int32_t *__restrict__ step_ptr,
@@ -775,22 +818,33 @@ hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants
     constexpr int RP = (kNT / LPS) * K;
     const int64_t ns = sch->n_steps;
     const int64_t max_rounds = ns + (sch->n + RP - 1) / RP + 1;
+    typedef typename std::conditional<(VS <= 8), uint8_t, uint16_t>::type RmT;
+    const int grid = (var->V + VS - 1) / VS;
     int64_t *cnt = nullptr, *dummy = nullptr;
     int32_t *r0 = nullptr, *rn = nullptr;
+    RmT *rmp = nullptr;
     hipError_t e = dalloc_n(&cnt, (size_t)ns + 2, s);
+    if (e == hipSuccess) e = dalloc_n(&rmp, (size_t)grid * (size_t)(sch->n > 0 ? sch->n : 1), s);
     if (e == hipSuccess) e = dalloc_n(&r0, (size_t)max_rounds, s);
     if (e == hipSuccess) e = dalloc_n(&rn, (size_t)max_rounds, s);
     if (e == hipSuccess) e = dalloc_n(&dummy, 2 * kNT, s);
-    if (e != hipSuccess) { dfree(cnt, s); dfree(r0, s); dfree(rn, s); dfree(dummy, s); return e; }
+    if (e != hipSuccess) {
+        dfree(cnt, s); dfree(r0, s); dfree(rn, s); dfree(dummy, s); dfree(rmp, s);
+        return e;
+    }
+    if (sch->n > 0) {
+        const dim3 tg((unsigned)((sch->n + 63) / 64), (unsigned)((var->W + 63) / 64));
+        k_rm_pos<VS, RmT><<<tg, 256, 0, s>>>(sch->n, var->W, grid, sch->pos_node, var->rm_bits, rmp);
+    }
     if (ns > 0) k_round_count<<<grid_for(ns, 256), 256, 0, s>>>(ns, sch->step_ptr, RP, cnt);
     e = scan_exclusive(cnt, cnt, ns, s);
     if (e == hipSuccess && ns > 0)
         k_round_fill<<<grid_for(ns, 256), 256, 0, s>>>(ns, sch->step_ptr, cnt, RP, r0, rn);
     const uint64_t cls_mask = sch->mask & g->cross_mask;
     PipeArgs args{sch->gat_ptr, sch->gat_src, sch->gat_spos, sch->gat_cls, sch->gat_gap, g->gap,
-                  var->table, var->n_cls, var->rm_bits, var->edge_on, cls_mask,
-                  sch->thread_carry ? 1 : 0, var->V, var->W, finish, start, makespan, dummy};
-    const int grid = (var->V + VS - 1) / VS;
+                  var->table, var->n_cls, var->rm_bits, rmp, (int64_t)sch->n, var->edge_on,
+                  cls_mask, sch->thread_carry ? 1 : 0, var->V, var->W, finish, start, makespan,
+                  dummy};
     const int64_t *nrp = cnt + ns;
     const bool tl = (int64_t)var->n_cls * VS <= kTabLds;
     // uniform: every gather class on in every variant, shift-only scales,
@@ -807,7 +861,7 @@ hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants
         else launch_one<LPS, VPL, K, false, false, false>(grid, s, r0, rn, nrp, rc, args);
         e = hipGetLastError();
     }
-    dfree(cnt, s); dfree(r0, s); dfree(rn, s); dfree(dummy, s);
+    dfree(cnt, s); dfree(r0, s); dfree(rn, s); dfree(dummy, s); dfree(rmp, s);
     return e;
 }
 

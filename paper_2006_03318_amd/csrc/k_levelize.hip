@@ -282,10 +282,8 @@ struct WinArgs {
     const int64_t *req_ptr;             // [C+1]
     const int32_t *req_chain;
     const int64_t *req_gpos;
-    int64_t *seg_start, *seg_len;       // [n]
-    int32_t *seg_step;                  // [n]
-    int64_t *step_seg;                  // [n+1]
-    int64_t *result;                    // [0] steps, [1] segments
+    int32_t *ftab;                      // [(n+1) x T] fronts at the start of each round
+    int64_t *result;                    // [0] steps
     uint32_t *err;
 };
 
@@ -301,32 +299,41 @@ __device__ __forceinline__ bool win_blocked(const WinArgs &a, const CandEnt &e, 
     return false;
 }
 
+// One barrier per round: round r reads the fronts of buffer r & 1 and writes
+// the advanced fronts, plus one flag per thread (advanced, unfinished), into
+// buffer (r + 1) & 1; a buffer is rewritten only two rounds later, after the
+// next barrier.  The fronts of every round go to a table from which the
+// segments are cut afterwards (k_win_seg_*).
 __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
+    static_assert(kWG / 64 >= kWinT, "a wave per graph thread");
     __shared__ CandEnt s_win[kWinEnt + 64];
-    __shared__ int32_t s_front[kWinT], s_nfront[kWinT], s_end[kWinT];
-    __shared__ int32_t s_ci[kWinT], s_nci[kWinT], s_ce[kWinT], s_wend[kWinT];
-    __shared__ int s_stop;
+    __shared__ int32_t s_front[2][kWinT];
+    __shared__ __align__(16) uint8_t s_adv[2][16], s_unf[2][16];   // flags of graph threads
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    const int nw = blockDim.x >> 6;               // waves; wave w takes threads w, w + nw, ...
+    const int t = threadIdx.x >> 6;               // wave t walks graph thread t
     const int W = 1 << a.wlog;
-    if (threadIdx.x < a.T) {
-        const int u = threadIdx.x;
-        s_front[u] = (int32_t)a.base[u];
-        s_end[u] = (int32_t)a.base[u + 1];
-        s_ci[u] = (int32_t)a.cbase[u];
-        s_ce[u] = (int32_t)a.cbase[u + 1];
-        s_wend[u] = (int32_t)a.cbase[u];
+    const int T = a.T;
+    const bool mine = t < T;
+    CandEnt *const win = s_win + (mine ? t : 0) * W;
+    // the wave's own thread: front end, candidate range and window in registers
+    const int end = mine ? (int)a.base[t + 1] : 0;
+    const int ce = mine ? (int)a.cbase[t + 1] : 0;
+    int ci = mine ? (int)a.cbase[t] : 0;
+    int wend = ci;
+    if (threadIdx.x < 32) reinterpret_cast<uint8_t *>(s_adv)[threadIdx.x] = 0;
+    if (threadIdx.x < 32) reinterpret_cast<uint8_t *>(s_unf)[threadIdx.x] = 0;
+    if (threadIdx.x < T) {
+        s_front[0][threadIdx.x] = (int32_t)a.base[threadIdx.x];
+        a.ftab[threadIdx.x] = (int32_t)a.base[threadIdx.x];
     }
-    if (threadIdx.x == 0) s_stop = 0;
     __syncthreads();
-    int64_t nseg = 0, round = 0;
+    int64_t round = 0;
     for (;;) {
+        const int cur = (int)(round & 1);
+        const int32_t *front = s_front[cur];
         // refill this thread's window when less than half of it lies ahead:
         // all loads of a refill are in flight together (one memory latency)
-        for (int t = wave; t < a.T; t += nw) {
-            CandEnt *win = s_win + t * W;
-            const int ci = s_ci[t], ce = s_ce[t], wend = s_wend[t];
+        if (mine) {
             if (wend < ce && wend - ci < (W >> 1)) {
                 const int nend = ci + W < ce ? ci + W : ce;
                 const int from = wend > ci ? wend : ci;     // entries behind ci are spent
@@ -344,14 +351,12 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
                         *dst = v[r];
                     }
                 }
-                if (lane == 0) s_wend[t] = nend;
+                wend = nend;
             }
         }
         // A: advance each thread's front past its ready candidates
-        for (int t = wave; t < a.T; t += nw) {
-            CandEnt *win = s_win + t * W;
-            const int f = s_front[t], end = s_end[t], ce = s_ce[t], wend = s_wend[t];
-            int ci = s_ci[t];
+        if (mine) {
+            const int f = front[t];
             int cnew = ce;
             if (f < end) {
                 for (;;) {
@@ -365,7 +370,7 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
                         for (int r = 0; r < kNear; r++) {
                             const int j = ci + r * 64 + lane;
                             const CandEnt e = win[j & (W - 1)];
-                            bl[r] = j < lim && win_blocked(a, e, j, s_front);
+                            bl[r] = j < lim && win_blocked(a, e, j, front);
                         }
                         bool hit = false;
 #pragma unroll
@@ -388,7 +393,7 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
 #pragma unroll
                         for (int r = 0; r < kFar; r++) {
                             const int j = ci + r * 64 + lane;
-                            const bool b = j < ce && win_blocked(a, e[r], j, s_front);
+                            const bool b = j < ce && win_blocked(a, e[r], j, front);
                             const unsigned long long bal = __ballot(b);
                             if (bal && !hit) { cnew = ci + r * 64 + __ffsll((long long)bal) - 1; hit = true; }
                         }
@@ -400,46 +405,58 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
                 cnew = ci;
             }
             if (lane == 0) {
-                s_nci[t] = cnew;
-                s_nfront[t] = f >= end ? f
-                              : (cnew < ce ? (cnew < wend ? win[cnew & (W - 1)].pos : a.pent[cnew].pos)
-                                           : end);
+                const int nf = f >= end ? f
+                               : (cnew < ce ? (cnew < wend ? win[cnew & (W - 1)].pos : a.pent[cnew].pos)
+                                            : end);
+                s_front[cur ^ 1][t] = nf;
+                s_adv[cur][t] = nf > f;
+                s_unf[cur][t] = f < end;
+                a.ftab[(round + 1) * T + t] = nf;
             }
+            ci = cnew;
         }
         __syncthreads();
-        // C + D (wave 0): emit one segment per advanced thread, move the fronts
-        if (wave == 0) {
-            int len = 0, unfinished = 0;
-            if (lane < a.T) {
-                len = s_nfront[lane] - s_front[lane];
-                unfinished = s_front[lane] < s_end[lane];
-            }
-            const unsigned long long adv = __ballot(len > 0);
-            const bool any_left = __ballot(unfinished) != 0;
-            if (!any_left) {
-                if (lane == 0) s_stop = 1;
-            } else if (adv == 0) {
-                if (lane == 0) { s_stop = 1; atomicOr(a.err, ERR_KAHN_CYCLE); }
-            } else {
-                if (len > 0) {
-                    const int64_t sidx = nseg + __popcll(adv & ((1ull << lane) - 1));
-                    a.seg_start[sidx] = s_front[lane];
-                    a.seg_len[sidx] = len;
-                    a.seg_step[sidx] = (int32_t)round;
-                }
-                if (lane == 0) a.step_seg[round] = nseg;
-                if (lane < a.T) { s_front[lane] = s_nfront[lane]; s_ci[lane] = s_nci[lane]; }
-                nseg += __popcll(adv);
-                round++;
-            }
+        // every wave reads the same flags: all threads done, or a stall (cycle)
+        const uint4 uf = *reinterpret_cast<const uint4 *>(s_unf[cur]);
+        const uint4 av = *reinterpret_cast<const uint4 *>(s_adv[cur]);
+        const bool unf = (uf.x | uf.y | uf.z | uf.w) != 0;
+        const bool adv = (av.x | av.y | av.z | av.w) != 0;
+        if (!unf) break;
+        if (!adv) {
+            if (threadIdx.x == 0) atomicOr(a.err, ERR_KAHN_CYCLE);
+            break;
         }
-        __syncthreads();
-        if (s_stop) break;
+        round++;
     }
-    if (threadIdx.x == 0) {
-        a.step_seg[round] = nseg;
-        a.result[0] = round;
-        a.result[1] = nseg;
+    if (threadIdx.x == 0) a.result[0] = round;
+}
+
+// segments from the front table: thread t advanced in round r when its front
+// moved; segments are numbered in (round, thread) order
+__global__ __launch_bounds__(kBS) void k_win_seg_count(int64_t R, int32_t T,
+                                                       const int32_t *__restrict__ ftab,
+                                                       int64_t *__restrict__ cnt) {
+    const int64_t i = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (i < R * T) cnt[i] = ftab[i + T] > ftab[i];
+}
+
+__global__ __launch_bounds__(kBS) void k_win_seg_fill(int64_t R, int32_t T,
+                                                      const int32_t *__restrict__ ftab,
+                                                      const int64_t *__restrict__ off,
+                                                      int64_t *__restrict__ seg_start,
+                                                      int64_t *__restrict__ seg_len,
+                                                      int32_t *__restrict__ seg_step,
+                                                      int64_t *__restrict__ step_seg) {
+    const int64_t i = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (i > R * T) return;
+    if (i % T == 0) step_seg[i / T] = off[i];          // i == R*T gives the total
+    if (i == R * T) return;
+    const int32_t f0 = ftab[i], f1 = ftab[i + T];
+    if (f1 > f0) {
+        const int64_t sidx = off[i];
+        seg_start[sidx] = f0;
+        seg_len[sidx] = f1 - f0;
+        seg_step[sidx] = (int32_t)(i / T);
     }
 }
 
@@ -710,6 +727,8 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
             *gcnt = nullptr, *lvl_cnt = nullptr;
     int32_t *req_chain = nullptr, *long_list = nullptr, *seg_step = nullptr, *level = nullptr;
     CandEnt *pent = nullptr;
+    int32_t *ftab = nullptr;
+    int64_t *seg_cnt = nullptr;
     const bool windowed = T <= kWinT;
     uint32_t *err = nullptr;
     unsigned long long *wmax = nullptr;
@@ -771,8 +790,9 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
     if (windowed) {
         int wlog = 6;                                  // 2^wlog entries per thread
         while ((int64_t)T << (wlog + 1) <= kWinEnt) wlog++;
+        CK(dalloc_n(&ftab, (size_t)(n + 2) * T, s));
         WinArgs wa{T, wlog, g->thread_base, cbase, pent, req_ptr, req_chain, req_gpos,
-                   seg_start, seg_len, seg_step, step_seg, result, err};
+                   ftab, result, err};
         k_kahn_win<<<1, kWG, 0, s>>>(wa);
         CK(hipGetLastError());
     } else {
@@ -790,6 +810,20 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
                                "(Kahn rounds stalled after %lld steps)", (long long)h_res[0]);
         st = DD_ECYCLE;
         goto done;
+    }
+    if (windowed) {                                    // cut the segments from the fronts
+        const int64_t R = h_res[0], RT = R * T;
+        CK(dalloc_n(&seg_cnt, (size_t)RT + 1, s));
+        if (RT > 0) {
+            k_win_seg_count<<<grid_for(RT, kBS), kBS, 0, s>>>(R, T, ftab, seg_cnt);
+            CK(hipGetLastError());
+        }
+        CK(scan_exclusive(seg_cnt, seg_cnt, RT, s));
+        k_win_seg_fill<<<grid_for(RT + 1, kBS), kBS, 0, s>>>(R, T, ftab, seg_cnt, seg_start,
+                                                             seg_len, seg_step, step_seg);
+        CK(hipGetLastError());
+        CK(hipMemcpyAsync(&h_res[1], seg_cnt + RT, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+        CK(hipStreamSynchronize(s));
     }
     {
         const int64_t nph = h_res[0], nseg = h_res[1];
@@ -908,6 +942,7 @@ done:
     dfree(nfront, s); dfree(nci, s); dfree(long_list, s); dfree(seg_start, s);
     dfree(seg_len, s); dfree(seg_off, s); dfree(seg_step, s); dfree(step_seg, s);
     dfree(gcnt, s); dfree(lvl_cnt, s); dfree(level, s); dfree(pent, s);
+    dfree(ftab, s); dfree(seg_cnt, s);
     return st;
 }
 

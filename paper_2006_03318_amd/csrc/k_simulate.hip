@@ -71,10 +71,11 @@ struct PipeArgs {
     int32_t thread_carry;         // previous task of a run comes from LDS carries
     int32_t V, W;
     int64_t *finish, *start, *makespan;
-    int64_t *dummy;               // [2 * kNT] target of stores from idle lanes
+    int64_t *dummy;               // [2 * threads] target of stores from idle lanes
 };
 
-constexpr int kTabLds = 4096;     // scale entries kept in LDS (8 B each)
+constexpr int kTabLds = 4096;     // scale entries kept in LDS at most (8 B each)
+constexpr size_t kLdsBytes = 160 * 1024;   // LDS of one compute unit (gfx950)
 constexpr int kSmall = 64;        // rounds of at most this many positions: one wave per variant
 typedef __attribute__((address_space(1))) int64_t gi64;   // global-memory int64
 
@@ -163,26 +164,27 @@ __device__ __forceinline__ void wave_scan(int64_t &a, int64_t &b, int &h) {
 // schedule's gathers use, every scale is a power of two and every duration
 // and gap is below 2^32 (one 32x32 multiply and a shift per scaled
 // duration; a gather source's gap comes from the record).
-template <int LPS, int VPL, int K, bool TLDS, bool START, bool UNI>
-__global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ round_r0,
+template <int LPS, int VPL, int K, bool TLDS, bool START, bool UNI, int NT>
+__global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ round_r0,
                                                   const int32_t *__restrict__ round_rn,
                                                   const int64_t *__restrict__ n_rounds,
                                                   const Rec *__restrict__ rec, PipeArgs a) {
     constexpr int VS = LPS * VPL;
-    constexpr int NS = kNT / LPS;
+    constexpr int NS = NT / LPS;
     constexpr int RP = NS * K;
-    constexpr int NE = NS * VS;           // slot summaries (= kNT * VPL)
+    constexpr int NE = NS * VS;           // slot summaries (= NT * VPL)
     constexpr int RW = RP * 3;            // 16-byte words of one ring buffer
-    constexpr int PF = (RW + kNT - 1) / kNT;
+    constexpr int PF = (RW + NT - 1) / NT;
     static_assert(sizeof(Rec) == 48, "record layout");
-    static_assert(RP <= kNT, "positions per round");
+    static_assert(RP <= NT, "positions per round");
     static_assert(PF <= 3, "record prefetch words per lane");
-    static_assert(NE / 64 <= 16, "chunk totals");
+    constexpr int NCH = NE / 64 > 0 ? NE / 64 : 1;   // 64-entry chunks of summaries
     static_assert(!UNI || TLDS, "uniform path keeps the table in LDS");
     // small rounds (at most 64 positions): wave w alone handles variants
-    // w, w + 8, ... for every position of the round (one per lane), so the
+    // w, w + NW, ... for every position of the round (one per lane), so the
     // round needs no slot scan across waves and only the ring barrier
-    constexpr int PS = (VS + 7) / 8;      // variants per wave in a small round
+    constexpr int NW = NT / 64;           // waves per workgroup
+    constexpr int PS = (VS + NW - 1) / NW;  // variants per wave in a small round
     static_assert(PS <= K && PS <= 2, "load slots for small rounds");
     // records of rounds k, k+1 (read) and k+2 (being filled): a ring of three;
     // beside them the removal bits of the workgroup's variants per position
@@ -193,9 +195,9 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
     __shared__ int64_t sR[RP * VS];
     __shared__ int64_t sA[NE], sB[NE];
     __shared__ uint8_t sH[NE];
-    __shared__ int64_t sTA[16], sTB[16];
-    __shared__ uint8_t sTH[16];
-    __shared__ uint64_t sT[TLDS ? kTabLds : 1];
+    __shared__ int64_t sTA[NCH], sTB[NCH];
+    __shared__ uint8_t sTH[NCH];
+    extern __shared__ uint64_t sT[];      // scale table (n_cls x VS), sized at launch
     __shared__ int64_t sTC[kMaxCarryThreads * VS];
     __shared__ unsigned long long sMs[VS];
     __shared__ int64_t sCarry[VS];        // release at the end of a big round
@@ -230,12 +232,12 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
     if (tid == 0) sFlags = 0;
     {   // the record ring starts zeroed (no stale fields past a round's end)
         uint4 *z = &sRec[0][0];
-        for (int i = tid; i < 3 * RW; i += kNT) z[i] = make_uint4(0u, 0u, 0u, 0u);
+        for (int i = tid; i < 3 * RW; i += NT) z[i] = make_uint4(0u, 0u, 0u, 0u);
     }
     __syncthreads();
     bool any_magic = false;
     if (TLDS) {
-        for (int i = tid; i < a.n_cls * VS; i += kNT) {
+        for (int i = tid; i < a.n_cls * VS; i += NT) {
             const int c = i / VS, o = i % VS;
             const int vx = v0 + o < a.V ? v0 + o : 0;
             const ScaleEntry e = a.table[(int64_t)c * V + vx];
@@ -244,7 +246,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
             sT[i] = (uint64_t)e.p | ((uint64_t)(e.shift & 0xff) << 32) | (mg ? (1ull << 40) : 0ull);
         }
     }
-    for (int i = tid; i < kMaxCarryThreads * VS; i += kNT) sTC[i] = 0;
+    for (int i = tid; i < kMaxCarryThreads * VS; i += NT) sTC[i] = 0;
     if (tid < VS) {
         sMs[tid] = 0;
         // per-variant values read inside the loop live in LDS: a register
@@ -256,8 +258,8 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         if (rr < nr) {
             const int r0 = round_r0[rr], rn = round_rn[rr];
             const uint4 *src = reinterpret_cast<const uint4 *>(rec + r0);
-            for (int i = tid; i < rn * 3; i += kNT) sRec[rr][i] = src[i];
-            for (int i = tid; i < rn; i += kNT) sRm[rr][i] = rmrow[r0 + i];
+            for (int i = tid; i < rn * 3; i += NT) sRec[rr][i] = src[i];
+            for (int i = tid; i < rn; i += NT) sRm[rr][i] = rmrow[r0 + i];
         }
     }
     __syncthreads();
@@ -294,7 +296,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
             (void)p1;
 #pragma unroll
             for (int jj = 0; jj < K; jj++) {
-                const int os = wv + 8 * jj;
+                const int os = wv + NW * jj;
                 const bool vv = jj < PS && os < VS && v0 + os < a.V;
                 const int64_t vs_ = vv ? v0 + os : 0;
                 const int64_t vwj = vs_ >> 5;
@@ -354,7 +356,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
     }
 
     typename I64V<VPL>::T carry = 0, ms = 0;
-    int64_t msS0 = 0, msS1 = 0;               // small rounds: variants w and w + 8
+    int64_t msS0 = 0, msS1 = 0;               // small rounds: variants w and w + NW
     int prev_r0 = 0;
     int b0 = 0, b1 = 1, b2 = 2;               // ring buffers of rounds k, k+1, k+2
     for (int64_t k = 0; k < nr; k++) {
@@ -377,8 +379,8 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         u32x4 nx0, nx1, nx2;
         nx0 = nsrc[tid < nxt_w ? tid : 0];
         const RmT nrm = rmrow[round_r0[k2] + (tid < nxt_w / 3 ? tid : 0)];
-        if (PF > 1) nx1 = nsrc[tid + kNT < nxt_w ? tid + kNT : 0];
-        if (PF > 2) nx2 = nsrc[tid + 2 * kNT < nxt_w ? tid + 2 * kNT : 0];
+        if (PF > 1) nx1 = nsrc[tid + NT < nxt_w ? tid + NT : 0];
+        if (PF > 2) nx2 = nsrc[tid + 2 * NT < nxt_w ? tid + 2 * NT : 0];
 
         if (rn <= kSmall) {
             // ---- small round: one position per lane, variants per wave ----
@@ -408,7 +410,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
             const int tcx = ((flags >> 2) & 63u) * VS;
 #pragma unroll
             for (int jj = 0; jj < K; jj++) {
-                const int os = wv + 8 * jj;
+                const int os = wv + NW * jj;
                 const bool vw_ok = jj < PS && os < VS && v0 + os < a.V;   // wave-uniform
                 const int64_t vs_ = vw_ok ? v0 + os : 0;
                 int64_t F = 0, S = 0;
@@ -647,7 +649,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         bool cact[VPL];
 #pragma unroll
         for (int j = 0; j < VPL; j++) {
-            const int e = tid + j * kNT;
+            const int e = tid + j * NT;
             cact[j] = __any((e % NS) <= ls);
             xa[j] = 0; xb[j] = 0; xh[j] = 1;
             if (cact[j]) {
@@ -658,13 +660,13 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         if (NS > 64) {
 #pragma unroll
             for (int j = 0; j < VPL; j++) {
-                const int e = tid + j * kNT;
+                const int e = tid + j * NT;
                 if (lane == 63) { sTA[e >> 6] = xa[j]; sTB[e >> 6] = xb[j]; sTH[e >> 6] = (uint8_t)xh[j]; }
             }
             __syncthreads();
 #pragma unroll
             for (int j = 0; j < VPL; j++) {
-                const int e = tid + j * kNT;
+                const int e = tid + j * NT;
                 const int chunk = (e % NS) >> 6;
                 const int first = (e / NS) * (NS >> 6);
                 if (cact[j] && chunk > 0 && !xh[j]) {
@@ -682,7 +684,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
         }
 #pragma unroll
         for (int j = 0; j < VPL; j++)
-            if (cact[j]) sB[tid + j * kNT] = xb[j];
+            if (cact[j]) sB[tid + j * NT] = xb[j];
         __syncthreads();                                     // B2
         // finalize: carry-in, results, stores, releases for the next round
 #pragma unroll
@@ -735,8 +737,8 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
             u32x4 *dst = reinterpret_cast<u32x4 *>(sRec[b2]);
             if (tid < nxt_w) dst[tid] = nx0;
             if (tid < nxt_w / 3) sRm[b2][tid] = nrm;
-            if (PF > 1 && tid + kNT < nxt_w) dst[tid + kNT] = nx1;
-            if (PF > 2 && tid + 2 * kNT < nxt_w) dst[tid + 2 * kNT] = nx2;
+            if (PF > 1 && tid + NT < nxt_w) dst[tid + NT] = nx1;
+            if (PF > 2 && tid + 2 * NT < nxt_w) dst[tid + 2 * NT] = nx2;
         }
         prev_r0 = r0;
         D = DN;
@@ -746,7 +748,7 @@ __global__ __launch_bounds__(kNT) void k_sim_pipe(const int32_t *__restrict__ ro
 #pragma unroll
     for (int j = 0; j < VPL; j++) atomicMax(&sMs[o0 + j], (unsigned long long)ms[j]);
     if (wv < VS) atomicMax(&sMs[wv], (unsigned long long)msS0);
-    if (PS > 1 && wv + 8 < VS) atomicMax(&sMs[wv + 8], (unsigned long long)msS1);
+    if (PS > 1 && wv + NW < VS) atomicMax(&sMs[wv + NW], (unsigned long long)msS1);
     __syncthreads();
     if (tid < VS && v0 + tid < a.V) a.makespan[v0 + tid] = (int64_t)sMs[tid];
 }
@@ -805,17 +807,30 @@ __global__ __launch_bounds__(256) void k_round_fill(int64_t nsteps, const int32_
     }
 }
 
-template <int LPS, int VPL, int K, bool TLDS, bool START, bool UNI>
+template <int LPS, int VPL, int K, bool TLDS, bool START, bool UNI, int NT>
 void launch_one(int grid, hipStream_t s, const int32_t *r0, const int32_t *rn,
                 const int64_t *nrp, const Rec *rec, const PipeArgs &args) {
-    k_sim_pipe<LPS, VPL, K, TLDS, START, UNI><<<grid, kNT, 0, s>>>(r0, rn, nrp, rec, args);
+    const size_t dyn = TLDS ? (size_t)args.n_cls * LPS * VPL * sizeof(uint64_t) : 0;
+    k_sim_pipe<LPS, VPL, K, TLDS, START, UNI, NT><<<grid, NT, dyn, s>>>(r0, rn, nrp, rec, args);
 }
 
-template <int LPS, int VPL, int K>
+// LDS of one workgroup: the kernel's static arrays plus the scale table
+template <int LPS, int VPL, int K, int NT>
+bool table_fits(int32_t n_cls) {
+    constexpr int VS = LPS * VPL;
+    if ((int64_t)n_cls * VS > kTabLds) return false;
+    hipFuncAttributes at{};
+    if (hipFuncGetAttributes(&at, reinterpret_cast<const void *>(
+                                      &k_sim_pipe<LPS, VPL, K, true, false, false, NT>)) != hipSuccess)
+        return false;
+    return at.sharedSizeBytes + (size_t)n_cls * VS * sizeof(uint64_t) <= kLdsBytes;
+}
+
+template <int LPS, int VPL, int K, int NT = kNT>
 hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants *var,
                        int64_t *finish, int64_t *start, int64_t *makespan, hipStream_t s) {
     constexpr int VS = LPS * VPL;
-    constexpr int RP = (kNT / LPS) * K;
+    constexpr int RP = (NT / LPS) * K;
     const int64_t ns = sch->n_steps;
     const int64_t max_rounds = ns + (sch->n + RP - 1) / RP + 1;
     typedef typename std::conditional<(VS <= 8), uint8_t, uint16_t>::type RmT;
@@ -827,7 +842,7 @@ hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants
     if (e == hipSuccess) e = dalloc_n(&rmp, (size_t)grid * (size_t)(sch->n > 0 ? sch->n : 1), s);
     if (e == hipSuccess) e = dalloc_n(&r0, (size_t)max_rounds, s);
     if (e == hipSuccess) e = dalloc_n(&rn, (size_t)max_rounds, s);
-    if (e == hipSuccess) e = dalloc_n(&dummy, 2 * kNT, s);
+    if (e == hipSuccess) e = dalloc_n(&dummy, 2 * NT, s);
     if (e != hipSuccess) {
         dfree(cnt, s); dfree(r0, s); dfree(rn, s); dfree(dummy, s); dfree(rmp, s);
         return e;
@@ -846,19 +861,19 @@ hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants
                   cls_mask, sch->thread_carry ? 1 : 0, var->V, var->W, finish, start, makespan,
                   dummy};
     const int64_t *nrp = cnt + ns;
-    const bool tl = (int64_t)var->n_cls * VS <= kTabLds;
+    const bool tl = table_fits<LPS, VPL, K, NT>(var->n_cls);
     // uniform: every gather class on in every variant, shift-only scales,
     // durations and gaps below 2^32 (a source's gap then rides in its record)
     const bool uni = tl && (var->all_mask & cls_mask) == cls_mask && !var->any_magic &&
                      g->dmax < (int64_t(1) << 32) && g->gmax < (int64_t(1) << 32);
     const Rec *rc = sch->rec;
     if (e == hipSuccess) {
-        if (uni && start) launch_one<LPS, VPL, K, true, true, true>(grid, s, r0, rn, nrp, rc, args);
-        else if (uni) launch_one<LPS, VPL, K, true, false, true>(grid, s, r0, rn, nrp, rc, args);
-        else if (tl && start) launch_one<LPS, VPL, K, true, true, false>(grid, s, r0, rn, nrp, rc, args);
-        else if (tl) launch_one<LPS, VPL, K, true, false, false>(grid, s, r0, rn, nrp, rc, args);
-        else if (start) launch_one<LPS, VPL, K, false, true, false>(grid, s, r0, rn, nrp, rc, args);
-        else launch_one<LPS, VPL, K, false, false, false>(grid, s, r0, rn, nrp, rc, args);
+        if (uni && start) launch_one<LPS, VPL, K, true, true, true, NT>(grid, s, r0, rn, nrp, rc, args);
+        else if (uni) launch_one<LPS, VPL, K, true, false, true, NT>(grid, s, r0, rn, nrp, rc, args);
+        else if (tl && start) launch_one<LPS, VPL, K, true, true, false, NT>(grid, s, r0, rn, nrp, rc, args);
+        else if (tl) launch_one<LPS, VPL, K, true, false, false, NT>(grid, s, r0, rn, nrp, rc, args);
+        else if (start) launch_one<LPS, VPL, K, false, true, false, NT>(grid, s, r0, rn, nrp, rc, args);
+        else launch_one<LPS, VPL, K, false, false, false, NT>(grid, s, r0, rn, nrp, rc, args);
         e = hipGetLastError();
     }
     dfree(cnt, s); dfree(r0, s); dfree(rn, s); dfree(dummy, s); dfree(rmp, s);

@@ -140,6 +140,12 @@ __device__ __forceinline__ void scan_step(int64_t &a, int64_t &b, int &h) {
     }
 }
 
+__device__ __forceinline__ int64_t readlane64(int64_t x, int l) {
+    const int lo = __builtin_amdgcn_readlane((int)(uint32_t)x, l);
+    const int hi = __builtin_amdgcn_readlane((int)((uint64_t)x >> 32), l);
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
 // inclusive segmented scan over the 64 lanes of a wave
 __device__ __forceinline__ void wave_scan(int64_t &a, int64_t &b, int &h) {
     scan_step<0x111, 0xf>(a, b, h);   // row_shr:1
@@ -647,17 +653,41 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         int64_t xa[VPL], xb[VPL];
         int xh[VPL];
         bool cact[VPL];
+        if (NS <= 64 * VPL) {
+            // a wave scans whole variants (its VPL chunks hold them): the
+            // chunks of one variant follow each other in the same wave
+            int64_t pa = 0, pb = 0;
+            int ph = 1;
 #pragma unroll
-        for (int j = 0; j < VPL; j++) {
-            const int e = tid + j * NT;
-            cact[j] = __any((e % NS) <= ls);
-            xa[j] = 0; xb[j] = 0; xh[j] = 1;
-            if (cact[j]) {
-                xa[j] = sA[e]; xb[j] = sB[e]; xh[j] = sH[e];
-                wave_scan(xa[j], xb[j], xh[j]);
+            for (int j = 0; j < VPL; j++) {
+                const int e = wv * 64 * VPL + j * 64 + lane;
+                cact[j] = __any((e % NS) <= ls);
+                xa[j] = 0; xb[j] = 0; xh[j] = 1;
+                if (cact[j]) {
+                    xa[j] = sA[e]; xb[j] = sB[e]; xh[j] = sH[e];
+                    wave_scan(xa[j], xb[j], xh[j]);
+                    if ((j * 64) % NS != 0 && !xh[j]) {       // continues the last chunk
+                        xb[j] = max64(pb + xa[j], xb[j]);
+                        xa[j] = pa + xa[j];
+                        xh[j] = ph;
+                    }
+                    sB[e] = xb[j];
+                }
+                pa = readlane64(xa[j], 63);
+                pb = readlane64(xb[j], 63);
+                ph = __builtin_amdgcn_readlane(xh[j], 63);
             }
-        }
-        if (NS > 64) {
+        } else {
+#pragma unroll
+            for (int j = 0; j < VPL; j++) {
+                const int e = tid + j * NT;
+                cact[j] = __any((e % NS) <= ls);
+                xa[j] = 0; xb[j] = 0; xh[j] = 1;
+                if (cact[j]) {
+                    xa[j] = sA[e]; xb[j] = sB[e]; xh[j] = sH[e];
+                    wave_scan(xa[j], xb[j], xh[j]);
+                }
+            }
 #pragma unroll
             for (int j = 0; j < VPL; j++) {
                 const int e = tid + j * NT;
@@ -670,21 +700,21 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 const int chunk = (e % NS) >> 6;
                 const int first = (e / NS) * (NS >> 6);
                 if (cact[j] && chunk > 0 && !xh[j]) {
-                    int64_t pa = sTA[first], pb = sTB[first];
-                    int ph = sTH[first];
+                    int64_t qa = sTA[first], qb = sTB[first];
+                    int qh = sTH[first];
                     for (int c = 1; c < chunk; c++) {
                         const int64_t ca = sTA[first + c], cb = sTB[first + c];
                         const int ch = sTH[first + c];
-                        if (!ch) { pb = max64(pb + ca, cb); pa = pa + ca; }
-                        else { pa = ca; pb = cb; ph = ch; }
+                        if (!ch) { qb = max64(qb + ca, cb); qa = qa + ca; }
+                        else { qa = ca; qb = cb; qh = ch; }
                     }
-                    xb[j] = max64(pb + xa[j], xb[j]); xa[j] = pa + xa[j]; xh[j] = ph;
+                    xb[j] = max64(qb + xa[j], xb[j]); xa[j] = qa + xa[j]; xh[j] = qh;
                 }
             }
-        }
 #pragma unroll
-        for (int j = 0; j < VPL; j++)
-            if (cact[j]) sB[tid + j * NT] = xb[j];
+            for (int j = 0; j < VPL; j++)
+                if (cact[j]) sB[tid + j * NT] = xb[j];
+        }
         __syncthreads();                                     // B2
         // finalize: carry-in, results, stores, releases for the next round
 #pragma unroll

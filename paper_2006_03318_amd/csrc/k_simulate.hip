@@ -365,7 +365,13 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
     int64_t msS0 = 0, msS1 = 0;               // small rounds: variants w and w + NW
     int prev_r0 = 0;
     int b0 = 0, b1 = 1, b2 = 2;               // ring buffers of rounds k, k+1, k+2
-    for (int64_t k = 0; k < nr; k++) {
+    // Small and big rounds run as two inner loops rather than one loop with
+    // an if/else: the compiler then sees no path through an iteration that
+    // skips both bodies, so it never makes a round wait for loads of the
+    // previous round, or for its stores, that were in fact consumed already.
+    int64_t k = 0;
+    auto round = [&](auto small_tag) {
+        constexpr bool SMALL_ROUND = decltype(small_tag)::value;
         const int r0 = round_r0[k], rn = round_rn[k];
         const Rec *R = reinterpret_cast<const Rec *>(sRec[b0]);
         uint64_t eon[VPL];
@@ -383,13 +389,36 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         const int nxt_w = k + 2 < nr ? round_rn[k2] * 3 : 0;
         const u32x4 *nsrc = reinterpret_cast<const u32x4 *>(rec + round_r0[k2]);
         u32x4 nx0, nx1, nx2;
-        nx0 = nsrc[tid < nxt_w ? tid : 0];
-        const RmT nrm = rmrow[round_r0[k2] + (tid < nxt_w / 3 ? tid : 0)];
-        if (PF > 1) nx1 = nsrc[tid + NT < nxt_w ? tid + NT : 0];
-        if (PF > 2) nx2 = nsrc[tid + 2 * NT < nxt_w ? tid + 2 * NT : 0];
+        RmT nrm;
+        // issued inside each round's branch, so that no path of the loop
+        // skips both the loads and the write below
+        auto load_next = [&]() {
+            nx0 = nsrc[tid < nxt_w ? tid : 0];
+            nrm = rmrow[round_r0[k2] + (tid < nxt_w / 3 ? tid : 0)];
+            if (PF > 1) nx1 = nsrc[tid + NT < nxt_w ? tid + NT : 0];
+            if (PF > 2) nx2 = nsrc[tid + 2 * NT < nxt_w ? tid + 2 * NT : 0];
+        };
+        // Round k+2 goes into the buffer that round k-1 used (every wave
+        // finished reading it before the previous round's last barrier).  It
+        // is written before this round's result stores: vector memory
+        // operations complete in order, so a later write would also wait for
+        // the stores to land.
+        auto put_next = [&]() {
+            // the loads land here on every path (a lane that skips its write
+            // would otherwise leave them pending into the next round)
+            asm volatile("" ::"v"(nx0), "v"((uint32_t)nrm));
+            if (PF > 1) asm volatile("" ::"v"(nx1));
+            if (PF > 2) asm volatile("" ::"v"(nx2));
+            u32x4 *dst = reinterpret_cast<u32x4 *>(sRec[b2]);
+            if (tid < nxt_w) dst[tid] = nx0;
+            if (tid < nxt_w / 3) sRm[b2][tid] = nrm;
+            if (PF > 1 && tid + NT < nxt_w) dst[tid + NT] = nx1;
+            if (PF > 2 && tid + 2 * NT < nxt_w) dst[tid + 2 * NT] = nx2;
+        };
 
-        if (rn <= kSmall) {
+        if constexpr (SMALL_ROUND) {
             // ---- small round: one position per lane, variants per wave ----
+            load_next();
             Dyn<K, VPL> DNs;
             issue(k1, bN, r0, DNs);
             const int q = lane;
@@ -414,6 +443,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             const bool any1 = __any(has1);
             const uint32_t extra = flags >> 8;
             const int tcx = ((flags >> 2) & 63u) * VS;
+            int64_t Fs[K], Ss[K];
+            bool sts[K];
 #pragma unroll
             for (int jj = 0; jj < K; jj++) {
                 const int os = wv + NW * jj;
@@ -498,29 +529,50 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     }
                     st = ok;
                 }
-                gi64 *o = st ? (gi64 *)(a.finish + ((int64_t)node * V + vs_)) : dummy;
+                Fs[jj] = F;
+                Ss[jj] = S;
+                sts[jj] = st;
+            }
+            put_next();
+#pragma unroll
+            for (int jj = 0; jj < K; jj++) {
+                const int os = wv + NW * jj;
+                const bool vw_ok = jj < PS && os < VS && v0 + os < a.V;
+                const int64_t vs_ = vw_ok ? v0 + os : 0;
+                gi64 *o = sts[jj] ? (gi64 *)(a.finish + ((int64_t)node * V + vs_)) : dummy;
                 asm volatile("" : "+v"(o));  // one store per slot in either layout
-                *o = F;
+                *o = Fs[jj];
                 if (START) {
-                    gi64 *os2 = st ? (gi64 *)(a.start + ((int64_t)node * V + vs_)) : dummy;
+                    gi64 *os2 = sts[jj] ? (gi64 *)(a.start + ((int64_t)node * V + vs_)) : dummy;
                     asm volatile("" : "+v"(os2));
-                    *os2 = S;
+                    *os2 = Ss[jj];
                 }
             }
             DN = DNs;
         } else {
         // ---- big round: slots of consecutive positions across all waves ----
+        load_next();
         const int ke = per_slot(rn);              // positions per slot this round
         const bool wact = __any(slot * ke < rn);  // some position of this wave is live
         // walk: local max-plus recurrence over this slot's K positions
         int64_t Fl[K][VPL], Dp[K][VPL], Dd[K][VPL];
         int32_t U[K];
+        int64_t Gp[K][VPL];                       // gap of each kept task (0 if removed)
+        uint32_t FLk[K];                          // flags (0 past the round's end)
+#pragma unroll
+        for (int i = 0; i < K; i++) {
+            U[i] = 0;
+            FLk[i] = 0;
+#pragma unroll
+            for (int j = 0; j < VPL; j++) Gp[i][j] = 0;
+        }
         int64_t A[VPL], B[VPL];
 #pragma unroll
         for (int j = 0; j < VPL; j++) { A[j] = 0; B[j] = 0; }
-        uint32_t before = 0, rmk[VPL];
+        // nk: positions not kept (removed, or past the round's end)
+        uint32_t before = 0, nk[VPL];
 #pragma unroll
-        for (int j = 0; j < VPL; j++) rmk[j] = 0;
+        for (int j = 0; j < VPL; j++) nk[j] = ~0u;
         bool hh = false;
         if (wact) {
 #pragma unroll
@@ -542,6 +594,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 const uint32_t rb = ok ? (uint32_t)sRm[b0][q] : 0u;   // removal bits of the task
                 const bool head = flags & 1u;
                 U[i] = node;
+                FLk[i] = flags;
                 const bool old0 = p0 < prev_r0, old1 = p1 < prev_r0;
                 int i0 = p0 - prev_r0, i1 = p1 - prev_r0;
                 i0 = i0 < 0 ? 0 : (i0 >= RP ? RP - 1 : i0);
@@ -627,12 +680,14 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     B[j] = F + gp;
                     Fl[i][j] = F;
                     if (START) Dd[i][j] = dp;
-                    if (rmv) rmk[j] |= 1u << i;
+                    Gp[i][j] = gp;
+                    if (live) nk[j] &= ~(1u << i);
                 }
                 hh = hh || head;
                 if (!hh) before |= 1u << i;
             }
         }
+        put_next();
         // slot summaries (variant-major); slot 0 absorbs the carry; slots of
         // idle waves are the identity (0, 0)
 #pragma unroll
@@ -653,7 +708,25 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         int64_t xa[VPL], xb[VPL];
         int xh[VPL];
         bool cact[VPL];
-        if (NS <= 64 * VPL) {
+        if (VPL == 2 && NS == 128) {
+            // wave w scans variant w, lane l its slots 2l and 2l+1: the pair
+            // is composed first, one wave scan covers the 64 pairs, and slot
+            // 2l takes the prefix of the previous pair (lane l-1; slot 0 is
+            // always a segment head, so lane 0 needs none)
+            const int e0 = wv * NS + 2 * lane;
+            const int64_t a0 = sA[e0], a1 = sA[e0 + 1];
+            const int64_t b0 = sB[e0], b1 = sB[e0 + 1];
+            const int h0 = sH[e0], h1 = sH[e0 + 1];
+            int64_t pa = h1 ? a1 : a0 + a1;
+            int64_t pb = h1 ? b1 : max64(b0 + a1, b1);
+            int ph = h0 | h1;
+            wave_scan(pa, pb, ph);
+            const int qlo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)pb, 0x138, 0xf, 0xf, false);   // wave_shr:1
+            const int qhi = __builtin_amdgcn_update_dpp(0, (int)((uint64_t)pb >> 32), 0x138, 0xf, 0xf, false);
+            const int64_t qb = (int64_t)(((uint64_t)(uint32_t)qhi << 32) | (uint32_t)qlo);
+            sB[e0] = h0 ? b0 : max64(qb + a0, b0);
+            sB[e0 + 1] = pb;
+        } else if (NS <= 64 * VPL) {
             // a wave scans whole variants (its VPL chunks hold them): the
             // chunks of one variant follow each other in the same wave
             int64_t pa = 0, pb = 0;
@@ -717,31 +790,36 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         }
         __syncthreads();                                     // B2
         // finalize: carry-in, results, stores, releases for the next round
+        // (the carry-in is read once, before any LDS write of the pass)
+        int64_t cin[VPL];
+#pragma unroll
+        for (int j = 0; j < VPL; j++)
+            cin[j] = slot == 0 ? carry[j] : sB[(o0 + j) * NS + (slot > 0 ? slot - 1 : 0)];
 #pragma unroll
         for (int i = 0; i < K; i++) {
             const int q = slot * ke + i;
             const bool ok = i < ke && q < rn;
-            Vals<VPL> fv, sv;
+            Vals<VPL> fv, sv, rv;
 #pragma unroll
-            for (int j = 0; j < VPL; j++) { fv.x[j] = 0; sv.x[j] = 0; }
+            for (int j = 0; j < VPL; j++) { fv.x[j] = 0; sv.x[j] = 0; rv.x[j] = 0; }
             if (wact) {
-                const int4 w0 = reinterpret_cast<const int4 *>(&R[q])[0];
-                const int64_t gap = ((int64_t)(uint32_t)w0.w << 32) | (uint32_t)w0.z;
-                const uint32_t flags = ok ? R[q].flags : 0u;
+                const uint32_t flags = FLk[i];
                 const bool last = tcar && (flags & 2u);
                 const int tcx = ((flags >> 2) & 63u) * VS + o0;
 #pragma unroll
                 for (int j = 0; j < VPL; j++) {
-                    const int64_t cin = slot == 0 ? carry[j] : sB[(o0 + j) * NS + slot - 1];
-                    const int64_t F = ((before >> i) & 1u) ? max64(cin + Dp[i][j], Fl[i][j]) : Fl[i][j];
-                    const bool rmv = (rmk[j] >> i) & 1u;
-                    const int64_t Rv = F + (rmv ? 0 : gap);
-                    if (ok) sR[q * VS + o0 + j] = Rv;
-                    if (last) sTC[tcx + j] = Rv;
+                    const int64_t F = ((before >> i) & 1u) ? max64(cin[j] + Dp[i][j], Fl[i][j]) : Fl[i][j];
+                    rv.x[j] = F + Gp[i][j];
                     fv.x[j] = F;
                     if (START) sv.x[j] = F - Dd[i][j];
-                    if (ok && lok && !rmv) ms[j] = max64(ms[j], F);
+                    // makespan over kept tasks (lanes past V never publish theirs)
+                    ms[j] = max64(ms[j], ((nk[j] >> i) & 1u) ? 0 : F);
                 }
+                // positions past the round's end write their own unused slot
+                // (no young gather reads it); slots past ke would overlap the
+                // next slot's positions
+                if (i < ke) *reinterpret_cast<Vals<VPL> *>(&sR[q * VS + o0]) = rv;
+                if (__any(last) && last) *reinterpret_cast<Vals<VPL> *>(&sTC[tcx]) = rv;
             }
             const bool st = ok && lok;
             gi64 *o = st ? (gi64 *)(a.finish + ((int64_t)U[i] * V + vf)) : dummy;
@@ -761,19 +839,14 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         }
         DN = DNb;
         }   // big round
-        // round k+2 goes into the buffer that round k-1 used: every wave
-        // finished reading it before the previous round's last barrier
-        {
-            u32x4 *dst = reinterpret_cast<u32x4 *>(sRec[b2]);
-            if (tid < nxt_w) dst[tid] = nx0;
-            if (tid < nxt_w / 3) sRm[b2][tid] = nrm;
-            if (PF > 1 && tid + NT < nxt_w) dst[tid + NT] = nx1;
-            if (PF > 2 && tid + 2 * NT < nxt_w) dst[tid + 2 * NT] = nx2;
-        }
         prev_r0 = r0;
         D = DN;
         const int bt = b0; b0 = b1; b1 = b2; b2 = bt;
         __syncthreads();                                     // B3
+    };
+    while (k < nr) {
+        for (; k < nr && round_rn[k] <= kSmall; k++) round(std::true_type{});
+        for (; k < nr && round_rn[k] > kSmall; k++) round(std::false_type{});
     }
 #pragma unroll
     for (int j = 0; j < VPL; j++) atomicMax(&sMs[o0 + j], (unsigned long long)ms[j]);

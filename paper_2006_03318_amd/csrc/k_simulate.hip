@@ -223,7 +223,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
     if ((nwg & 7) == 0) wg = (blockIdx.x & 7) * (nwg >> 3) + (blockIdx.x >> 3);
     const int v0 = wg * VS;
     const int vf = v0 + lis * VPL;            // first variant of this lane
-    const bool lok = vf < a.V;                // VPL == 2 implies V even: vf + 1 < V too
+    const bool lok = vf < a.V;                // V is a multiple of VPL: vf + VPL - 1 < V too
     const int vvf = lok ? vf : 0;
     const uint32_t vsh = (uint32_t)(vvf & 31);
     const int vw = vvf >> 5;
@@ -426,7 +426,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
             const int4 w0 = r4[0], w1 = r4[1], w2 = r4[2];
             const int64_t dur = ((int64_t)(uint32_t)w0.y << 32) | (uint32_t)w0.x;
-            const int64_t gap = ((int64_t)(uint32_t)w0.w << 32) | (uint32_t)w0.z;
+            const int64_t gap = UNI ? (int64_t)(uint32_t)w0.z
+                                    : (((int64_t)(uint32_t)w0.w << 32) | (uint32_t)w0.z);
             const int32_t node = w1.x, s0 = w1.y, s1 = w1.z, p0 = w1.w, p1 = w2.x;
             const uint32_t cl = (uint32_t)w2.y;
             const int cls = ok ? (int)(cl & 0xffff) : 0;
@@ -583,7 +584,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
                 const int4 w0 = r4[0], w1 = r4[1], w2 = r4[2];
                 const int64_t dur = ((int64_t)(uint32_t)w0.y << 32) | (uint32_t)w0.x;
-                const int64_t gap = ((int64_t)(uint32_t)w0.w << 32) | (uint32_t)w0.z;
+                const int64_t gap = UNI ? (int64_t)(uint32_t)w0.z
+                                    : (((int64_t)(uint32_t)w0.w << 32) | (uint32_t)w0.z);
                 const int32_t node = w1.x, s0 = w1.y, s1 = w1.z, p0 = w1.w, p1 = w2.x;
                 // positions past the round's end hold stale LDS: nothing read
                 // from them may form an address
@@ -607,57 +609,84 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 const bool anyh = __any(head);
                 const uint32_t extra = flags >> 8;
                 const int tcx = ((flags >> 2) & 63u) * VS + o0;
+                // latest release over the parents present in each variant; every
+                // wave-uniform decision below is taken once for all VPL variants
+                int64_t X[VPL];
+#pragma unroll
+                for (int j = 0; j < VPL; j++) X[j] = 0;
+                if (any0) {
+                    const Vals<VPL> yn = *reinterpret_cast<const Vals<VPL> *>(&sR[i0 * VS + o0]);
+                    const int64_t g0g = UNI ? (int64_t)(uint32_t)w2.w : D.g0gap[i];
+#pragma unroll
+                    for (int j = 0; j < VPL; j++) {
+                        const int64_t ro = D.f0[i].x[j] + (((D.r0w[i] >> (vsh + j)) & 1u) ? 0 : g0g);
+                        const int64_t rel = old0 ? ro : yn.x[j];
+                        const bool on = has0 && (all_on || cls_on(eon[j], c0));
+                        X[j] = on ? rel : 0;
+                    }
+                }
+                if (any1) {
+                    Vals<VPL> ro{};
+                    if (__any(has1 && old1)) {           // rare: loaded on demand
+                        const int64_t a1 = has1 && old1 ? s1 : 0;
+                        const uint32_t r1w = a.rm[a1 * W + vw];
+                        const int64_t g1 = a.gap[a1];
+                        const Vals<VPL> f1 = *reinterpret_cast<const Vals<VPL> *>(a.finish + a1 * V + vvf);
+#pragma unroll
+                        for (int j = 0; j < VPL; j++)
+                            ro.x[j] = f1.x[j] + (((r1w >> (vsh + j)) & 1u) ? 0 : g1);
+                    }
+                    const Vals<VPL> yn = *reinterpret_cast<const Vals<VPL> *>(&sR[i1 * VS + o0]);
+#pragma unroll
+                    for (int j = 0; j < VPL; j++) {
+                        const int64_t rel = old1 ? ro.x[j] : yn.x[j];
+                        const bool on = has1 && (all_on || cls_on(eon[j], c1));
+                        X[j] = on ? max64(X[j], rel) : X[j];
+                    }
+                }
+                if (tcar && anyh) {                            // previous task of the thread
+                    const Vals<VPL> tc = *reinterpret_cast<const Vals<VPL> *>(&sTC[tcx]);
+#pragma unroll
+                    for (int j = 0; j < VPL; j++) X[j] = head ? max64(X[j], tc.x[j]) : X[j];
+                }
+                if (__any(extra != 0u) && extra) {             // rare: wide fan-in
+                    const int64_t e1 = a.gat_ptr[r0 + q + 1];
+                    for (int64_t e = a.gat_ptr[r0 + q] + 2; e < e1; e++) {
+                        const uint8_t c = a.gat_cls[e];
+                        const int32_t sp = a.gat_spos[e];
+                        Vals<VPL> rel;
+                        if (sp < prev_r0) {
+                            const int64_t sx = a.gat_src[e];
+                            const uint32_t rw = a.rm[sx * W + vw];
+                            const int64_t gg = a.gat_gap[e];
+                            const Vals<VPL> fx = *reinterpret_cast<const Vals<VPL> *>(a.finish + sx * V + vvf);
+#pragma unroll
+                            for (int j = 0; j < VPL; j++)
+                                rel.x[j] = fx.x[j] + (((rw >> (vsh + j)) & 1u) ? 0 : gg);
+                        } else {
+                            rel = *reinterpret_cast<const Vals<VPL> *>(&sR[(sp - prev_r0) * VS + o0]);
+                        }
+#pragma unroll
+                        for (int j = 0; j < VPL; j++)
+                            if (cls_on(eon[j], c)) X[j] = max64(X[j], rel.x[j]);
+                    }
+                }
+                if (anyh) {                                    // a run starts: reset the fold
+#pragma unroll
+                    for (int j = 0; j < VPL; j++) {
+                        A[j] = head ? 0 : A[j];
+                        B[j] = head ? 0 : B[j];
+                    }
+                }
 #pragma unroll
                 for (int j = 0; j < VPL; j++) {
-                    const uint32_t bit = vsh + j;
                     const bool rmv = (rb >> (o0 + j)) & 1u;
-                    int64_t X = 0;
-                    if (any0) {
-                        const int64_t g0g = UNI ? (int64_t)(uint32_t)w2.w : D.g0gap[i];
-                        const int64_t ro = D.f0[i].x[j] + (((D.r0w[i] >> bit) & 1u) ? 0 : g0g);
-                        const int64_t rn0 = sR[i0 * VS + o0 + j];
-                        const int64_t rel = old0 ? ro : rn0;
-                        const bool on = has0 && (all_on || cls_on(eon[j], c0));
-                        X = on ? rel : 0;
-                    }
-                    if (any1) {
-                        int64_t ro = 0;
-                        if (__any(has1 && old1)) {       // rare: loaded on demand
-                            const int64_t a1 = has1 && old1 ? s1 : 0;
-                            const bool r1 = (a.rm[a1 * W + vw] >> bit) & 1u;
-                            ro = a.finish[a1 * V + vvf + j] + (r1 ? 0 : a.gap[a1]);
-                        }
-                        const int64_t rn1 = sR[i1 * VS + o0 + j];
-                        const int64_t rel = old1 ? ro : rn1;
-                        const bool on = has1 && (all_on || cls_on(eon[j], c1));
-                        X = on ? max64(X, rel) : X;
-                    }
-                    if (tcar && anyh) {                        // previous task of the thread
-                        const int64_t tc = sTC[tcx + j];
-                        X = head ? max64(X, tc) : X;
-                    }
-                    if (extra) {                               // rare: wide fan-in
-                        const int64_t e1 = a.gat_ptr[r0 + q + 1];
-                        for (int64_t e = a.gat_ptr[r0 + q] + 2; e < e1; e++) {
-                            const uint8_t c = a.gat_cls[e];
-                            if (!cls_on(eon[j], c)) continue;
-                            const int32_t sp = a.gat_spos[e];
-                            int64_t rel;
-                            if (sp < prev_r0) {
-                                const int64_t sx = a.gat_src[e];
-                                const bool rs = (a.rm[sx * W + vw] >> bit) & 1u;
-                                rel = a.finish[sx * V + vvf + j] + (rs ? 0 : a.gat_gap[e]);
-                            } else {
-                                rel = sR[(sp - prev_r0) * VS + o0 + j];
-                            }
-                            X = max64(X, rel);
-                        }
-                    }
                     const bool live = ok && !rmv;
                     int64_t dp;
                     if (UNI) {
                         const uint64_t te = sT[cls * VS + o0 + j];
-                        dp = (int64_t)(((uint64_t)(uint32_t)dur * (uint32_t)te) >> ((uint32_t)(te >> 32) & 0xff));
+                        const uint32_t pm = live ? (uint32_t)te : 0u;   // removed: zero duration
+                        dp = (int64_t)(((uint64_t)(uint32_t)dur * pm) >> ((uint32_t)(te >> 32) & 0xff));
                     } else if (TLDS) {
                         const uint64_t te = sT[cls * VS + o0 + j];
                         if (shift_only) {
@@ -668,13 +697,9 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     } else {
                         dp = scaled(dur, a.table[(int64_t)cls * V + vvf + j]);
                     }
-                    dp = live ? dp : 0;
+                    if (!UNI) dp = live ? dp : 0;
                     const int64_t gp = live ? gap : 0;
-                    if (anyh) {
-                        A[j] = head ? 0 : A[j];
-                        B[j] = head ? 0 : B[j];
-                    }
-                    const int64_t F = max64(B[j], X) + dp;
+                    const int64_t F = max64(B[j], X[j]) + dp;
                     Dp[i][j] = A[j] + dp;
                     A[j] += dp + gp;
                     B[j] = F + gp;
@@ -708,24 +733,35 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         int64_t xa[VPL], xb[VPL];
         int xh[VPL];
         bool cact[VPL];
-        if (VPL == 2 && NS == 128) {
-            // wave w scans variant w, lane l its slots 2l and 2l+1: the pair
-            // is composed first, one wave scan covers the 64 pairs, and slot
-            // 2l takes the prefix of the previous pair (lane l-1; slot 0 is
-            // always a segment head, so lane 0 needs none)
-            const int e0 = wv * NS + 2 * lane;
-            const int64_t a0 = sA[e0], a1 = sA[e0 + 1];
-            const int64_t b0 = sB[e0], b1 = sB[e0 + 1];
-            const int h0 = sH[e0], h1 = sH[e0 + 1];
-            int64_t pa = h1 ? a1 : a0 + a1;
-            int64_t pb = h1 ? b1 : max64(b0 + a1, b1);
-            int ph = h0 | h1;
+        if (NS == 64 * VPL) {
+            // wave w scans variant w, lane l its VPL consecutive slots: the
+            // lane folds them first (keeping each prefix), one wave scan
+            // covers the 64 lane totals, and every slot then takes the
+            // prefix of the lanes before it (slot 0 is always a segment
+            // head, so lane 0 needs none)
+            const int e0 = wv * NS + VPL * lane;
+            int64_t ta[VPL], tb[VPL];
+            int th[VPL];
+#pragma unroll
+            for (int m = 0; m < VPL; m++) {
+                const int64_t am = sA[e0 + m], bm = sB[e0 + m];
+                const int hm = sH[e0 + m];
+                if (m == 0) {
+                    ta[0] = am; tb[0] = bm; th[0] = hm;
+                } else {
+                    ta[m] = hm ? am : ta[m - 1] + am;
+                    tb[m] = hm ? bm : max64(tb[m - 1] + am, bm);
+                    th[m] = hm | th[m - 1];
+                }
+            }
+            int64_t pa = ta[VPL - 1], pb = tb[VPL - 1];
+            int ph = th[VPL - 1];
             wave_scan(pa, pb, ph);
             const int qlo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)pb, 0x138, 0xf, 0xf, false);   // wave_shr:1
             const int qhi = __builtin_amdgcn_update_dpp(0, (int)((uint64_t)pb >> 32), 0x138, 0xf, 0xf, false);
             const int64_t qb = (int64_t)(((uint64_t)(uint32_t)qhi << 32) | (uint32_t)qlo);
-            sB[e0] = h0 ? b0 : max64(qb + a0, b0);
-            sB[e0 + 1] = pb;
+#pragma unroll
+            for (int m = 0; m < VPL; m++) sB[e0 + m] = th[m] ? tb[m] : max64(qb + ta[m], tb[m]);
         } else if (NS <= 64 * VPL) {
             // a wave scans whole variants (its VPL chunks hold them): the
             // chunks of one variant follow each other in the same wave

@@ -265,14 +265,54 @@ __global__ __launch_bounds__(kWG) void k_kahn_rounds(KahnArgs a) {
 // Windowed rounds for graphs with at most kWinT threads: the same rounds as
 // above, with each thread's next candidates staged in LDS (a wave per thread,
 // waves taking threads w, w + waves, ...) so that a round reads no global
-// memory except to refill a window
-// that is less than half full, to test a candidate beyond its window, or for
-// a requirement past the first two of a candidate.
+// memory except to refill a window that is less than half full, to cross a
+// ready run longer than the window, or for a requirement past the first two
+// of a candidate.
+//
+// A long ready run is crossed with tile maxima: for tiles of 64 and of 4096
+// consecutive candidates (global candidate order), the largest requirement
+// position on each parent thread.  A tile whose maxima all lie behind the
+// round's fronts holds no blocked candidate.  Candidates before the search
+// start are ready already, so only a tile that also holds another thread's
+// candidates can look blocked without being so; the search then simply goes
+// on after it.
 constexpr int kWinT = 16;
 constexpr int kWinEnt = 6144;           // LDS candidate entries shared by all threads
 constexpr int kRefill = 8;              // window entries loaded per lane at once
-constexpr int kFar = 16;                // candidates per lane and step past the window
 constexpr int kNear = 1;                // candidates per lane and step inside the window
+
+// tile maxima over candidates: tm1[k * T + s] = largest requirement position
+// on thread s among candidates [64k, 64k + 64) (-1 if none); one wave per tile
+__global__ __launch_bounds__(kBS) void k_tile_max1(int64_t C, int32_t T,
+                                                   const int64_t *__restrict__ req_ptr,
+                                                   const int32_t *__restrict__ req_chain,
+                                                   const int64_t *__restrict__ req_gpos,
+                                                   int32_t *__restrict__ tm1) {
+    const int64_t j = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    const int64_t k = j >> 6;
+    const bool ok = j < C;
+    const int64_t q0 = ok ? req_ptr[j] : 0, q1 = ok ? req_ptr[j + 1] : 0;
+    for (int32_t ts = 0; ts < T; ts++) {
+        int64_t r = -1;
+        for (int64_t q = q0; q < q1; q++)
+            if (req_chain[q] == ts && req_gpos[q] > r) r = req_gpos[q];
+        r = wave_max64(r);
+        if ((threadIdx.x & 63) == 0 && (k << 6) < C) tm1[k * T + ts] = (int32_t)r;
+    }
+}
+
+// tm2[m * T + s] = maximum of tm1 over tiles [64m, 64m + 64)
+__global__ __launch_bounds__(kBS) void k_tile_max2(int64_t C1, int32_t T,
+                                                   const int32_t *__restrict__ tm1,
+                                                   int32_t *__restrict__ tm2) {
+    const int64_t k = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    const int64_t m = k >> 6;
+    for (int32_t ts = 0; ts < T; ts++) {
+        int64_t r = k < C1 ? tm1[k * T + ts] : -1;
+        r = wave_max64(r);
+        if ((threadIdx.x & 63) == 0 && (m << 6) < C1) tm2[m * T + ts] = (int32_t)r;
+    }
+}
 
 struct WinArgs {
     int32_t T, wlog;                    // window of 2^wlog entries per thread
@@ -282,6 +322,7 @@ struct WinArgs {
     const int64_t *req_ptr;             // [C+1]
     const int32_t *req_chain;
     const int64_t *req_gpos;
+    const int32_t *tm1, *tm2;           // tile maxima (tiles of 64 and 4096 candidates)
     int32_t *ftab;                      // [(n+1) x T] fronts at the start of each round
     int64_t *result;                    // [0] steps
     uint32_t *err;
@@ -381,24 +422,42 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
                         if (hit) break;
                         ci = ci + kNear * 64 < lim ? ci + kNear * 64 : lim;
                     } else {
-                        // past the window (a long ready run): kFar x 64
-                        // candidates from global memory, all loads in flight
-                        CandEnt e[kFar];
+                        // past the window (a long ready run): tiles of 4096,
+                        // then of 64, then single candidates, 64 per probe
+                        int32_t fr[kWinT];
 #pragma unroll
-                        for (int r = 0; r < kFar; r++) {
-                            const int j = ci + r * 64 + lane;
-                            e[r] = a.pent[j < ce ? j : ce - 1];
-                        }
-                        bool hit = false;
+                        for (int ts = 0; ts < kWinT; ts++) fr[ts] = ts < T ? front[ts] : 0;
+                        auto tile_blocked = [&](const int32_t *row) {
+                            bool b = false;
 #pragma unroll
-                        for (int r = 0; r < kFar; r++) {
-                            const int j = ci + r * 64 + lane;
-                            const bool b = j < ce && win_blocked(a, e[r], j, front);
-                            const unsigned long long bal = __ballot(b);
-                            if (bal && !hit) { cnew = ci + r * 64 + __ffsll((long long)bal) - 1; hit = true; }
+                            for (int ts = 0; ts < kWinT; ts++)
+                                if (ts < T && row[ts] >= fr[ts]) b = true;
+                            return b;
+                        };
+                        int64_t pos = ci;          // every candidate before pos is ready
+                        cnew = ce;
+                        while (pos < ce) {
+                            const int64_t k2 = pos >> 12, t2 = k2 + lane;
+                            const bool b2 = (t2 << 12) < ce && tile_blocked(a.tm2 + t2 * T);
+                            const unsigned long long bal2 = __ballot(b2);
+                            if (!bal2) { pos = (k2 + 64) << 12; continue; }
+                            const int64_t L2 = k2 + __ffsll((long long)bal2) - 1;
+                            pos = pos > (L2 << 12) ? pos : (L2 << 12);
+                            const int64_t end2 = ce < ((L2 + 1) << 12) ? ce : ((L2 + 1) << 12);
+                            const int64_t k1 = pos >> 6, t1 = k1 + lane;
+                            const bool b1 = (t1 << 6) < end2 && tile_blocked(a.tm1 + t1 * T);
+                            const unsigned long long bal1 = __ballot(b1);
+                            if (!bal1) { pos = end2; continue; }
+                            const int64_t L1 = k1 + __ffsll((long long)bal1) - 1;
+                            pos = pos > (L1 << 6) ? pos : (L1 << 6);
+                            const int64_t end1 = ce < ((L1 + 1) << 6) ? ce : ((L1 + 1) << 6);
+                            const int64_t j = pos + lane;
+                            const bool b0 = j < end1 && win_blocked(a, a.pent[j < end1 ? j : pos], j, front);
+                            const unsigned long long bal0 = __ballot(b0);
+                            if (bal0) { cnew = (int)(pos + __ffsll((long long)bal0) - 1); break; }
+                            pos = end1;
                         }
-                        if (hit) break;
-                        ci += kFar * 64;
+                        break;
                     }
                 }
             } else {
@@ -727,7 +786,7 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
             *gcnt = nullptr, *lvl_cnt = nullptr;
     int32_t *req_chain = nullptr, *long_list = nullptr, *seg_step = nullptr, *level = nullptr;
     CandEnt *pent = nullptr;
-    int32_t *ftab = nullptr;
+    int32_t *ftab = nullptr, *tm1 = nullptr, *tm2 = nullptr;
     int64_t *seg_cnt = nullptr;
     const bool windowed = T <= kWinT;
     uint32_t *err = nullptr;
@@ -791,8 +850,18 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
         int wlog = 6;                                  // 2^wlog entries per thread
         while ((int64_t)T << (wlog + 1) <= kWinEnt) wlog++;
         CK(dalloc_n(&ftab, (size_t)(n + 2) * T, s));
+        const int64_t C1 = (h_C + 63) / 64, C2 = (C1 + 63) / 64;
+        CK(dalloc_n(&tm1, (size_t)(C1 > 0 ? C1 : 1) * T, s));
+        CK(dalloc_n(&tm2, (size_t)(C2 > 0 ? C2 : 1) * T, s));
+        if (h_C > 0) {
+            k_tile_max1<<<grid_for(C1 * 64, kBS), kBS, 0, s>>>(h_C, T, req_ptr, req_chain, req_gpos,
+                                                               tm1);
+            CK(hipGetLastError());
+            k_tile_max2<<<grid_for(C2 * 64, kBS), kBS, 0, s>>>(C1, T, tm1, tm2);
+            CK(hipGetLastError());
+        }
         WinArgs wa{T, wlog, g->thread_base, cbase, pent, req_ptr, req_chain, req_gpos,
-                   ftab, result, err};
+                   tm1, tm2, ftab, result, err};
         k_kahn_win<<<1, kWG, 0, s>>>(wa);
         CK(hipGetLastError());
     } else {
@@ -942,7 +1011,7 @@ done:
     dfree(nfront, s); dfree(nci, s); dfree(long_list, s); dfree(seg_start, s);
     dfree(seg_len, s); dfree(seg_off, s); dfree(seg_step, s); dfree(step_seg, s);
     dfree(gcnt, s); dfree(lvl_cnt, s); dfree(level, s); dfree(pent, s);
-    dfree(ftab, s); dfree(seg_cnt, s);
+    dfree(ftab, s); dfree(tm1, s); dfree(tm2, s); dfree(seg_cnt, s);
     return st;
 }
 

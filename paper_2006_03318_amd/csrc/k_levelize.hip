@@ -361,6 +361,7 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
     const int ce = mine ? (int)a.cbase[t + 1] : 0;
     int ci = mine ? (int)a.cbase[t] : 0;
     int wend = ci;
+    int f = mine ? (int)a.base[t] : 0;             // the wave's own front (also in LDS for the others)
     if (threadIdx.x < 32) reinterpret_cast<uint8_t *>(s_adv)[threadIdx.x] = 0;
     if (threadIdx.x < 32) reinterpret_cast<uint8_t *>(s_unf)[threadIdx.x] = 0;
     if (threadIdx.x < T) {
@@ -397,8 +398,8 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
         }
         // A: advance each thread's front past its ready candidates
         if (mine) {
-            const int f = front[t];
             int cnew = ce;
+            int npos = end;                        // order position of candidate cnew (end if none)
             if (f < end) {
                 for (;;) {
                     if (ci >= ce) { cnew = ce; break; }
@@ -407,17 +408,24 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
                         // of all of them in flight together
                         const int lim = wend < ce ? wend : ce;
                         bool bl[kNear];
+                        int ep[kNear];
 #pragma unroll
                         for (int r = 0; r < kNear; r++) {
                             const int j = ci + r * 64 + lane;
                             const CandEnt e = win[j & (W - 1)];
                             bl[r] = j < lim && win_blocked(a, e, j, front);
+                            ep[r] = e.pos;
                         }
                         bool hit = false;
 #pragma unroll
                         for (int r = 0; r < kNear; r++) {
                             const unsigned long long bal = __ballot(bl[r]);
-                            if (bal && !hit) { cnew = ci + r * 64 + __ffsll((long long)bal) - 1; hit = true; }
+                            if (bal && !hit) {
+                                const int L = __ffsll((long long)bal) - 1;
+                                cnew = ci + r * 64 + L;
+                                npos = __builtin_amdgcn_readlane(ep[r], L);   // the finder's entry
+                                hit = true;
+                            }
                         }
                         if (hit) break;
                         ci = ci + kNear * 64 < lim ? ci + kNear * 64 : lim;
@@ -452,9 +460,15 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
                             pos = pos > (L1 << 6) ? pos : (L1 << 6);
                             const int64_t end1 = ce < ((L1 + 1) << 6) ? ce : ((L1 + 1) << 6);
                             const int64_t j = pos + lane;
-                            const bool b0 = j < end1 && win_blocked(a, a.pent[j < end1 ? j : pos], j, front);
+                            const CandEnt e0 = a.pent[j < end1 ? j : pos];
+                            const bool b0 = j < end1 && win_blocked(a, e0, j, front);
                             const unsigned long long bal0 = __ballot(b0);
-                            if (bal0) { cnew = (int)(pos + __ffsll((long long)bal0) - 1); break; }
+                            if (bal0) {
+                                const int L = __ffsll((long long)bal0) - 1;
+                                cnew = (int)(pos + L);
+                                npos = __builtin_amdgcn_readlane(e0.pos, L);
+                                break;
+                            }
                             pos = end1;
                         }
                         break;
@@ -463,16 +477,15 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
             } else {
                 cnew = ci;
             }
+            const int nf = f >= end ? f : (cnew < ce ? npos : end);
             if (lane == 0) {
-                const int nf = f >= end ? f
-                               : (cnew < ce ? (cnew < wend ? win[cnew & (W - 1)].pos : a.pent[cnew].pos)
-                                            : end);
                 s_front[cur ^ 1][t] = nf;
                 s_adv[cur][t] = nf > f;
                 s_unf[cur][t] = f < end;
                 a.ftab[(round + 1) * T + t] = nf;
             }
             ci = cnew;
+            f = nf;
         }
         __syncthreads();
         // every wave reads the same flags: all threads done, or a stall (cycle)

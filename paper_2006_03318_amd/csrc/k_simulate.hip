@@ -282,24 +282,23 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
     // wave with K positions per slot
     auto per_slot = [&](int rn) { return rn <= NS ? 1 : (rn + NS - 1) / NS; };
 
-    // loads of round kk (records in ring buffer b); a gather is old when its
-    // source position precedes prev_r0 (its round has ended before round kk-1)
-    auto issue = [&](int64_t kk, int b, int prev_r0, Dyn<K, VPL> &d) {
-        const int rn = round_rn[kk];
+    // loads of a round of rn positions (records in ring buffer b); a gather
+    // is old when its source position precedes prev_r0 (its round has ended
+    // before the round that issues these loads)
+    // (the layout is a compile-time choice: with a run-time branch between the
+    // two layouts, the compiler would make each wait for the other's loads)
+    auto issue = [&](auto small_tag, int rn, int b, int prev_r0, Dyn<K, VPL> &d) {
+        constexpr bool SMALL_LAYOUT = decltype(small_tag)::value;
         const int ke = per_slot(rn);
         const Rec *R = reinterpret_cast<const Rec *>(sRec[b]);
-        if (rn <= kSmall) {
+        if constexpr (SMALL_LAYOUT) {
             // small layout: position = lane; slot jj of the load registers
-            // holds variant w + 8 jj of this wave (K loads of the removal
-            // word either way, so that both layouts issue alike)
+            // holds variant w + 8 jj of this wave
             const int q = lane;
             const bool ok = q < rn;
-            const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
-            const int4 w1 = r4[1];
-            const int p1 = r4[2].x;
+            const int4 w1 = reinterpret_cast<const int4 *>(&R[q])[1];
             const bool n0 = ok && w1.y >= 0 && w1.w < prev_r0;
             const int64_t a0 = n0 ? w1.y : 0;
-            (void)p1;
 #pragma unroll
             for (int jj = 0; jj < K; jj++) {
                 const int os = wv + NW * jj;
@@ -313,43 +312,55 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 uint32_t r0 = 0;
                 int64_t gg = 0;
                 if (jj < PS) {
-                    if (__any(n0 && vv)) {
-                        f.x[0] = a.finish[a0 * V + vs_];
-                        r0 = a.rm[a0 * W + vwj];
-                        if (!UNI) gg = a.gap[a0];
-                    }
+                    // issued on every path (row 0 when unused): with a known
+                    // count of loads, the ring refill waits for the record
+                    // loads only
+                    f.x[0] = a.finish[a0 * V + vs_];
+                    r0 = a.rm[a0 * W + vwj];
+                    if (!UNI) gg = a.gap[a0];
                 }
                 d.f0[jj] = f;
                 d.r0w[jj] = r0;
                 d.g0gap[jj] = gg;
             }
-            return;
-        }
+        } else {
 #pragma unroll
-        for (int i = 0; i < K; i++) {
-            const int q = slot * ke + i;
-            const bool ok = i < ke && q < rn;
-            const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
-            const int4 w1 = r4[1];   // node, g0_src, g1_src, g0_spos
-            const int p1 = r4[2].x;  // g1_spos
-            const bool n0 = ok && w1.y >= 0 && w1.w < prev_r0;
-            const int64_t a0 = n0 ? w1.y : 0;
-            (void)p1;
-            Vals<VPL> f{};
-            uint32_t r0 = 0;
-            int64_t gg = 0;
-            if (__any(n0)) {
-                f = *reinterpret_cast<const Vals<VPL> *>(a.finish + a0 * V + vvf);
-                r0 = a.rm[a0 * W + vw];
-                if (!UNI) gg = a.gap[a0];
+            for (int i = 0; i < K; i++) {
+                const int q = slot * ke + i;
+                const bool ok = i < ke && q < rn;
+                const int4 w1 = reinterpret_cast<const int4 *>(&R[q])[1];   // node, g0_src, g1_src, g0_spos
+                const bool n0 = ok && w1.y >= 0 && w1.w < prev_r0;
+                const int64_t a0 = n0 ? w1.y : 0;
+                // issued on every path (row 0 when unused), like the small layout
+                const Vals<VPL> f = *reinterpret_cast<const Vals<VPL> *>(a.finish + a0 * V + vvf);
+                const uint32_t r0 = a.rm[a0 * W + vw];
+                const int64_t gg = UNI ? 0 : a.gap[a0];
+                d.f0[i] = f;
+                d.r0w[i] = r0;
+                d.g0gap[i] = gg;
             }
-            d.f0[i] = f;
-            d.r0w[i] = r0;
-            d.g0gap[i] = gg;
         }
     };
+    // (start, size) of rounds k .. k+3, the last clamped to the final round:
+    // each round loads the entry three rounds ahead, so no round waits for
+    // a scalar load of its own bounds
+    auto rmeta = [&](int64_t i, int &r0_, int &rn_) {
+        const int64_t c = i < nr ? i : nr - 1;
+        r0_ = round_r0[c];
+        rn_ = round_rn[c];
+    };
+    int m0r0 = 0, m0rn = 0, m1r0 = 0, m1rn = 0, m2r0 = 0, m2rn = 0, m3r0 = 0, m3rn = 0;
+    if (nr > 0) {
+        rmeta(0, m0r0, m0rn);
+        rmeta(1, m1r0, m1rn);
+        rmeta(2, m2r0, m2rn);
+        rmeta(3, m3r0, m3rn);
+    }
     Dyn<K, VPL> D;
-    if (nr > 0) issue(0, 0, 0, D);
+    if (nr > 0) {
+        if (m0rn <= kSmall) issue(std::true_type{}, m0rn, 0, 0, D);
+        else issue(std::false_type{}, m0rn, 0, 0, D);
+    }
     // Consume the first round's loads here: the loop's registers then hold
     // no load in flight on entry, and the wait-count bookkeeping does not
     // make every round's walk wait for part of the next round's loads.
@@ -370,9 +381,11 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
     // skips both bodies, so it never makes a round wait for loads of the
     // previous round, or for its stores, that were in fact consumed already.
     int64_t k = 0;
-    auto round = [&](auto small_tag) {
+    auto round = [&](auto small_tag, auto next_small_tag) {
         constexpr bool SMALL_ROUND = decltype(small_tag)::value;
-        const int r0 = round_r0[k], rn = round_rn[k];
+        const int r0 = m0r0, rn = m0rn;
+        int m4r0, m4rn;                           // round k+4, used from the next round on
+        if (nr > 0) rmeta(k + 4, m4r0, m4rn);
         const Rec *R = reinterpret_cast<const Rec *>(sRec[b0]);
         uint64_t eon[VPL];
 #pragma unroll
@@ -382,19 +395,16 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         // walk does not queue behind them and the two register sets are
         // never live together
         Dyn<K, VPL> DN;
-        const int64_t k1 = k + 1 < nr ? k + 1 : k;
+        const int rn1 = m1rn;                     // round k+1 (this round if last)
         const int bN = k + 1 < nr ? b1 : b0;
-        // records of round k+2: global -> registers now, -> LDS at the round's end
-        const int64_t k2 = k + 2 < nr ? k + 2 : k;
-        const int nxt_w = k + 2 < nr ? round_rn[k2] * 3 : 0;
-        const u32x4 *nsrc = reinterpret_cast<const u32x4 *>(rec + round_r0[k2]);
+        // records of round k+2: global -> registers, -> LDS before the stores
+        const int nxt_w = k + 2 < nr ? m2rn * 3 : 0;
+        const u32x4 *nsrc = reinterpret_cast<const u32x4 *>(rec + m2r0);
         u32x4 nx0, nx1, nx2;
         RmT nrm;
-        // issued inside each round's branch, so that no path of the loop
-        // skips both the loads and the write below
         auto load_next = [&]() {
             nx0 = nsrc[tid < nxt_w ? tid : 0];
-            nrm = rmrow[round_r0[k2] + (tid < nxt_w / 3 ? tid : 0)];
+            nrm = rmrow[m2r0 + (tid < nxt_w / 3 ? tid : 0)];
             if (PF > 1) nx1 = nsrc[tid + NT < nxt_w ? tid + NT : 0];
             if (PF > 2) nx2 = nsrc[tid + 2 * NT < nxt_w ? tid + 2 * NT : 0];
         };
@@ -420,7 +430,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             // ---- small round: one position per lane, variants per wave ----
             load_next();
             Dyn<K, VPL> DNs;
-            issue(k1, bN, r0, DNs);
+            issue(next_small_tag, rn1, bN, r0, DNs);
             const int q = lane;
             const bool ok = q < rn;
             const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
@@ -725,7 +735,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         }
         __syncthreads();                                     // B1
         Dyn<K, VPL> DNb;
-        issue(k1, bN, r0, DNb);
+        issue(next_small_tag, rn1, bN, r0, DNb);
         // inclusive scan of slot summaries per variant: DPP within the wave,
         // then earlier 64-slot chunks of the same variant; chunks whose
         // slots all lie past the round's end are skipped
@@ -878,11 +888,20 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         prev_r0 = r0;
         D = DN;
         const int bt = b0; b0 = b1; b1 = b2; b2 = bt;
+        m0r0 = m1r0; m0rn = m1rn; m1r0 = m2r0; m1rn = m2rn;
+        m2r0 = m3r0; m2rn = m3rn; m3r0 = m4r0; m3rn = m4rn;
         __syncthreads();                                     // B3
     };
+    // one loop per kind of round and kind of the round after it (the
+    // prefetch layout); every kind appears in the order, so each pass of
+    // the outer loop takes at least one round
+    const std::true_type sm{};
+    const std::false_type bg{};
     while (k < nr) {
-        for (; k < nr && round_rn[k] <= kSmall; k++) round(std::true_type{});
-        for (; k < nr && round_rn[k] > kSmall; k++) round(std::false_type{});
+        for (; k < nr && m0rn <= kSmall && m1rn <= kSmall; k++) round(sm, sm);
+        for (; k < nr && m0rn <= kSmall && m1rn > kSmall; k++) round(sm, bg);
+        for (; k < nr && m0rn > kSmall && m1rn <= kSmall; k++) round(bg, sm);
+        for (; k < nr && m0rn > kSmall && m1rn > kSmall; k++) round(bg, bg);
     }
 #pragma unroll
     for (int j = 0; j < VPL; j++) atomicMax(&sMs[o0 + j], (unsigned long long)ms[j]);

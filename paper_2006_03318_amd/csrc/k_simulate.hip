@@ -178,7 +178,11 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
     constexpr int VS = LPS * VPL;
     constexpr int NS = NT / LPS;
     constexpr int RP = NS * K;
-    constexpr int NE = NS * VS;           // slot summaries (= NT * VPL)
+    // slot summaries, variant-major with a row stride of NSP: when a wave
+    // scans whole variants, 4 entries of padding put the rows written by
+    // one wave on different banks
+    constexpr int NSP = NS == 64 * VPL ? NS + 4 : NS;
+    constexpr int NE = NSP * VS;
     constexpr int RW = RP * 3;            // 16-byte words of one ring buffer
     constexpr int PF = (RW + NT - 1) / NT;
     static_assert(sizeof(Rec) == 48, "record layout");
@@ -727,7 +731,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         // idle waves are the identity (0, 0)
 #pragma unroll
         for (int j = 0; j < VPL; j++) {
-            const int e = (o0 + j) * NS + slot;
+            const int e = (o0 + j) * NSP + slot;
             const bool fold = slot == 0 && !hh;
             sA[e] = A[j];
             sB[e] = fold ? max64(carry[j] + A[j], B[j]) : B[j];
@@ -749,7 +753,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             // covers the 64 lane totals, and every slot then takes the
             // prefix of the lanes before it (slot 0 is always a segment
             // head, so lane 0 needs none)
-            const int e0 = wv * NS + VPL * lane;
+            const int e0 = wv * NSP + VPL * lane;
             int64_t ta[VPL], tb[VPL];
             int th[VPL];
 #pragma unroll
@@ -840,7 +844,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         int64_t cin[VPL];
 #pragma unroll
         for (int j = 0; j < VPL; j++)
-            cin[j] = slot == 0 ? carry[j] : sB[(o0 + j) * NS + (slot > 0 ? slot - 1 : 0)];
+            cin[j] = slot == 0 ? carry[j] : sB[(o0 + j) * NSP + (slot > 0 ? slot - 1 : 0)];
 #pragma unroll
         for (int i = 0; i < K; i++) {
             const int q = slot * ke + i;
@@ -878,7 +882,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             }
         }
 #pragma unroll
-        for (int j = 0; j < VPL; j++) carry[j] = sB[(o0 + j) * NS + ls];
+        for (int j = 0; j < VPL; j++) carry[j] = sB[(o0 + j) * NSP + ls];
         if (slot == 0) {
 #pragma unroll
             for (int j = 0; j < VPL; j++) sCarry[o0 + j] = carry[j];

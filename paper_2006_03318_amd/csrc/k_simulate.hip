@@ -63,9 +63,9 @@ struct PipeArgs {
     const ScaleEntry *table;      // [n_cls][V]
     int32_t n_cls;
     const uint32_t *rm;           // [n][W]
-    const void *rmp;              // [workgroups][n] removal bits of the workgroup's variants
-                                  // per schedule position (u8 for VS <= 8, else u16)
-    int64_t npos;                 // positions (= tasks)
+    const void *rmp;              // [workgroups][rmp_stride] removal bits of the workgroup's
+                                  // variants per schedule position (u8 for VS <= 8, else u16)
+    int64_t rmp_stride;           // positions rounded up to 16 bytes of row
     const uint64_t *edge_on;      // [V]
     uint64_t cls_mask;            // edge classes present in the schedule's gathers
     int32_t thread_carry;         // previous task of a run comes from LDS carries
@@ -237,7 +237,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
     // stores that must not land go to one 16-byte spot per wave (one line)
     gi64 *const dummy = (gi64 *)(a.dummy + (tid >> 6) * 2);
     const bool tcar = a.thread_carry != 0;
-    const RmT *const rmrow = reinterpret_cast<const RmT *>(a.rmp) + (int64_t)wg * a.npos;
+    const RmT *const rmrow = reinterpret_cast<const RmT *>(a.rmp) + (int64_t)wg * a.rmp_stride;
 
     if (tid == 0) sFlags = 0;
     {   // the record ring starts zeroed (no stale fields past a round's end)
@@ -917,36 +917,52 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
 
 // Removal bits per schedule position for each workgroup's VS variants:
 // rmp[g][q] = bits g*VS .. g*VS+VS-1 of task pos_node[q]'s removal row.
-// A block transposes a tile of 64 positions x 64 words through LDS, so both
-// the row reads and the per-workgroup writes are contiguous.
+// A block transposes 128 positions x 64 words through LDS: the row reads are
+// contiguous, and every lane writes 16 bytes of one workgroup's row (rows
+// are padded to a multiple of 16 bytes).
 template <int VS, typename RmT>
-__global__ __launch_bounds__(256) void k_rm_pos(int64_t n, int32_t W, int32_t nwg,
+__global__ __launch_bounds__(256) void k_rm_pos(int64_t n, int64_t stride, int32_t W, int32_t nwg,
                                                 const int32_t *__restrict__ pos_node,
                                                 const uint32_t *__restrict__ rm,
                                                 RmT *__restrict__ rmp) {
-    __shared__ uint32_t tile[64][65];
-    const int64_t q0 = (int64_t)blockIdx.x * 64;
+    constexpr int TP = 128;                       // positions per block
+    constexpr int PER = 16 / (int)sizeof(RmT);    // positions per 16-byte store
+    constexpr int SEG = TP / PER;                 // stores per workgroup row
+    __shared__ uint32_t tile[TP][65];
+    const int64_t q0 = (int64_t)blockIdx.x * TP;
     const int w0 = blockIdx.y * 64;
-    for (int i = threadIdx.x; i < 64 * 64; i += 256) {
-        const int pl = i >> 6, wl = i & 63;
-        const int64_t q = q0 + pl;
-        const int w = w0 + wl;
-        uint32_t v = 0;
-        if (q < n && w < W) v = rm[(int64_t)pos_node[q] * W + w];
-        tile[pl][wl] = v;
+    constexpr int LD = TP * 64 / 256;             // words loaded per lane, all in flight
+    uint32_t v[LD];
+#pragma unroll
+    for (int r = 0; r < LD; r++) {
+        const int i = threadIdx.x + r * 256;
+        const int64_t q = q0 + (i >> 6);
+        const int w = w0 + (i & 63);
+        v[r] = (q < n && w < W) ? rm[(int64_t)pos_node[q < n ? q : 0] * W + (w < W ? w : 0)] : 0u;
+    }
+#pragma unroll
+    for (int r = 0; r < LD; r++) {
+        const int i = threadIdx.x + r * 256;
+        tile[i >> 6][i & 63] = v[r];
     }
     __syncthreads();
     const int g0 = (int)((int64_t)w0 * 32 / VS);
     int64_t g1 = (int64_t)(w0 + 64) * 32 / VS;
     if (g1 > nwg) g1 = nwg;
     constexpr uint32_t mask = VS >= 32 ? ~0u : ((1u << VS) - 1u);
-    for (int64_t i = threadIdx.x; i < (g1 - g0) * 64; i += 256) {
-        const int g = g0 + (int)(i >> 6);
-        const int pl = (int)(i & 63);
-        const int64_t q = q0 + pl;
-        if (q >= n) continue;
+    for (int64_t i = threadIdx.x; i < (g1 - g0) * SEG; i += 256) {
+        const int g = g0 + (int)(i / SEG);
+        const int pl = (int)(i % SEG) * PER;
+        if (q0 + pl >= n) continue;               // the row's padding ends at stride >= n
         const int bitpos = g * VS;
-        rmp[(int64_t)g * n + q] = (RmT)((tile[pl][bitpos / 32 - w0] >> (bitpos % 32)) & mask);
+        const int wl = bitpos / 32 - w0, sh = bitpos % 32;
+        union {
+            RmT b[PER];
+            uint4 v;
+        } u;
+#pragma unroll
+        for (int m = 0; m < PER; m++) u.b[m] = (RmT)((tile[pl + m][wl] >> sh) & mask);
+        *reinterpret_cast<uint4 *>(rmp + (int64_t)g * stride + q0 + pl) = u.v;
     }
 }
 
@@ -1000,8 +1016,10 @@ hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants
     int64_t *cnt = nullptr, *dummy = nullptr;
     int32_t *r0 = nullptr, *rn = nullptr;
     RmT *rmp = nullptr;
+    constexpr int64_t kPer = 16 / (int64_t)sizeof(RmT);
+    const int64_t rstride = (sch->n + kPer - 1) / kPer * kPer;   // rmp row stride
     hipError_t e = dalloc_n(&cnt, (size_t)ns + 2, s);
-    if (e == hipSuccess) e = dalloc_n(&rmp, (size_t)grid * (size_t)(sch->n > 0 ? sch->n : 1), s);
+    if (e == hipSuccess) e = dalloc_n(&rmp, (size_t)grid * (size_t)(rstride > 0 ? rstride : kPer), s);
     if (e == hipSuccess) e = dalloc_n(&r0, (size_t)max_rounds, s);
     if (e == hipSuccess) e = dalloc_n(&rn, (size_t)max_rounds, s);
     if (e == hipSuccess) e = dalloc_n(&dummy, 2 * NT, s);
@@ -1010,8 +1028,9 @@ hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants
         return e;
     }
     if (sch->n > 0) {
-        const dim3 tg((unsigned)((sch->n + 63) / 64), (unsigned)((var->W + 63) / 64));
-        k_rm_pos<VS, RmT><<<tg, 256, 0, s>>>(sch->n, var->W, grid, sch->pos_node, var->rm_bits, rmp);
+        const dim3 tg((unsigned)((sch->n + 127) / 128), (unsigned)((var->W + 63) / 64));
+        k_rm_pos<VS, RmT><<<tg, 256, 0, s>>>(sch->n, rstride, var->W, grid, sch->pos_node,
+                                             var->rm_bits, rmp);
     }
     if (ns > 0) k_round_count<<<grid_for(ns, 256), 256, 0, s>>>(ns, sch->step_ptr, RP, cnt);
     e = scan_exclusive(cnt, cnt, ns, s);
@@ -1019,7 +1038,7 @@ hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants
         k_round_fill<<<grid_for(ns, 256), 256, 0, s>>>(ns, sch->step_ptr, cnt, RP, r0, rn);
     const uint64_t cls_mask = sch->mask & g->cross_mask;
     PipeArgs args{sch->gat_ptr, sch->gat_src, sch->gat_spos, sch->gat_cls, sch->gat_gap, g->gap,
-                  var->table, var->n_cls, var->rm_bits, rmp, (int64_t)sch->n, var->edge_on,
+                  var->table, var->n_cls, var->rm_bits, rmp, rstride, var->edge_on,
                   cls_mask, sch->thread_carry ? 1 : 0, var->V, var->W, finish, start, makespan,
                   dummy};
     const int64_t *nrp = cnt + ns;

@@ -122,22 +122,33 @@ __device__ __forceinline__ int64_t scaled8(int64_t d, uint64_t e, const ScaleEnt
     return (int64_t)(a >> sh);
 }
 
-// one Kogge-Stone step of the segmented max-plus scan across the wave, the
-// left operand taken with a DPP lane shift (lanes without one see identity)
+// Run heads without flags.  A range of positions maps the release entering
+// it to c -> max(c + a, b), with b >= a.  A range that holds the first task of
+// a run ignores c; it is written with a = kHead + (its weights after the
+// head), so c + a < 0 <= b for every c that occurs: every simulated time is
+// below 2^62 (the graph and transform checks reject anything larger), and c
+// plus the weights of later positions is itself such a time.  Composing keeps
+// a >= kHead, so no sum overflows.
+constexpr int64_t kHead = -(int64_t(1) << 62);
+
+// (la, lb) then (a, b)
+__device__ __forceinline__ void compose(int64_t la, int64_t lb, int64_t &a, int64_t &b) {
+    b = max64(lb + a, b);
+    a = a < 0 ? a : la + a;
+}
+
+// one Kogge-Stone step of the max-plus scan across the wave, the left
+// operand taken with a DPP lane shift (lanes without one see the identity
+// (0, 0), as b >= a)
 template <int CTRL, int RMASK>
-__device__ __forceinline__ void scan_step(int64_t &a, int64_t &b, int &h) {
+__device__ __forceinline__ void scan_step(int64_t &a, int64_t &b) {
     const int alo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)a, CTRL, RMASK, 0xf, false);
     const int ahi = __builtin_amdgcn_update_dpp(0, (int)((uint64_t)a >> 32), CTRL, RMASK, 0xf, false);
     const int blo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, RMASK, 0xf, false);
     const int bhi = __builtin_amdgcn_update_dpp(0, (int)((uint64_t)b >> 32), CTRL, RMASK, 0xf, false);
-    const int lh = __builtin_amdgcn_update_dpp(0, h, CTRL, RMASK, 0xf, false);
     const int64_t la = (int64_t)(((uint64_t)(uint32_t)ahi << 32) | (uint32_t)alo);
     const int64_t lb = (int64_t)(((uint64_t)(uint32_t)bhi << 32) | (uint32_t)blo);
-    if (!h) {
-        b = max64(lb + a, b);
-        a = la + a;
-        h = lh;
-    }
+    compose(la, lb, a, b);
 }
 
 __device__ __forceinline__ int64_t readlane64(int64_t x, int l) {
@@ -146,14 +157,14 @@ __device__ __forceinline__ int64_t readlane64(int64_t x, int l) {
     return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
 }
 
-// inclusive segmented scan over the 64 lanes of a wave
-__device__ __forceinline__ void wave_scan(int64_t &a, int64_t &b, int &h) {
-    scan_step<0x111, 0xf>(a, b, h);   // row_shr:1
-    scan_step<0x112, 0xf>(a, b, h);   // row_shr:2
-    scan_step<0x114, 0xf>(a, b, h);   // row_shr:4
-    scan_step<0x118, 0xf>(a, b, h);   // row_shr:8
-    scan_step<0x142, 0xa>(a, b, h);   // row_bcast:15 into rows 1 and 3
-    scan_step<0x143, 0xc>(a, b, h);   // row_bcast:31 into rows 2 and 3
+// inclusive scan over the 64 lanes of a wave
+__device__ __forceinline__ void wave_scan(int64_t &a, int64_t &b) {
+    scan_step<0x111, 0xf>(a, b);   // row_shr:1
+    scan_step<0x112, 0xf>(a, b);   // row_shr:2
+    scan_step<0x114, 0xf>(a, b);   // row_shr:4
+    scan_step<0x118, 0xf>(a, b);   // row_shr:8
+    scan_step<0x142, 0xa>(a, b);   // row_bcast:15 into rows 1 and 3
+    scan_step<0x143, 0xc>(a, b);   // row_bcast:31 into rows 2 and 3
 }
 
 // Lane layout: slot = tid / LPS handles K consecutive positions; the LPS
@@ -204,9 +215,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
     __shared__ RmT sRm[3][RP];
     __shared__ int64_t sR[RP * VS];
     __shared__ int64_t sA[NE], sB[NE];
-    __shared__ uint8_t sH[NE];
     __shared__ int64_t sTA[NCH], sTB[NCH];
-    __shared__ uint8_t sTH[NCH];
     extern __shared__ uint64_t sT[];      // scale table (n_cls x VS), sized at launch
     __shared__ int64_t sTC[kMaxCarryThreads * VS];
     __shared__ unsigned long long sMs[VS];
@@ -526,13 +535,13 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     const bool live = ok && !rmv;
                     dp = live ? dp : 0;
                     const int64_t gp = live ? gap : 0;
-                    // one position per lane: c -> max(c + A, B); the round's
-                    // first position closes the segment (carry folded in)
-                    int64_t sa = ok ? dp + gp : 0;
+                    // one position per lane: c -> max(c + A, B), a run head
+                    // written with kHead; the round's first position takes
+                    // the carry (no effect on a head)
+                    int64_t sa = ok ? (head ? kHead : dp + gp) : 0;
                     int64_t sb = ok ? X + dp + gp : 0;
-                    int sh = ok && (head || q == 0);
-                    if (q == 0 && ok && !head) sb = max64(sCarry[os] + sa, sb);
-                    wave_scan(sa, sb, sh);
+                    if (q == 0 && ok) sb = max64(sCarry[os] + sa, sb);
+                    wave_scan(sa, sb);
                     const int64_t Rv = sb;
                     F = Rv - gp;
                     S = F - dp;
@@ -585,10 +594,9 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
 #pragma unroll
         for (int j = 0; j < VPL; j++) { A[j] = 0; B[j] = 0; }
         // nk: positions not kept (removed, or past the round's end)
-        uint32_t before = 0, nk[VPL];
+        uint32_t nk[VPL];
 #pragma unroll
         for (int j = 0; j < VPL; j++) nk[j] = ~0u;
-        bool hh = false;
         if (wact) {
 #pragma unroll
             for (int i = 0; i < K; i++) {
@@ -688,7 +696,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 if (anyh) {                                    // a run starts: reset the fold
 #pragma unroll
                     for (int j = 0; j < VPL; j++) {
-                        A[j] = head ? 0 : A[j];
+                        A[j] = head ? kHead : A[j];            // the carry no longer reaches it
                         B[j] = head ? 0 : B[j];
                     }
                 }
@@ -722,20 +730,16 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     Gp[i][j] = gp;
                     if (live) nk[j] &= ~(1u << i);
                 }
-                hh = hh || head;
-                if (!hh) before |= 1u << i;
             }
         }
         put_next();
-        // slot summaries (variant-major); slot 0 absorbs the carry; slots of
-        // idle waves are the identity (0, 0)
+        // slot summaries (variant-major); slot 0 absorbs the carry and
+        // starts its variant (kHead); slots of idle waves are the identity
 #pragma unroll
         for (int j = 0; j < VPL; j++) {
             const int e = (o0 + j) * NSP + slot;
-            const bool fold = slot == 0 && !hh;
-            sA[e] = A[j];
-            sB[e] = fold ? max64(carry[j] + A[j], B[j]) : B[j];
-            sH[e] = hh || slot == 0;
+            sA[e] = slot == 0 ? kHead : A[j];
+            sB[e] = slot == 0 ? max64(carry[j] + A[j], B[j]) : B[j];
         }
         __syncthreads();                                     // B1
         Dyn<K, VPL> DNb;
@@ -745,76 +749,62 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         // slots all lie past the round's end are skipped
         const int ls = (rn - 1) / ke;                        // last live slot
         int64_t xa[VPL], xb[VPL];
-        int xh[VPL];
         bool cact[VPL];
         if (NS == 64 * VPL) {
             // wave w scans variant w, lane l its VPL consecutive slots: the
             // lane folds them first (keeping each prefix), one wave scan
             // covers the 64 lane totals, and every slot then takes the
-            // prefix of the lanes before it (slot 0 is always a segment
-            // head, so lane 0 needs none)
+            // release of the lanes before it (lane 0 sees 0: its slot 0
+            // already holds the carry)
             const int e0 = wv * NSP + VPL * lane;
             int64_t ta[VPL], tb[VPL];
-            int th[VPL];
 #pragma unroll
             for (int m = 0; m < VPL; m++) {
-                const int64_t am = sA[e0 + m], bm = sB[e0 + m];
-                const int hm = sH[e0 + m];
-                if (m == 0) {
-                    ta[0] = am; tb[0] = bm; th[0] = hm;
-                } else {
-                    ta[m] = hm ? am : ta[m - 1] + am;
-                    tb[m] = hm ? bm : max64(tb[m - 1] + am, bm);
-                    th[m] = hm | th[m - 1];
-                }
+                ta[m] = sA[e0 + m];
+                tb[m] = sB[e0 + m];
+                if (m > 0) compose(ta[m - 1], tb[m - 1], ta[m], tb[m]);
             }
             int64_t pa = ta[VPL - 1], pb = tb[VPL - 1];
-            int ph = th[VPL - 1];
-            wave_scan(pa, pb, ph);
+            wave_scan(pa, pb);
             const int qlo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)pb, 0x138, 0xf, 0xf, false);   // wave_shr:1
             const int qhi = __builtin_amdgcn_update_dpp(0, (int)((uint64_t)pb >> 32), 0x138, 0xf, 0xf, false);
             const int64_t qb = (int64_t)(((uint64_t)(uint32_t)qhi << 32) | (uint32_t)qlo);
 #pragma unroll
-            for (int m = 0; m < VPL; m++) sB[e0 + m] = th[m] ? tb[m] : max64(qb + ta[m], tb[m]);
+            for (int m = 0; m < VPL; m++) sB[e0 + m] = max64(qb + ta[m], tb[m]);
         } else if (NS <= 64 * VPL) {
             // a wave scans whole variants (its VPL chunks hold them): the
             // chunks of one variant follow each other in the same wave
             int64_t pa = 0, pb = 0;
-            int ph = 1;
 #pragma unroll
             for (int j = 0; j < VPL; j++) {
                 const int e = wv * 64 * VPL + j * 64 + lane;
                 cact[j] = __any((e % NS) <= ls);
-                xa[j] = 0; xb[j] = 0; xh[j] = 1;
+                xa[j] = 0; xb[j] = 0;
                 if (cact[j]) {
-                    xa[j] = sA[e]; xb[j] = sB[e]; xh[j] = sH[e];
-                    wave_scan(xa[j], xb[j], xh[j]);
-                    if ((j * 64) % NS != 0 && !xh[j]) {       // continues the last chunk
-                        xb[j] = max64(pb + xa[j], xb[j]);
-                        xa[j] = pa + xa[j];
-                        xh[j] = ph;
-                    }
+                    xa[j] = sA[e]; xb[j] = sB[e];
+                    wave_scan(xa[j], xb[j]);
+                    // after the last chunk (a variant's first slot is a head)
+                    if (j > 0) compose(pa, pb, xa[j], xb[j]);
                     sB[e] = xb[j];
                 }
                 pa = readlane64(xa[j], 63);
                 pb = readlane64(xb[j], 63);
-                ph = __builtin_amdgcn_readlane(xh[j], 63);
             }
         } else {
 #pragma unroll
             for (int j = 0; j < VPL; j++) {
                 const int e = tid + j * NT;
                 cact[j] = __any((e % NS) <= ls);
-                xa[j] = 0; xb[j] = 0; xh[j] = 1;
+                xa[j] = 0; xb[j] = 0;
                 if (cact[j]) {
-                    xa[j] = sA[e]; xb[j] = sB[e]; xh[j] = sH[e];
-                    wave_scan(xa[j], xb[j], xh[j]);
+                    xa[j] = sA[e]; xb[j] = sB[e];
+                    wave_scan(xa[j], xb[j]);
                 }
             }
 #pragma unroll
             for (int j = 0; j < VPL; j++) {
                 const int e = tid + j * NT;
-                if (lane == 63) { sTA[e >> 6] = xa[j]; sTB[e >> 6] = xb[j]; sTH[e >> 6] = (uint8_t)xh[j]; }
+                if (lane == 63) { sTA[e >> 6] = xa[j]; sTB[e >> 6] = xb[j]; }
             }
             __syncthreads();
 #pragma unroll
@@ -822,16 +812,14 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 const int e = tid + j * NT;
                 const int chunk = (e % NS) >> 6;
                 const int first = (e / NS) * (NS >> 6);
-                if (cact[j] && chunk > 0 && !xh[j]) {
+                if (cact[j] && chunk > 0) {
                     int64_t qa = sTA[first], qb = sTB[first];
-                    int qh = sTH[first];
                     for (int c = 1; c < chunk; c++) {
-                        const int64_t ca = sTA[first + c], cb = sTB[first + c];
-                        const int ch = sTH[first + c];
-                        if (!ch) { qb = max64(qb + ca, cb); qa = qa + ca; }
-                        else { qa = ca; qb = cb; qh = ch; }
+                        int64_t ca = sTA[first + c], cb = sTB[first + c];
+                        compose(qa, qb, ca, cb);
+                        qa = ca; qb = cb;
                     }
-                    xb[j] = max64(qb + xa[j], xb[j]); xa[j] = qa + xa[j]; xh[j] = qh;
+                    compose(qa, qb, xa[j], xb[j]);
                 }
             }
 #pragma unroll
@@ -858,7 +846,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 const int tcx = ((flags >> 2) & 63u) * VS + o0;
 #pragma unroll
                 for (int j = 0; j < VPL; j++) {
-                    const int64_t F = ((before >> i) & 1u) ? max64(cin[j] + Dp[i][j], Fl[i][j]) : Fl[i][j];
+                    // positions after a run head hold Dp <= kHead + weights: no effect
+                    const int64_t F = max64(cin[j] + Dp[i][j], Fl[i][j]);
                     rv.x[j] = F + Gp[i][j];
                     fv.x[j] = F;
                     if (START) sv.x[j] = F - Dd[i][j];

@@ -593,10 +593,13 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         int64_t A[VPL], B[VPL];
 #pragma unroll
         for (int j = 0; j < VPL; j++) { A[j] = 0; B[j] = 0; }
-        // nk: positions not kept (removed, or past the round's end)
-        uint32_t nk[VPL];
+        // high word added to a position's finish before the makespan max:
+        // kHead for positions not kept (removed, or past the round's end)
+        uint32_t nkh[K][VPL];
 #pragma unroll
-        for (int j = 0; j < VPL; j++) nk[j] = ~0u;
+        for (int i = 0; i < K; i++)
+#pragma unroll
+            for (int j = 0; j < VPL; j++) nkh[i][j] = (uint32_t)((uint64_t)kHead >> 32);
         if (wact) {
 #pragma unroll
             for (int i = 0; i < K; i++) {
@@ -728,7 +731,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     Fl[i][j] = F;
                     if (START) Dd[i][j] = dp;
                     Gp[i][j] = gp;
-                    if (live) nk[j] &= ~(1u << i);
+                    nkh[i][j] = live ? 0u : (uint32_t)((uint64_t)kHead >> 32);
                 }
             }
         }
@@ -852,7 +855,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     fv.x[j] = F;
                     if (START) sv.x[j] = F - Dd[i][j];
                     // makespan over kept tasks (lanes past V never publish theirs)
-                    ms[j] = max64(ms[j], ((nk[j] >> i) & 1u) ? 0 : F);
+                    ms[j] = max64(ms[j], (int64_t)((uint64_t)F + ((uint64_t)nkh[i][j] << 32)));
                 }
                 // positions past the round's end write their own unused slot
                 // (no young gather reads it); slots past ke would overlap the

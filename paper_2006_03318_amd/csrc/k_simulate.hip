@@ -855,7 +855,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     fv.x[j] = F;
                     if (START) sv.x[j] = F - Dd[i][j];
                     // makespan over kept tasks (lanes past V never publish theirs)
-                    ms[j] = max64(ms[j], (int64_t)((uint64_t)F + ((uint64_t)nkh[i][j] << 32)));
+                    // (positions past ke were not walked: no finish to take)
+                    if (i < ke) ms[j] = max64(ms[j], (int64_t)((uint64_t)F + ((uint64_t)nkh[i][j] << 32)));
                 }
                 // positions past the round's end write their own unused slot
                 // (no young gather reads it); slots past ke would overlap the

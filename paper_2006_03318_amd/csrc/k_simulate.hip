@@ -640,7 +640,11 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
 #pragma unroll
                 for (int j = 0; j < VPL; j++) X[j] = 0;
                 if (any0) {
-                    const Vals<VPL> yn = *reinterpret_cast<const Vals<VPL> *>(&sR[i0 * VS + o0]);
+                    Vals<VPL> yn = *reinterpret_cast<const Vals<VPL> *>(&sR[i0 * VS + o0]);
+                    // read on every lane: the choice below stays a select
+                    // instead of a branch that sinks half of the read
+#pragma unroll
+                    for (int j = 0; j < VPL; j++) asm volatile("" : "+v"(yn.x[j]));
                     const int64_t g0g = UNI ? (int64_t)(uint32_t)w2.w : D.g0gap[i];
 #pragma unroll
                     for (int j = 0; j < VPL; j++) {

@@ -840,6 +840,15 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
 #pragma unroll
         for (int j = 0; j < VPL; j++)
             cin[j] = slot == 0 ? carry[j] : sB[(o0 + j) * NSP + (slot > 0 ? slot - 1 : 0)];
+        // does any lane of the wave end a thread's run in this round (its
+        // release then goes to the thread carries)?  Mostly not.
+        bool anylast = false;
+        if (tcar) {
+            uint32_t lf = 0;
+#pragma unroll
+            for (int i = 0; i < K; i++) lf |= FLk[i];
+            anylast = __any(lf & 2u);
+        }
 #pragma unroll
         for (int i = 0; i < K; i++) {
             const int q = slot * ke + i;
@@ -866,7 +875,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 // (no young gather reads it); slots past ke would overlap the
                 // next slot's positions
                 if (i < ke) *reinterpret_cast<Vals<VPL> *>(&sR[q * VS + o0]) = rv;
-                if (__any(last) && last) *reinterpret_cast<Vals<VPL> *>(&sTC[tcx]) = rv;
+                if (anylast && last) *reinterpret_cast<Vals<VPL> *>(&sTC[tcx]) = rv;
             }
             const bool st = ok && lok;
             gi64 *o = st ? (gi64 *)(a.finish + ((int64_t)U[i] * V + vf)) : dummy;

@@ -139,13 +139,15 @@ __device__ __forceinline__ void compose(int64_t la, int64_t lb, int64_t &a, int6
 
 // one Kogge-Stone step of the max-plus scan across the wave, the left
 // operand taken with a DPP lane shift (lanes without one see the identity
-// (0, 0), as b >= a)
+// (0, 0), as b >= a).  Row shifts write every lane (bound control: 0 where
+// the source lies outside the row), so no lane needs its old value.
 template <int CTRL, int RMASK>
 __device__ __forceinline__ void scan_step(int64_t &a, int64_t &b) {
-    const int alo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)a, CTRL, RMASK, 0xf, false);
-    const int ahi = __builtin_amdgcn_update_dpp(0, (int)((uint64_t)a >> 32), CTRL, RMASK, 0xf, false);
-    const int blo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, RMASK, 0xf, false);
-    const int bhi = __builtin_amdgcn_update_dpp(0, (int)((uint64_t)b >> 32), CTRL, RMASK, 0xf, false);
+    constexpr bool BC = RMASK == 0xf;
+    const int alo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)a, CTRL, RMASK, 0xf, BC);
+    const int ahi = __builtin_amdgcn_update_dpp(0, (int)((uint64_t)a >> 32), CTRL, RMASK, 0xf, BC);
+    const int blo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, RMASK, 0xf, BC);
+    const int bhi = __builtin_amdgcn_update_dpp(0, (int)((uint64_t)b >> 32), CTRL, RMASK, 0xf, BC);
     const int64_t la = (int64_t)(((uint64_t)(uint32_t)ahi << 32) | (uint32_t)alo);
     const int64_t lb = (int64_t)(((uint64_t)(uint32_t)bhi << 32) | (uint32_t)blo);
     compose(la, lb, a, b);
@@ -773,8 +775,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             }
             int64_t pa = ta[VPL - 1], pb = tb[VPL - 1];
             wave_scan(pa, pb);
-            const int qlo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)pb, 0x138, 0xf, 0xf, false);   // wave_shr:1
-            const int qhi = __builtin_amdgcn_update_dpp(0, (int)((uint64_t)pb >> 32), 0x138, 0xf, 0xf, false);
+            const int qlo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)pb, 0x138, 0xf, 0xf, true);   // wave_shr:1
+            const int qhi = __builtin_amdgcn_update_dpp(0, (int)((uint64_t)pb >> 32), 0x138, 0xf, 0xf, true);
             const int64_t qb = (int64_t)(((uint64_t)(uint32_t)qhi << 32) | (uint32_t)qlo);
 #pragma unroll
             for (int m = 0; m < VPL; m++) sB[e0 + m] = max64(qb + ta[m], tb[m]);

@@ -174,10 +174,11 @@ __device__ __forceinline__ void wave_scan(int64_t &a, int64_t &b) {
 // workgroup), so one 8*VPL-byte load or store serves every variant of the
 // lane and the per-position bookkeeping is paid once per VPL variants.
 // Idle lanes keep issuing the same prefetch loads (clamped addresses) and
-// stores (to a dummy target), so the count of memory operations in flight
-// is the same on every path and the wait for the next round's data never
-// includes this round's stores.  Waves whose slots all lie past the end of
-// a round skip the arithmetic (rounds at the end of a phase are ragged).
+// stores (to a dummy target), so within each kind of round the count of
+// memory operations in flight is the same on every path and the wait for
+// the next round's data never includes this round's stores.  Waves whose
+// slots all lie past the end of a round skip the arithmetic (rounds at the
+// end of a phase are ragged).
 //
 // UNI: every variant of the launch enables every edge class that the
 // schedule's gathers use, every scale is a power of two and every duration
@@ -561,12 +562,12 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             }
             put_next();
 #pragma unroll
-            for (int jj = 0; jj < K; jj++) {
+            for (int jj = 0; jj < PS; jj++) {   // the wave's variant slots only
                 const int os = wv + NW * jj;
-                const bool vw_ok = jj < PS && os < VS && v0 + os < a.V;
+                const bool vw_ok = os < VS && v0 + os < a.V;
                 const int64_t vs_ = vw_ok ? v0 + os : 0;
                 gi64 *o = sts[jj] ? (gi64 *)(a.finish + ((int64_t)node * V + vs_)) : dummy;
-                asm volatile("" : "+v"(o));  // one store per slot in either layout
+                asm volatile("" : "+v"(o));  // one unconditional store per slot
                 *o = Fs[jj];
                 if (START) {
                     gi64 *os2 = sts[jj] ? (gi64 *)(a.start + ((int64_t)node * V + vs_)) : dummy;

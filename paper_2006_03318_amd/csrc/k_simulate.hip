@@ -271,6 +271,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
     for (int i = tid; i < kMaxCarryThreads * VS; i += NT) sTC[i] = 0;
     if (tid < VS) {
         sMs[tid] = 0;
+        sCarry[tid] = 0;   // read by a first round that is small (finite, so heads ignore it)
         // per-variant values read inside the loop live in LDS: a register
         // loaded before the loop would make every round wait for all traffic
         sEon[tid] = a.edge_on[v0 + tid < a.V ? v0 + tid : 0];

@@ -240,7 +240,7 @@ dd_status dd_graph_load(int32_t n, int32_t n_threads, const int64_t *in_ptr, con
     TRY(hipMemcpyAsync(&h_err, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "read err");
     TRY(hipStreamSynchronize(s), "sync");
     if (h_err) { st = map_err_bits(h_err); goto fail_out; }
-    if (n > 0) TRY(dd::launch_validate_edges(g, d_in_ptr, d_in_src, edge_cls ? d_ecls : nullptr, err, s), "validate edges");
+    if (n > 0) TRY(dd::launch_validate_edges(g, d_in_ptr, d_in_src, edge_cls ? d_ecls : nullptr, succ, err, s), "validate edges");
     TRY(dd::dalloc_n(&g->rank, N1, s), "alloc rank");
     TRY(dd::dalloc_n(&nxt, N1, s), "alloc");
     TRY(dd::dalloc_n(&nxt2, N1, s), "alloc");

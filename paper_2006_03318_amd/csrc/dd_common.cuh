@@ -73,4 +73,18 @@ __device__ __forceinline__ T load_coherent(const T *p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Atomics on one word that every wave of a launch updates: the atomic is
+// skipped when the word (read device-coherently) already covers the value.
+// The word only grows, so a skip never loses an update, and a launch of
+// thousands of waves does not queue on that word.
+__device__ __forceinline__ void atomic_max_hot(unsigned long long *p, unsigned long long v) {
+    if (v > load_coherent(p)) atomicMax(p, v);
+}
+__device__ __forceinline__ void atomic_or_hot(unsigned long long *p, unsigned long long v) {
+    if (v & ~load_coherent(p)) atomicOr(p, v);
+}
+__device__ __forceinline__ void atomic_or_hot(uint32_t *p, uint32_t v) {
+    if (v & ~load_coherent(p)) atomicOr(p, v);
+}
+
 }  // namespace dd

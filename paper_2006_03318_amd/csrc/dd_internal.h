@@ -150,7 +150,8 @@ inline int grid_for(int64_t n, int bs) {
 hipError_t launch_validate_nodes(const dd_graph *g, const int64_t *in_ptr, int32_t *succ,
                                  int32_t *heads, uint32_t *err, LoadStats *st, hipStream_t s);
 hipError_t launch_validate_edges(const dd_graph *g, const int64_t *in_ptr, const int32_t *in_src,
-                                 const uint8_t *edge_cls, uint32_t *err, hipStream_t s);
+                                 const uint8_t *edge_cls, const int32_t *succ, uint32_t *err,
+                                 hipStream_t s);
 hipError_t launch_rank_chains(const dd_graph *g, const int32_t *succ, int32_t *tmp_nxt,
                               int32_t *tmp_nxt2, int32_t *tmp_rank2, uint32_t *err,
                               hipStream_t s);

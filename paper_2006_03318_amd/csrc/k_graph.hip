@@ -108,7 +108,7 @@ __global__ __launch_bounds__(kBS) void k_validate_nodes(
             e |= ERR_PREV_RANGE;
         } else if (p >= 0) {
             if (tid[p] != t) e |= ERR_PREV_THREAD;
-            else if (atomicAdd(&succ[p], 1) != 0) e |= ERR_SUCC;
+            else succ[p] = (int32_t)u + 1;   // one claimer wins; the others are found later
         } else if (t_ok) {
             if (atomicAdd(&heads[t], 1) != 0) e |= ERR_HEADS;
         }
@@ -157,13 +157,19 @@ __global__ __launch_bounds__(kBS) void k_validate_nodes(
     }
 }
 
+// (runs once the per-task fields are valid: also reports a task named as
+// previous task by two tasks, which left only one of them in succ)
 __global__ __launch_bounds__(kBS) void k_validate_edges(int32_t n, const int64_t *__restrict__ in_ptr,
                                                         const int32_t *__restrict__ in_src,
                                                         const uint8_t *__restrict__ ecls,
+                                                        const int32_t *__restrict__ prev,
+                                                        const int32_t *__restrict__ succ,
                                                         uint32_t *__restrict__ err) {
     const int64_t u = (int64_t)blockIdx.x * kBS + threadIdx.x;
     uint32_t e = 0;
     if (u < n) {
+        const int32_t p = prev[u];
+        if (p >= 0 && succ[p] != (int32_t)u + 1) e |= ERR_SUCC;
         for (int64_t k = in_ptr[u]; k < in_ptr[u + 1]; k++) {
             const int32_t s = in_src[k];
             if (s < 0 || s >= n) e |= ERR_SRC_RANGE;
@@ -216,7 +222,7 @@ __global__ __launch_bounds__(kBS) void k_thread_len(int32_t n, const int32_t *__
                                                     const int32_t *__restrict__ rank,
                                                     int64_t *__restrict__ len) {
     const int64_t u = (int64_t)blockIdx.x * kBS + threadIdx.x;
-    if (u < n && succ[u] == 0) len[tid[u]] = (int64_t)rank[u] + 1;   // last task of its thread
+    if (u < n && succ[u] == 0) len[tid[u]] = (int64_t)rank[u] + 1;   // last task of its thread (no successor)
 }
 
 __global__ __launch_bounds__(kBS) void k_order(int32_t n, const int32_t *__restrict__ tid,
@@ -255,8 +261,8 @@ __global__ __launch_bounds__(kBS) void k_cross_count(
         mask |= (uint64_t)shfl_xor64((int64_t)mask, o);
     }
     if ((threadIdx.x & 63) == 0) {
-        if (e) atomicOr(err, e);
-        if (mask) atomicOr(&st->cross_mask, (unsigned long long)mask);
+        atomic_or_hot(err, e);
+        atomic_or_hot(&st->cross_mask, (unsigned long long)mask);
     }
 }
 
@@ -290,8 +296,10 @@ hipError_t launch_validate_nodes(const dd_graph *g, const int64_t *in_ptr, int32
 }
 
 hipError_t launch_validate_edges(const dd_graph *g, const int64_t *in_ptr, const int32_t *in_src,
-                                 const uint8_t *edge_cls, uint32_t *err, hipStream_t s) {
-    k_validate_edges<<<grid_for(g->n, kBS), kBS, 0, s>>>(g->n, in_ptr, in_src, edge_cls, err);
+                                 const uint8_t *edge_cls, const int32_t *succ, uint32_t *err,
+                                 hipStream_t s) {
+    k_validate_edges<<<grid_for(g->n, kBS), kBS, 0, s>>>(g->n, in_ptr, in_src, edge_cls,
+                                                         g->thread_prev, succ, err);
     return hipGetLastError();
 }
 

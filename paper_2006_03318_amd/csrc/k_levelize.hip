@@ -657,7 +657,7 @@ __global__ __launch_bounds__(kBS) void k_step_width(int64_t nsteps, const int32_
     const int64_t r = (int64_t)blockIdx.x * kBS + threadIdx.x;
     int64_t w = r < nsteps ? (int64_t)(step_ptr[r + 1] - step_ptr[r]) : 0;
     w = wave_max64(w);
-    if ((threadIdx.x & 63) == 0) atomicMax(wmax, (unsigned long long)w);
+    if ((threadIdx.x & 63) == 0) atomic_max_hot(wmax, (unsigned long long)w);
 }
 
 // Kahn levels from the phase schedule (one workgroup, phases in order)
@@ -736,7 +736,7 @@ __global__ __launch_bounds__(kWG) void k_levels(LevelArgs a) {
         }
     }
     lmax = wave_max64(lmax);
-    if ((threadIdx.x & 63) == 0) atomicMax(a.max_level, (unsigned long long)lmax);
+    if ((threadIdx.x & 63) == 0) atomic_max_hot(a.max_level, (unsigned long long)lmax);
 }
 
 __global__ __launch_bounds__(kBS) void k_level_count(int32_t n, const int32_t *__restrict__ level,

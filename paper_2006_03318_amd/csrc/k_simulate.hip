@@ -53,6 +53,14 @@ __device__ __forceinline__ int64_t scaled(int64_t d, const ScaleEntry &se) {
 
 __device__ __forceinline__ int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
 
+// 64-bit value from its two 32-bit halves, as one register pair (left
+// visible as shift-or, the compiler adds the halves to a sum one at a time)
+__device__ __forceinline__ int64_t join64(int lo, int hi) {
+    int64_t r = (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+    asm("" : "+v"(r));
+    return r;
+}
+
 struct PipeArgs {
     const int64_t *gat_ptr;       // [n+1] gathers of each position
     const int32_t *gat_src;       // gathers beyond two per position
@@ -148,15 +156,15 @@ __device__ __forceinline__ void scan_step(int64_t &a, int64_t &b) {
     const int ahi = __builtin_amdgcn_update_dpp(0, (int)((uint64_t)a >> 32), CTRL, RMASK, 0xf, BC);
     const int blo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, RMASK, 0xf, BC);
     const int bhi = __builtin_amdgcn_update_dpp(0, (int)((uint64_t)b >> 32), CTRL, RMASK, 0xf, BC);
-    const int64_t la = (int64_t)(((uint64_t)(uint32_t)ahi << 32) | (uint32_t)alo);
-    const int64_t lb = (int64_t)(((uint64_t)(uint32_t)bhi << 32) | (uint32_t)blo);
+    const int64_t la = join64(alo, ahi);
+    const int64_t lb = join64(blo, bhi);
     compose(la, lb, a, b);
 }
 
 __device__ __forceinline__ int64_t readlane64(int64_t x, int l) {
     const int lo = __builtin_amdgcn_readlane((int)(uint32_t)x, l);
     const int hi = __builtin_amdgcn_readlane((int)((uint64_t)x >> 32), l);
-    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+    return join64(lo, hi);
 }
 
 // inclusive scan over the 64 lanes of a wave
@@ -779,7 +787,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             wave_scan(pa, pb);
             const int qlo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)pb, 0x138, 0xf, 0xf, true);   // wave_shr:1
             const int qhi = __builtin_amdgcn_update_dpp(0, (int)((uint64_t)pb >> 32), 0x138, 0xf, 0xf, true);
-            const int64_t qb = (int64_t)(((uint64_t)(uint32_t)qhi << 32) | (uint32_t)qlo);
+            const int64_t qb = join64(qlo, qhi);
 #pragma unroll
             for (int m = 0; m < VPL; m++) sB[e0 + m] = max64(qb + ta[m], tb[m]);
         } else if (NS <= 64 * VPL) {

@@ -23,16 +23,18 @@ __device__ uint32_t ceil_log2(uint32_t q) {
     return l;
 }
 
+constexpr int kTabBlocks = 512;   // grid-stride blocks: one set of atomics per block
+
 __global__ __launch_bounds__(kBS) void k_scale_table(const dd_ratio *__restrict__ in, int64_t count,
                                                      ScaleEntry *__restrict__ out,
                                                      uint32_t *__restrict__ err,
                                                      unsigned long long *__restrict__ pmax,
                                                      unsigned long long *__restrict__ rmax_bits) {
-    const int64_t i = (int64_t)blockIdx.x * kBS + threadIdx.x;
     uint32_t e = 0, mg = 0;
     int64_t pm = 0;
     int64_t rb = 0;
-    if (i < count) {
+    for (int64_t i = (int64_t)blockIdx.x * kBS + threadIdx.x; i < count;
+         i += (int64_t)gridDim.x * kBS) {
         int32_t p = 1, q = 1;
         if (in) { p = in[i].p; q = in[i].q; }
         ScaleEntry se{0ull, 0u, 0u};
@@ -57,23 +59,38 @@ __global__ __launch_bounds__(kBS) void k_scale_table(const dd_ratio *__restrict_
                 se.shift = l - 2;
                 mg = 1;
             }
-            pm = p;
+            pm = p > pm ? p : pm;
             const double ratio = (double)p / (double)q;
-            rb = (int64_t)__double_as_longlong(ratio);   // order-preserving for ratio >= 0
+            const int64_t b = (int64_t)__double_as_longlong(ratio);   // order-preserving for ratio >= 0
+            rb = b > rb ? b : rb;
         }
         out[i] = se;
     }
+    // wave, then the block's waves through LDS: one set of atomics per block
     pm = wave_max64(pm);
     rb = wave_max64(rb);
     for (int o = 32; o > 0; o >>= 1) {
         e |= (uint32_t)__shfl_xor((int)e, o, 64);
         mg |= (uint32_t)__shfl_xor((int)mg, o, 64);
     }
+    constexpr int NW = kBS / 64;
+    __shared__ int64_t red[4][NW];
+    const int w = threadIdx.x >> 6;
     if ((threadIdx.x & 63) == 0) {
-        if (e) atomicOr(err, e);
-        if (mg) atomicOr(err + 1, mg);
-        atomicMax(pmax, (unsigned long long)pm);
-        atomicMax(rmax_bits, (unsigned long long)rb);
+        red[0][w] = pm; red[1][w] = rb; red[2][w] = e; red[3][w] = mg;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int k = 1; k < NW; k++) {
+            pm = red[0][k] > pm ? red[0][k] : pm;
+            rb = red[1][k] > rb ? red[1][k] : rb;
+            e |= (uint32_t)red[2][k];
+            mg |= (uint32_t)red[3][k];
+        }
+        atomic_or_hot(err, e);
+        atomic_or_hot(err + 1, mg);
+        atomic_max_hot(pmax, (unsigned long long)pm);
+        atomic_max_hot(rmax_bits, (unsigned long long)rb);
     }
 }
 
@@ -86,7 +103,10 @@ hipError_t launch_build_scale_table(const dd_ratio *scale_dev, int32_t n_cls, in
     const int64_t count = (int64_t)n_cls * V;
     unsigned long long *pmax = reinterpret_cast<unsigned long long *>(err + 2);
     unsigned long long *rmax = reinterpret_cast<unsigned long long *>(err + 4);
-    k_scale_table<<<grid_for(count, kBS), kBS, 0, s>>>(scale_dev, count, table, err, pmax, rmax);
+    const int64_t nb = grid_for(count, kBS);
+    if (count > 0)
+        k_scale_table<<<(unsigned)(nb < kTabBlocks ? nb : kTabBlocks), kBS, 0, s>>>(scale_dev, count, table,
+                                                                                   err, pmax, rmax);
     return hipGetLastError();
 }
 

@@ -100,6 +100,14 @@ def test_load_errors():
     g = H.graph(2, [0, 1, 0], [], [1, 2, 3], [0, 0, 0])
     g.thread_prev[2] = -1
     _expect(B.DD_ECHAIN, lambda: _load(g))
+    # two tasks name the same previous task (the thread order forks)
+    g = H.graph(1, [0, 0, 0], [], [1, 2, 3], [0, 0, 0])
+    g.thread_prev[2] = 0
+    _expect(B.DD_ECHAIN, lambda: _load(g))
+    # the same fork deep inside a long thread
+    g = H.graph(1, [0] * 3000, [], [1] * 3000, [0] * 3000)
+    g.thread_prev[2500] = 1700
+    _expect(B.DD_ECHAIN, lambda: _load(g))
     # thread order loops (plus a proper head elsewhere)
     g = H.graph(1, [0, 0, 0], [], [1, 2, 3], [0, 0, 0], thread_order=[[0]])
     g.thread_prev[1] = 2

@@ -59,9 +59,14 @@ __global__ __launch_bounds__(kBS) void k_req_count(int32_t n, Req r, uint64_t ma
     flag[p] = c > 0;
 }
 
-// A candidate packed for the windowed rounds: its order position and its
-// first two requirements (parent position in order space, parent thread);
-// meta = thread of req 0 | thread of req 1 << 8 | requirement count << 16.
+constexpr int kWinT = 16;               // graph threads of the windowed rounds at most
+
+// A candidate packed for the windowed rounds: its order position and, for
+// the first two parent threads (by id) among its requirements, the largest
+// requirement position on each (order space); meta = first thread | second
+// thread << 8 | number of distinct parent threads << 16.  It is blocked when
+// one of those maxima lies at or past its thread's front; only a candidate
+// with parents on three or more threads needs its full requirement list.
 struct alignas(16) CandEnt {
     int32_t pos, g0, g1;
     uint32_t meta;
@@ -84,8 +89,9 @@ __global__ __launch_bounds__(kBS) void k_req_fill(int32_t n, Req r, uint64_t mas
     int64_t o = rptr_by_pos[p];
     req_ptr[i] = o;
     const int32_t u = r.order[p];
-    CandEnt ce{(int32_t)p, 0, 0, 0u};
-    uint32_t nr = 0;
+    int32_t mx[kWinT];                  // largest requirement per parent thread (-1: none)
+#pragma unroll
+    for (int z = 0; z < kWinT; z++) mx[z] = -1;
     for (int64_t k = r.xin_ptr[u]; k < r.xin_ptr[u + 1]; k++) {
         if (!on(mask, r.xin_cls[k])) continue;
         const int32_t s = r.xin_src[k];
@@ -93,13 +99,23 @@ __global__ __launch_bounds__(kBS) void k_req_fill(int32_t n, Req r, uint64_t mas
         const int64_t gp = r.base[ts] + r.rank[s];
         req_chain[o] = ts;
         req_gpos[o] = gp;
-        if (nr == 0) { ce.g0 = (int32_t)gp; ce.meta |= (uint32_t)ts & 0xff; }
-        if (nr == 1) { ce.g1 = (int32_t)gp; ce.meta |= ((uint32_t)ts & 0xff) << 8; }
-        nr++;
+#pragma unroll
+        for (int z = 0; z < kWinT; z++)
+            if (z == ts && (int32_t)gp > mx[z]) mx[z] = (int32_t)gp;
         o++;
     }
-    ce.meta |= (nr < 0xffff ? nr : 0xffffu) << 16;
-    if (pent) pent[i] = ce;
+    if (!pent) return;                  // (more than kWinT threads: no windowed rounds)
+    CandEnt ce{(int32_t)p, 0, 0, 0u};
+    uint32_t nd = 0;
+#pragma unroll
+    for (int z = 0; z < kWinT; z++) {
+        if (mx[z] < 0) continue;
+        if (nd == 0) { ce.g0 = mx[z]; ce.meta |= (uint32_t)z; }
+        if (nd == 1) { ce.g1 = mx[z]; ce.meta |= (uint32_t)z << 8; }
+        nd++;
+    }
+    ce.meta |= nd << 16;
+    pent[i] = ce;
 }
 
 __global__ __launch_bounds__(kBS) void k_cand_base(int32_t T, const int64_t *__restrict__ base,
@@ -276,10 +292,8 @@ __global__ __launch_bounds__(kWG) void k_kahn_rounds(KahnArgs a) {
 // start are ready already, so only a tile that also holds another thread's
 // candidates can look blocked without being so; the search then simply goes
 // on after it.
-constexpr int kWinT = 16;
-constexpr int kWinEnt = 6144;           // LDS candidate entries shared by all threads
+constexpr int kWinBytes = 6144 * 16;    // LDS window of candidate entries, shared by all threads
 constexpr int kRefill = 8;              // window entries loaded per lane at once
-constexpr int kNear = 1;                // candidates per lane and step inside the window
 
 // tile maxima over candidates: tm1[k * T + s] = largest requirement position
 // on thread s among candidates [64k, 64k + 64) (-1 if none); one wave per tile
@@ -330,11 +344,11 @@ struct WinArgs {
 
 __device__ __forceinline__ bool win_blocked(const WinArgs &a, const CandEnt &e, int64_t j,
                                             const int32_t *front) {
-    const uint32_t nr = e.meta >> 16;
+    const uint32_t nd = e.meta >> 16;
     if (e.g0 >= front[e.meta & 0xff]) return true;
-    if (nr > 1 && e.g1 >= front[(e.meta >> 8) & 0xff]) return true;
-    if (nr > 2) {
-        for (int64_t k = a.req_ptr[j] + 2; k < a.req_ptr[j + 1]; k++)
+    if (nd > 1 && e.g1 >= front[(e.meta >> 8) & 0xff]) return true;
+    if (nd > 2) {                        // parents on three or more threads
+        for (int64_t k = a.req_ptr[j]; k < a.req_ptr[j + 1]; k++)
             if (a.req_gpos[k] >= front[a.req_chain[k]]) return true;
     }
     return false;
@@ -342,16 +356,18 @@ __device__ __forceinline__ bool win_blocked(const WinArgs &a, const CandEnt &e, 
 
 // One barrier per round: round r reads the fronts of buffer r & 1 and writes
 // the advanced fronts, plus one flag per thread (advanced, unfinished), into
-// buffer (r + 1) & 1; a buffer is rewritten only two rounds later, after the
-// next barrier.  The fronts of every round go to a table from which the
-// segments are cut afterwards (k_win_seg_*).
+// buffer (r + 1) & 1 and r & 1; a buffer is rewritten only two rounds later,
+// after the next barrier.  The fronts of every round go to a table from which
+// the segments are cut afterwards (k_win_seg_*).
 __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
     static_assert(kWG / 64 >= kWinT, "a wave per graph thread");
-    __shared__ CandEnt s_win[kWinEnt + 64];
-    __shared__ int32_t s_front[2][kWinT];
+    constexpr int kWinE = kWinBytes / (int)sizeof(CandEnt);
+    __shared__ CandEnt s_win[kWinE + 64];
+    __shared__ __align__(16) int32_t s_front[2][kWinT];
     __shared__ __align__(16) uint8_t s_adv[2][16], s_unf[2][16];   // flags of graph threads
     const int lane = threadIdx.x & 63;
-    const int t = threadIdx.x >> 6;               // wave t walks graph thread t
+    // wave t walks graph thread t (uniform: the wave's state stays scalar)
+    const int t = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int W = 1 << a.wlog;
     const int T = a.T;
     const bool mine = t < T;
@@ -364,77 +380,68 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
     int f = mine ? (int)a.base[t] : 0;             // the wave's own front (also in LDS for the others)
     if (threadIdx.x < 32) reinterpret_cast<uint8_t *>(s_adv)[threadIdx.x] = 0;
     if (threadIdx.x < 32) reinterpret_cast<uint8_t *>(s_unf)[threadIdx.x] = 0;
+    if (threadIdx.x < 2 * kWinT) s_front[0][threadIdx.x] = 0;   // fronts past T stay 0
+    __syncthreads();
     if (threadIdx.x < T) {
         s_front[0][threadIdx.x] = (int32_t)a.base[threadIdx.x];
         a.ftab[threadIdx.x] = (int32_t)a.base[threadIdx.x];
     }
     __syncthreads();
     int64_t round = 0;
+    int32_t frow = 0;                             // front table rows of the current batch
     for (;;) {
         const int cur = (int)(round & 1);
-        const int32_t *front = s_front[cur];
-        // refill this thread's window when less than half of it lies ahead:
-        // all loads of a refill are in flight together (one memory latency)
-        if (mine) {
-            if (wend < ce && wend - ci < (W >> 1)) {
-                const int nend = ci + W < ce ? ci + W : ce;
-                const int from = wend > ci ? wend : ci;     // entries behind ci are spent
-                for (int j0 = from; j0 < nend; j0 += kRefill * 64) {
-                    CandEnt v[kRefill];
+        // refill this thread's window when less than half of it lies ahead
+        if (mine && wend < ce && wend - ci < (W >> 1)) {
+            // all loads of a refill are in flight together (one memory latency)
+            const int nend = ci + W < ce ? ci + W : ce;
+            const int from = wend > ci ? wend : ci;     // entries behind ci are spent
+            for (int j0 = from; j0 < nend; j0 += kRefill * 64) {
+                CandEnt v[kRefill];
 #pragma unroll
-                    for (int r = 0; r < kRefill; r++) {
-                        const int j = j0 + r * 64 + lane;
-                        v[r] = a.pent[j < nend ? j : from];
-                    }
-#pragma unroll
-                    for (int r = 0; r < kRefill; r++) {   // past the end: a spare slot
-                        const int j = j0 + r * 64 + lane;
-                        CandEnt *dst = j < nend ? &win[j & (W - 1)] : &s_win[kWinEnt + lane];
-                        *dst = v[r];
-                    }
+                for (int r = 0; r < kRefill; r++) {
+                    const int j = j0 + r * 64 + lane;
+                    v[r] = a.pent[j < nend ? j : from];
                 }
-                wend = nend;
+#pragma unroll
+                for (int r = 0; r < kRefill; r++) {   // past the end: a spare slot
+                    const int j = j0 + r * 64 + lane;
+                    CandEnt *dst = j < nend ? &win[j & (W - 1)] : &s_win[kWinE + lane];
+                    *dst = v[r];
+                }
             }
+            wend = nend;
         }
-        // A: advance each thread's front past its ready candidates
+        // advance this thread's front past its ready candidates
         if (mine) {
             int cnew = ce;
             int npos = end;                        // order position of candidate cnew (end if none)
+            const int32_t *front = s_front[cur];
             if (f < end) {
                 for (;;) {
                     if (ci >= ce) { cnew = ce; break; }
                     if (ci < wend) {
-                        // kNear x 64 candidates from the LDS window, the reads
-                        // of all of them in flight together
                         const int lim = wend < ce ? wend : ce;
-                        bool bl[kNear];
-                        int ep[kNear];
-#pragma unroll
-                        for (int r = 0; r < kNear; r++) {
-                            const int j = ci + r * 64 + lane;
-                            const CandEnt e = win[j & (W - 1)];
-                            bl[r] = j < lim && win_blocked(a, e, j, front);
-                            ep[r] = e.pos;
+                        const int j = ci + lane;
+                        const CandEnt e = win[j & (W - 1)];
+                        const bool bl = j < lim && win_blocked(a, e, j, front);
+                        const unsigned long long bal = __ballot(bl);
+                        if (bal) {
+                            const int L = __ffsll((long long)bal) - 1;
+                            cnew = ci + L;
+                            npos = __builtin_amdgcn_readlane(e.pos, L);   // the finder's entry
+                            break;
                         }
-                        bool hit = false;
-#pragma unroll
-                        for (int r = 0; r < kNear; r++) {
-                            const unsigned long long bal = __ballot(bl[r]);
-                            if (bal && !hit) {
-                                const int L = __ffsll((long long)bal) - 1;
-                                cnew = ci + r * 64 + L;
-                                npos = __builtin_amdgcn_readlane(ep[r], L);   // the finder's entry
-                                hit = true;
-                            }
-                        }
-                        if (hit) break;
-                        ci = ci + kNear * 64 < lim ? ci + kNear * 64 : lim;
+                        ci = ci + 64 < lim ? ci + 64 : lim;
                     } else {
                         // past the window (a long ready run): tiles of 4096,
                         // then of 64, then single candidates, 64 per probe
-                        int32_t fr[kWinT];
+                        int32_t fr[kWinT];         // the round's fronts (wave-uniform)
 #pragma unroll
-                        for (int ts = 0; ts < kWinT; ts++) fr[ts] = ts < T ? front[ts] : 0;
+                        for (int q = 0; q < kWinT / 4; q++) {
+                            const int4 v = reinterpret_cast<const int4 *>(front)[q];
+                            fr[4 * q] = v.x; fr[4 * q + 1] = v.y; fr[4 * q + 2] = v.z; fr[4 * q + 3] = v.w;
+                        }
                         auto tile_blocked = [&](const int32_t *row) {
                             bool b = false;
 #pragma unroll
@@ -460,13 +467,13 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
                             pos = pos > (L1 << 6) ? pos : (L1 << 6);
                             const int64_t end1 = ce < ((L1 + 1) << 6) ? ce : ((L1 + 1) << 6);
                             const int64_t j = pos + lane;
-                            const CandEnt e0 = a.pent[j < end1 ? j : pos];
-                            const bool b0 = j < end1 && win_blocked(a, e0, j, front);
+                            const CandEnt e1 = a.pent[j < end1 ? j : pos];
+                            const bool b0 = j < end1 && win_blocked(a, e1, j, front);
                             const unsigned long long bal0 = __ballot(b0);
                             if (bal0) {
                                 const int L = __ffsll((long long)bal0) - 1;
                                 cnew = (int)(pos + L);
-                                npos = __builtin_amdgcn_readlane(e0.pos, L);
+                                npos = __builtin_amdgcn_readlane(e1.pos, L);
                                 break;
                             }
                             pos = end1;
@@ -482,8 +489,13 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
                 s_front[cur ^ 1][t] = nf;
                 s_adv[cur][t] = nf > f;
                 s_unf[cur][t] = f < end;
-                a.ftab[(round + 1) * T + t] = nf;
             }
+            // front table row round + 1: lane (round & 63) keeps it until a
+            // batch of 64 rows goes out in one store (a store each round would
+            // make the next round wait for it)
+            const int slotr = (int)(round & 63);
+            frow = lane == slotr ? nf : frow;
+            if (slotr == 63) a.ftab[(round - 63 + lane + 1) * T + t] = frow;
             ci = cnew;
             f = nf;
         }
@@ -493,9 +505,15 @@ __global__ __launch_bounds__(kWG) void k_kahn_win(WinArgs a) {
         const uint4 av = *reinterpret_cast<const uint4 *>(s_adv[cur]);
         const bool unf = (uf.x | uf.y | uf.z | uf.w) != 0;
         const bool adv = (av.x | av.y | av.z | av.w) != 0;
-        if (!unf) break;
-        if (!adv) {
-            if (threadIdx.x == 0) atomicOr(a.err, ERR_KAHN_CYCLE);
+        if (!unf || !adv) {
+            if (!unf) {
+                // rows of the last, partial batch
+                const int slotr = (int)(round & 63);
+                if (mine && slotr != 63 && lane <= slotr)
+                    a.ftab[(round - slotr + lane + 1) * T + t] = frow;
+            } else if (threadIdx.x == 0) {
+                atomicOr(a.err, ERR_KAHN_CYCLE);
+            }
             break;
         }
         round++;
@@ -861,7 +879,7 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
     CK(hipGetLastError());
     if (windowed) {
         int wlog = 6;                                  // 2^wlog entries per thread
-        while ((int64_t)T << (wlog + 1) <= kWinEnt) wlog++;
+        while ((int64_t)T << (wlog + 1) <= kWinBytes / (int64_t)sizeof(CandEnt)) wlog++;
         CK(dalloc_n(&ftab, (size_t)(n + 2) * T, s));
         const int64_t C1 = (h_C + 63) / 64, C2 = (C1 + 63) / 64;
         CK(dalloc_n(&tm1, (size_t)(C1 > 0 ? C1 : 1) * T, s));

@@ -936,9 +936,10 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
 // Removal bits per schedule position for each workgroup's VS variants:
 // rmp[g][q] = bits g*VS .. g*VS+VS-1 of task pos_node[q]'s removal row.
 // A block transposes 128 positions x 64 words through LDS: the row reads are
-// contiguous, and every lane writes 16 bytes of one workgroup's row (rows
-// are padded to a multiple of 16 bytes).
-template <int VS, typename RmT>
+// contiguous (16 bytes per lane when rows are 16-byte aligned), and every
+// lane writes 16 bytes of one workgroup's row (rows are padded to a multiple
+// of 16 bytes).
+template <int VS, typename RmT, bool V4>
 __global__ __launch_bounds__(256) void k_rm_pos(int64_t n, int64_t stride, int32_t W, int32_t nwg,
                                                 const int32_t *__restrict__ pos_node,
                                                 const uint32_t *__restrict__ rm,
@@ -949,19 +950,40 @@ __global__ __launch_bounds__(256) void k_rm_pos(int64_t n, int64_t stride, int32
     __shared__ uint32_t tile[TP][65];
     const int64_t q0 = (int64_t)blockIdx.x * TP;
     const int w0 = blockIdx.y * 64;
-    constexpr int LD = TP * 64 / 256;             // words loaded per lane, all in flight
-    uint32_t v[LD];
+    if constexpr (V4) {
+        // 16 lanes per row, 16 rows per pass, all 8 passes in flight (W % 4 == 0)
+        constexpr int LD = TP * 16 / 256;
+        uint4 v[LD];
 #pragma unroll
-    for (int r = 0; r < LD; r++) {
-        const int i = threadIdx.x + r * 256;
-        const int64_t q = q0 + (i >> 6);
-        const int w = w0 + (i & 63);
-        v[r] = (q < n && w < W) ? rm[(int64_t)pos_node[q < n ? q : 0] * W + (w < W ? w : 0)] : 0u;
-    }
+        for (int r = 0; r < LD; r++) {
+            const int i = threadIdx.x + r * 256;
+            const int64_t q = q0 + (i >> 4);
+            const int w = w0 + (i & 15) * 4;
+            const bool ok = q < n && w < W;
+            v[r] = ok ? *reinterpret_cast<const uint4 *>(rm + (int64_t)pos_node[q] * W + w)
+                      : make_uint4(0u, 0u, 0u, 0u);
+        }
 #pragma unroll
-    for (int r = 0; r < LD; r++) {
-        const int i = threadIdx.x + r * 256;
-        tile[i >> 6][i & 63] = v[r];
+        for (int r = 0; r < LD; r++) {
+            const int i = threadIdx.x + r * 256;
+            uint32_t *t = &tile[i >> 4][(i & 15) * 4];
+            t[0] = v[r].x; t[1] = v[r].y; t[2] = v[r].z; t[3] = v[r].w;
+        }
+    } else {
+        constexpr int LD = TP * 64 / 256;         // words loaded per lane, all in flight
+        uint32_t v[LD];
+#pragma unroll
+        for (int r = 0; r < LD; r++) {
+            const int i = threadIdx.x + r * 256;
+            const int64_t q = q0 + (i >> 6);
+            const int w = w0 + (i & 63);
+            v[r] = (q < n && w < W) ? rm[(int64_t)pos_node[q < n ? q : 0] * W + (w < W ? w : 0)] : 0u;
+        }
+#pragma unroll
+        for (int r = 0; r < LD; r++) {
+            const int i = threadIdx.x + r * 256;
+            tile[i >> 6][i & 63] = v[r];
+        }
     }
     __syncthreads();
     const int g0 = (int)((int64_t)w0 * 32 / VS);
@@ -1047,8 +1069,12 @@ hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants
     }
     if (sch->n > 0) {
         const dim3 tg((unsigned)((sch->n + 127) / 128), (unsigned)((var->W + 63) / 64));
-        k_rm_pos<VS, RmT><<<tg, 256, 0, s>>>(sch->n, rstride, var->W, grid, sch->pos_node,
-                                             var->rm_bits, rmp);
+        if (var->W % 4 == 0)
+            k_rm_pos<VS, RmT, true><<<tg, 256, 0, s>>>(sch->n, rstride, var->W, grid, sch->pos_node,
+                                                       var->rm_bits, rmp);
+        else
+            k_rm_pos<VS, RmT, false><<<tg, 256, 0, s>>>(sch->n, rstride, var->W, grid, sch->pos_node,
+                                                        var->rm_bits, rmp);
     }
     if (ns > 0) k_round_count<<<grid_for(ns, 256), 256, 0, s>>>(ns, sch->step_ptr, RP, cnt);
     e = scan_exclusive(cnt, cnt, ns, s);

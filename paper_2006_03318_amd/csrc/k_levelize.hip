@@ -118,12 +118,16 @@ __global__ __launch_bounds__(kBS) void k_req_fill(int32_t n, Req r, uint64_t mas
     pent[i] = ce;
 }
 
-__global__ __launch_bounds__(kBS) void k_cand_base(int32_t T, const int64_t *__restrict__ base,
+// (also closes the requirement lists: req_ptr[C] = R, from the scan totals)
+__global__ __launch_bounds__(kBS) void k_cand_base(int32_t T, int64_t n, const int64_t *__restrict__ base,
                                                    const int64_t *__restrict__ cidx,
+                                                   const int64_t *__restrict__ rptr,
+                                                   int64_t *__restrict__ req_ptr,
                                                    int64_t *__restrict__ cbase,
                                                    int64_t *__restrict__ front,
                                                    int64_t *__restrict__ ci) {
     const int64_t t = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (t == 0) req_ptr[cidx[n]] = rptr[n];
     if (t > T) return;
     cbase[t] = cidx[base[t]];
     if (t < T) {
@@ -297,13 +301,15 @@ constexpr int kRefill = 8;              // window entries loaded per lane at onc
 
 // tile maxima over candidates: tm1[k * T + s] = largest requirement position
 // on thread s among candidates [64k, 64k + 64) (-1 if none); one wave per tile
-__global__ __launch_bounds__(kBS) void k_tile_max1(int64_t C, int32_t T,
+__global__ __launch_bounds__(kBS) void k_tile_max1(const int64_t *__restrict__ pC, int32_t T,
                                                    const int64_t *__restrict__ req_ptr,
                                                    const int32_t *__restrict__ req_chain,
                                                    const int64_t *__restrict__ req_gpos,
                                                    int32_t *__restrict__ tm1) {
+    const int64_t C = *pC;                // candidates (the grid covers every position)
     const int64_t j = (int64_t)blockIdx.x * kBS + threadIdx.x;
     const int64_t k = j >> 6;
+    if ((k << 6) >= C) return;           // whole waves past the last tile
     const bool ok = j < C;
     const int64_t q0 = ok ? req_ptr[j] : 0, q1 = ok ? req_ptr[j + 1] : 0;
     for (int32_t ts = 0; ts < T; ts++) {
@@ -316,11 +322,13 @@ __global__ __launch_bounds__(kBS) void k_tile_max1(int64_t C, int32_t T,
 }
 
 // tm2[m * T + s] = maximum of tm1 over tiles [64m, 64m + 64)
-__global__ __launch_bounds__(kBS) void k_tile_max2(int64_t C1, int32_t T,
+__global__ __launch_bounds__(kBS) void k_tile_max2(const int64_t *__restrict__ pC, int32_t T,
                                                    const int32_t *__restrict__ tm1,
                                                    int32_t *__restrict__ tm2) {
+    const int64_t C1 = (*pC + 63) / 64;   // tiles of 64 candidates
     const int64_t k = (int64_t)blockIdx.x * kBS + threadIdx.x;
     const int64_t m = k >> 6;
+    if ((m << 6) >= C1) return;          // whole waves past the last tile
     for (int32_t ts = 0; ts < T; ts++) {
         int64_t r = k < C1 ? tm1[k * T + ts] : -1;
         r = wave_max64(r);
@@ -810,6 +818,8 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
     const int64_t n = g->n;
     const int32_t T = g->n_threads;
     const int64_t N1 = n + 1;
+    const int64_t Cmax = n;                  // candidates <= tasks
+    const int64_t Rmax = g->n_cross;         // requirements <= cross edges
     int64_t *cnt = nullptr, *flag = nullptr, *cidx = nullptr, *rptr = nullptr, *cand_pos = nullptr,
             *req_ptr = nullptr, *req_gpos = nullptr, *cbase = nullptr, *front = nullptr,
             *ci = nullptr, *nfront = nullptr, *nci = nullptr, *seg_start = nullptr,
@@ -823,7 +833,6 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
     uint32_t *err = nullptr;
     unsigned long long *wmax = nullptr;
     int64_t h_res[2] = {0, 0};
-    int64_t h_C = 0, h_R = 0;
     uint32_t h_err = 0;
     unsigned long long h_w = 0;
     Req rq{g->thread_base, g->order, g->rank, g->thread_id, g->xin_ptr, g->xin_src, g->xin_cls};
@@ -849,14 +858,12 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
     }
     CK(scan_exclusive(flag, cidx, n, s));
     CK(scan_exclusive(cnt, rptr, n, s));
-    CK(hipMemcpyAsync(&h_C, cidx + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
-    CK(hipMemcpyAsync(&h_R, rptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
-    CK(hipStreamSynchronize(s));
-    CK(dalloc_n(&cand_pos, (size_t)h_C + 1, s));
-    CK(dalloc_n(&req_ptr, (size_t)h_C + 1, s));
-    CK(dalloc_n(&req_chain, (size_t)h_R + 1, s));
-    CK(dalloc_n(&req_gpos, (size_t)h_R + 1, s));
-    if (windowed) CK(dalloc_n(&pent, (size_t)h_C + 1, s));
+    // sized by their bounds, so no count has to come back to the host first
+    CK(dalloc_n(&cand_pos, (size_t)Cmax + 1, s));
+    CK(dalloc_n(&req_ptr, (size_t)Cmax + 1, s));
+    CK(dalloc_n(&req_chain, (size_t)Rmax + 1, s));
+    CK(dalloc_n(&req_gpos, (size_t)Rmax + 1, s));
+    if (windowed) CK(dalloc_n(&pent, (size_t)Cmax + 1, s));
     CK(dalloc_n(&cbase, (size_t)T + 1, s));
     CK(dalloc_n(&front, (size_t)T, s));
     CK(dalloc_n(&ci, (size_t)T, s));
@@ -873,22 +880,21 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
                                       req_chain, req_gpos, pent);
         CK(hipGetLastError());
     }
-    CK(hipMemcpyAsync(req_ptr + h_C, &h_R, sizeof(int64_t), hipMemcpyHostToDevice, s));
-    k_cand_base<<<grid_for((int64_t)T + 1, kBS), kBS, 0, s>>>(T, g->thread_base, cidx, cbase,
-                                                               front, ci);
+    k_cand_base<<<grid_for((int64_t)T + 1, kBS), kBS, 0, s>>>(T, n, g->thread_base, cidx, rptr,
+                                                               req_ptr, cbase, front, ci);
     CK(hipGetLastError());
     if (windowed) {
         int wlog = 6;                                  // 2^wlog entries per thread
         while ((int64_t)T << (wlog + 1) <= kWinBytes / (int64_t)sizeof(CandEnt)) wlog++;
         CK(dalloc_n(&ftab, (size_t)(n + 2) * T, s));
-        const int64_t C1 = (h_C + 63) / 64, C2 = (C1 + 63) / 64;
+        const int64_t C1 = (Cmax + 63) / 64, C2 = (C1 + 63) / 64;   // tiles at most
         CK(dalloc_n(&tm1, (size_t)(C1 > 0 ? C1 : 1) * T, s));
         CK(dalloc_n(&tm2, (size_t)(C2 > 0 ? C2 : 1) * T, s));
-        if (h_C > 0) {
-            k_tile_max1<<<grid_for(C1 * 64, kBS), kBS, 0, s>>>(h_C, T, req_ptr, req_chain, req_gpos,
-                                                               tm1);
+        if (n > 0) {
+            k_tile_max1<<<grid_for(C1 * 64, kBS), kBS, 0, s>>>(cidx + n, T, req_ptr, req_chain,
+                                                               req_gpos, tm1);
             CK(hipGetLastError());
-            k_tile_max2<<<grid_for(C2 * 64, kBS), kBS, 0, s>>>(C1, T, tm1, tm2);
+            k_tile_max2<<<grid_for(C2 * 64, kBS), kBS, 0, s>>>(cidx + n, T, tm1, tm2);
             CK(hipGetLastError());
         }
         WinArgs wa{T, wlog, g->thread_base, cbase, pent, req_ptr, req_chain, req_gpos,

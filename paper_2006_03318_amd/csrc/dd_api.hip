@@ -260,14 +260,16 @@ dd_status dd_graph_load(int32_t n, int32_t n_threads, const int64_t *in_ptr, con
     } else {
         TRY(hipMemsetAsync(g->xin_ptr, 0, sizeof(int64_t), s), "memset");
     }
+    // cross-edge lists sized by the edge count (an upper bound), so they are
+    // filled before the one read-back of the counts and error bits
+    TRY(dd::dalloc_n(&g->xin_src, (size_t)E + 1, s), "alloc");
+    TRY(dd::dalloc_n(&g->xin_cls, (size_t)E + 1, s), "alloc");
+    if (n > 0) TRY(dd::launch_cross_fill(g, d_in_ptr, d_in_src, edge_cls ? d_ecls : nullptr, s), "cross fill");
     TRY(hipMemcpyAsync(&h_err, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "read err");
     TRY(hipMemcpyAsync(&g->n_cross, g->xin_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s), "read");
     TRY(hipMemcpyAsync(&hs, stats, sizeof(hs), hipMemcpyDeviceToHost, s), "read stats");
     TRY(hipStreamSynchronize(s), "sync");
     if (h_err) { st = map_err_bits(h_err); goto fail_out; }
-    TRY(dd::dalloc_n(&g->xin_src, (size_t)g->n_cross + 1, s), "alloc");
-    TRY(dd::dalloc_n(&g->xin_cls, (size_t)g->n_cross + 1, s), "alloc");
-    if (n > 0) TRY(dd::launch_cross_fill(g, d_in_ptr, d_in_src, edge_cls ? d_ecls : nullptr, s), "cross fill");
     g->dsum = ((__int128)hs.dsum_hi << 32) + (__int128)hs.dsum_lo;
     {
         const __int128 gs = ((__int128)hs.gsum_hi << 32) + (__int128)hs.gsum_lo;

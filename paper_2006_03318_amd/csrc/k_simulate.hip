@@ -493,11 +493,17 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     const int64_t vwj = vs_ >> 5;
                     const uint64_t eo = sEon[os];
                     const bool rmv = (rb >> os) & 1u;
+                    // the LDS reads that depend on the record, issued together
+                    int64_t yn = sR[i0 * VS + os];
+                    int64_t tcv = sTC[tcx + os];
+                    uint64_t tev = TLDS ? sT[cls * VS + os] : 0ull;
+                    int64_t crv = sCarry[os];
+                    asm volatile("" : "+v"(yn), "+v"(tcv), "+v"(tev), "+v"(crv));
                     int64_t X;
                     {
                         const int64_t g0g = UNI ? (int64_t)(uint32_t)w2.w : D.g0gap[jj];
                         const int64_t ro = D.f0[jj].x[0] + (((D.r0w[jj] >> bit) & 1u) ? 0 : g0g);
-                        const int64_t rel = old0 ? ro : sR[i0 * VS + os];
+                        const int64_t rel = old0 ? ro : yn;
                         const bool on = has0 && (all_on || cls_on(eo, c0));
                         X = on ? rel : 0;
                     }
@@ -512,7 +518,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                         const bool on = has1 && (all_on || cls_on(eo, c1));
                         X = on ? max64(X, rel) : X;
                     }
-                    if (tcar) X = head ? max64(X, sTC[tcx + os]) : X;
+                    if (tcar) X = head ? max64(X, tcv) : X;
                     if (extra) {
                         const int64_t e1 = a.gat_ptr[r0 + q + 1];
                         for (int64_t e = a.gat_ptr[r0 + q] + 2; e < e1; e++) {
@@ -532,10 +538,10 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     }
                     int64_t dp;
                     if (UNI) {
-                        const uint64_t te = sT[cls * VS + os];
+                        const uint64_t te = tev;
                         dp = (int64_t)(((uint64_t)(uint32_t)dur * (uint32_t)te) >> ((uint32_t)(te >> 32) & 0xff));
                     } else if (TLDS) {
-                        const uint64_t te = sT[cls * VS + os];
+                        const uint64_t te = tev;
                         if (shift_only) {
                             dp = (int64_t)(((uint64_t)dur * (uint32_t)te) >> ((uint32_t)(te >> 32) & 0xff));
                         } else {
@@ -552,7 +558,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     // the carry (no effect on a head)
                     int64_t sa = ok ? (head ? kHead : dp + gp) : 0;
                     int64_t sb = ok ? X + dp + gp : 0;
-                    if (q == 0 && ok) sb = max64(sCarry[os] + sa, sb);
+                    if (q == 0 && ok) sb = max64(crv + sa, sb);
                     wave_scan(sa, sb);
                     const int64_t Rv = sb;
                     F = Rv - gp;

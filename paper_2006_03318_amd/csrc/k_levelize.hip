@@ -297,7 +297,7 @@ __global__ __launch_bounds__(kWG) void k_kahn_rounds(KahnArgs a) {
 // candidates can look blocked without being so; the search then simply goes
 // on after it.
 constexpr int kWinBytes = 6144 * 16;    // LDS window of candidate entries, shared by all threads
-constexpr int kRefill = 8;              // window entries loaded per lane at once
+constexpr int kRefill = 16;             // window entries loaded per lane at once
 
 // tile maxima over candidates: tm1[k * T + s] = largest requirement position
 // on thread s among candidates [64k, 64k + 64) (-1 if none); one wave per tile

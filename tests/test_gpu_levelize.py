@@ -49,6 +49,22 @@ def test_random_steps(seed):
     assert np_ == (int(ph.max()) + 1 if g.n else 0)
 
 
+@pytest.mark.parametrize("n", [63, 64, 65, 66, 127, 128, 129, 130])
+def test_ping_pong_round_counts(n):
+    """Two threads that hand over at every task: one Kahn round per task, so
+    the round count crosses the 64-row batches in which the rounds' fronts
+    are written (a last batch that is full, one row short, one row over)."""
+    require_gpu()
+    thread = [i % 2 for i in range(n)]
+    edges = [(i - 1, i) for i in range(1, n)]
+    g = H.graph(2, thread, edges, [3 + i % 5 for i in range(n)], [i % 2 for i in range(n)])
+    lv, ph = O.steps(g, 1)
+    gp, nph, _ = _steps_gpu(g, 1, B.DD_PHASES)
+    say("ping-pong", n, "phases", nph)
+    assert nph == int(ph.max()) + 1
+    assert np.array_equal(gp, ph)
+
+
 @pytest.mark.parametrize("k", [1, 2, 3, 4])
 def test_config_steps(k):
     require_gpu()

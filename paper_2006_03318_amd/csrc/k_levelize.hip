@@ -538,29 +538,47 @@ __global__ __launch_bounds__(kBS) void k_win_seg_count(int64_t R, int32_t T,
     if (i < R * T) cnt[i] = ftab[i + T] > ftab[i];
 }
 
+// The position offset of segment (r, t) comes straight from the front table:
+// every thread's advance before round r, plus the advances of lower threads
+// in round r.  nseg[0] receives the segment count; seg_off[nseg] = n.
 __global__ __launch_bounds__(kBS) void k_win_seg_fill(int64_t R, int32_t T,
                                                       const int32_t *__restrict__ ftab,
                                                       const int64_t *__restrict__ off,
                                                       int64_t *__restrict__ seg_start,
                                                       int64_t *__restrict__ seg_len,
+                                                      int64_t *__restrict__ seg_off,
                                                       int32_t *__restrict__ seg_step,
-                                                      int64_t *__restrict__ step_seg) {
+                                                      int64_t *__restrict__ step_seg,
+                                                      int64_t *__restrict__ nseg) {
     const int64_t i = (int64_t)blockIdx.x * kBS + threadIdx.x;
     if (i > R * T) return;
     if (i % T == 0) step_seg[i / T] = off[i];          // i == R*T gives the total
-    if (i == R * T) return;
+    const int64_t r = i / T;
+    const int t = (int)(i % T);
+    if (i == R * T) {
+        nseg[0] = off[i];
+        int64_t done = 0;
+        for (int z = 0; z < T; z++) done += ftab[R * T + z] - ftab[z];
+        seg_off[off[i]] = done;
+        return;
+    }
     const int32_t f0 = ftab[i], f1 = ftab[i + T];
     if (f1 > f0) {
+        int64_t o = 0;
+        for (int z = 0; z < T; z++) o += ftab[r * T + z] - ftab[z];
+        for (int z = 0; z < t; z++) o += ftab[(r + 1) * T + z] - ftab[r * T + z];
         const int64_t sidx = off[i];
         seg_start[sidx] = f0;
         seg_len[sidx] = f1 - f0;
-        seg_step[sidx] = (int32_t)(i / T);
+        seg_off[sidx] = o;
+        seg_step[sidx] = (int32_t)r;
     }
 }
 
 // positions in step order: segment of each position by binary search
 __global__ __launch_bounds__(kBS) void k_positions(
-    int64_t n, int64_t nseg, const int64_t *__restrict__ seg_off, const int64_t *__restrict__ seg_start,
+    int64_t n, const int64_t *__restrict__ pnseg, const int64_t *__restrict__ seg_off,
+    const int64_t *__restrict__ seg_start,
     const int32_t *__restrict__ seg_step, const int32_t *__restrict__ order,
     const int64_t *__restrict__ dur, const int64_t *__restrict__ gap,
     const uint16_t *__restrict__ cls, int32_t *__restrict__ pos_node,
@@ -569,6 +587,7 @@ __global__ __launch_bounds__(kBS) void k_positions(
     int32_t *__restrict__ node_step) {
     const int64_t q = (int64_t)blockIdx.x * kBS + threadIdx.x;
     if (q >= n) return;
+    const int64_t nseg = *pnseg;
     int64_t lo = 0, hi = nseg - 1;          // last segment with seg_off <= q
     while (lo < hi) {
         const int64_t mid = (lo + hi + 1) >> 1;
@@ -926,14 +945,15 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
         }
         CK(scan_exclusive(seg_cnt, seg_cnt, RT, s));
         k_win_seg_fill<<<grid_for(RT + 1, kBS), kBS, 0, s>>>(R, T, ftab, seg_cnt, seg_start,
-                                                             seg_len, seg_step, step_seg);
+                                                             seg_len, seg_off, seg_step, step_seg,
+                                                             result + 1);
         CK(hipGetLastError());
-        CK(hipMemcpyAsync(&h_res[1], seg_cnt + RT, sizeof(int64_t), hipMemcpyDeviceToHost, s));
-        CK(hipStreamSynchronize(s));
     }
     {
-        const int64_t nph = h_res[0], nseg = h_res[1];
-        CK(scan_exclusive(seg_len, seg_off, nseg, s));
+        // (the windowed rounds leave the segment count on the device; it
+        // comes back with the gather count below)
+        const int64_t nph = h_res[0];
+        if (!windowed) CK(scan_exclusive(seg_len, seg_off, h_res[1], s));
         CK(dalloc_n(&sch->pos_node, N1, s));
         CK(dalloc_n(&sch->pos_flags, N1, s));
         CK(dalloc_n(&sch->pos_dur, N1, s));
@@ -942,7 +962,7 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
         CK(dalloc_n(&sch->node_step, N1, s));
         CK(dalloc_n(&sch->gat_ptr, N1, s));
         if (n > 0) {
-            k_positions<<<gN, kBS, 0, s>>>(n, nseg, seg_off, seg_start, seg_step, g->order, g->dur,
+            k_positions<<<gN, kBS, 0, s>>>(n, result + 1, seg_off, seg_start, seg_step, g->order, g->dur,
                                            g->gap, g->cls, sch->pos_node, sch->pos_flags,
                                            sch->pos_dur, sch->pos_gap, sch->pos_cls,
                                            sch->node_step);
@@ -950,7 +970,6 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
         }
         if (mode == DD_PHASES) {
             sch->n_steps = nph;
-            sch->n_segments = nseg;
             CK(dalloc_n(&sch->step_ptr, (size_t)nph + 1, s));
             k_step_ptr<<<grid_for(nph + 1, kBS), kBS, 0, s>>>(nph, step_seg, seg_off, sch->step_ptr);
             CK(hipGetLastError());
@@ -1004,8 +1023,11 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
         CK(scan_exclusive(gcnt, sch->gat_ptr, n, s));
         int64_t h_G = 0;
         CK(hipMemcpyAsync(&h_G, sch->gat_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+        if (mode == DD_PHASES)
+            CK(hipMemcpyAsync(&h_res[1], result + 1, sizeof(int64_t), hipMemcpyDeviceToHost, s));
         CK(hipStreamSynchronize(s));
         sch->n_gathers = h_G;
+        if (mode == DD_PHASES) sch->n_segments = h_res[1];
         CK(dalloc_n(&sch->gat_src, (size_t)h_G + 1, s));
         CK(dalloc_n(&sch->gat_pos, (size_t)h_G + 1, s));
         CK(dalloc_n(&sch->gat_cls, (size_t)h_G + 1, s));

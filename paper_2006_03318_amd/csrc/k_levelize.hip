@@ -655,11 +655,12 @@ __global__ __launch_bounds__(kBS) void k_inverse(int64_t n, const int32_t *__res
     if (q < n) pos_of[pos_node[q]] = (int32_t)q;
 }
 
-__global__ __launch_bounds__(kBS) void k_gather_spos(int64_t G, const int32_t *__restrict__ gsrc,
+__global__ __launch_bounds__(kBS) void k_gather_spos(const int64_t *__restrict__ pG,
+                                                     const int32_t *__restrict__ gsrc,
                                                      const int32_t *__restrict__ pos_of,
                                                      int32_t *__restrict__ gspos) {
     const int64_t e = (int64_t)blockIdx.x * kBS + threadIdx.x;
-    if (e < G) gspos[e] = pos_of[gsrc[e]];
+    if (e < *pG) gspos[e] = pos_of[gsrc[e]];
 }
 
 // the per-position record the simulation streams through LDS
@@ -1021,17 +1022,14 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
             CK(hipGetLastError());
         }
         CK(scan_exclusive(gcnt, sch->gat_ptr, n, s));
-        int64_t h_G = 0;
-        CK(hipMemcpyAsync(&h_G, sch->gat_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
-        if (mode == DD_PHASES)
-            CK(hipMemcpyAsync(&h_res[1], result + 1, sizeof(int64_t), hipMemcpyDeviceToHost, s));
-        CK(hipStreamSynchronize(s));
-        sch->n_gathers = h_G;
-        if (mode == DD_PHASES) sch->n_segments = h_res[1];
-        CK(dalloc_n(&sch->gat_src, (size_t)h_G + 1, s));
-        CK(dalloc_n(&sch->gat_pos, (size_t)h_G + 1, s));
-        CK(dalloc_n(&sch->gat_cls, (size_t)h_G + 1, s));
-        CK(dalloc_n(&sch->gat_gap, (size_t)h_G + 1, s));
+        // gather lists sized by their bound (cross edges, plus one thread
+        // predecessor per run head without thread carries); the count comes
+        // back with the last read-back
+        const int64_t Gmax = g->n_cross + (sch->thread_carry ? 0 : n);
+        CK(dalloc_n(&sch->gat_src, (size_t)Gmax + 1, s));
+        CK(dalloc_n(&sch->gat_pos, (size_t)Gmax + 1, s));
+        CK(dalloc_n(&sch->gat_cls, (size_t)Gmax + 1, s));
+        CK(dalloc_n(&sch->gat_gap, (size_t)Gmax + 1, s));
         if (n > 0) {
             k_gather_fill<<<gN, kBS, 0, s>>>(n, sch->pos_node, sch->pos_flags, g->thread_prev,
                                              g->xin_ptr, g->xin_src, g->xin_cls, mask,
@@ -1043,13 +1041,13 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
         {
             int32_t *pos_of = nullptr;
             CK(dalloc_n(&pos_of, N1, s));
-            CK(dalloc_n(&sch->gat_spos, (size_t)h_G + 1, s));
+            CK(dalloc_n(&sch->gat_spos, (size_t)Gmax + 1, s));
             CK(dalloc_n(&sch->rec, N1, s));
             if (n > 0) {
                 k_inverse<<<gN, kBS, 0, s>>>(n, sch->pos_node, pos_of);
-                if (h_G > 0)
-                    k_gather_spos<<<grid_for(h_G, kBS), kBS, 0, s>>>(h_G, sch->gat_src, pos_of,
-                                                                    sch->gat_spos);
+                if (Gmax > 0)
+                    k_gather_spos<<<grid_for(Gmax, kBS), kBS, 0, s>>>(sch->gat_ptr + n, sch->gat_src,
+                                                                     pos_of, sch->gat_spos);
                 k_records<<<gN, kBS, 0, s>>>(n, g->thread_id, sch->pos_node, sch->pos_flags, sch->pos_dur,
                                              sch->pos_gap, sch->pos_cls, sch->gat_ptr, sch->gat_src,
                                              sch->gat_spos, sch->gat_cls, sch->gat_gap, sch->rec);
@@ -1059,9 +1057,15 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
         }
         k_step_width<<<grid_for(sch->n_steps, kBS), kBS, 0, s>>>(sch->n_steps, sch->step_ptr, wmax);
         CK(hipGetLastError());
+        int64_t h_G = 0;
         CK(hipMemcpyAsync(&h_w, wmax, sizeof(h_w), hipMemcpyDeviceToHost, s));
+        CK(hipMemcpyAsync(&h_G, sch->gat_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+        if (mode == DD_PHASES)
+            CK(hipMemcpyAsync(&h_res[1], result + 1, sizeof(int64_t), hipMemcpyDeviceToHost, s));
         CK(hipStreamSynchronize(s));
         sch->max_width = (int64_t)h_w;
+        sch->n_gathers = h_G;
+        if (mode == DD_PHASES) sch->n_segments = h_res[1];
     }
 done:
     dfree(cnt, s); dfree(flag, s); dfree(cidx, s); dfree(rptr, s); dfree(err, s);

@@ -87,7 +87,7 @@ hipError_t scan_exclusive(const int64_t *in, int64_t *out, int64_t n, hipStream_
 namespace {
 constexpr int kBS = 256;
 
-constexpr int kValBlocks = 1024;   // grid-stride blocks: one set of atomics per block
+constexpr int kValBlocks = 256;    // grid-stride blocks: one set of atomics per block
 
 __global__ __launch_bounds__(kBS) void k_validate_nodes(
     int32_t n, int32_t T, const int32_t *__restrict__ prev, const int32_t *__restrict__ tid,
@@ -146,14 +146,14 @@ __global__ __launch_bounds__(kBS) void k_validate_nodes(
             e |= (uint32_t)red[6][i];
             gm = red[7][i] > gm ? red[7][i] : gm;
         }
-        atomicAdd(&st->dsum_hi, (unsigned long long)dhi);
-        atomicAdd(&st->dsum_lo, (unsigned long long)dlo);
-        atomicAdd(&st->gsum_hi, (unsigned long long)ghi);
-        atomicAdd(&st->gsum_lo, (unsigned long long)glo);
-        atomicMax(&st->dmax, (unsigned long long)dm);
-        atomicMax(&st->gmax, (unsigned long long)gm);
-        atomicMax(&st->cls_max, (unsigned long long)cm);
-        if (e) atomicOr(err, e);
+        if (dhi) atomicAdd(&st->dsum_hi, (unsigned long long)dhi);
+        if (dlo) atomicAdd(&st->dsum_lo, (unsigned long long)dlo);
+        if (ghi) atomicAdd(&st->gsum_hi, (unsigned long long)ghi);
+        if (glo) atomicAdd(&st->gsum_lo, (unsigned long long)glo);
+        atomic_max_hot(&st->dmax, (unsigned long long)dm);
+        atomic_max_hot(&st->gmax, (unsigned long long)gm);
+        atomic_max_hot(&st->cls_max, (unsigned long long)cm);
+        atomic_or_hot(err, e);
     }
 }
 

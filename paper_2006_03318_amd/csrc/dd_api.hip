@@ -13,6 +13,12 @@
 
 #include "dd_internal.h"
 
+namespace dd {
+// tiled chain ranking (k_graph.hip)
+hipError_t launch_rank_tiles(const dd_graph *g, int32_t *dloc, int32_t *ext, int32_t *xlist,
+                             int64_t *xidx, uint32_t *err, hipStream_t s);
+}  // namespace dd
+
 namespace {
 
 thread_local char g_err[512] = "";
@@ -212,6 +218,7 @@ dd_status dd_graph_load(int32_t n, int32_t n_threads, const int64_t *in_ptr, con
     dd::LoadStats *stats = nullptr;
     int64_t ends[2] = {0, 0};
     uint32_t h_err = 0;
+    uint32_t h_err2[2] = {0u, 0u};     // error bits; too many tile exits for the tiled ranking
     dd::LoadStats hs{};
     const size_t N1 = (size_t)n + 1;
     int64_t E = 0;
@@ -245,16 +252,23 @@ dd_status dd_graph_load(int32_t n, int32_t n_threads, const int64_t *in_ptr, con
     TRY(dd::dalloc_n(&nxt, N1, s), "alloc");
     TRY(dd::dalloc_n(&nxt2, N1, s), "alloc");
     TRY(dd::dalloc_n(&rank2, N1, s), "alloc");
-    if (n > 0) TRY(dd::launch_rank_chains(g, succ, nxt, nxt2, rank2, err, s), "rank chains");
-    TRY(hipMemcpyAsync(&h_err, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "read err");
+    TRY(dd::dalloc_n(&cnt, N1, s), "alloc");
+    if (n > 0) TRY(dd::launch_rank_tiles(g, nxt, nxt2, rank2, cnt, err, s), "rank chains");
+    TRY(hipMemcpyAsync(h_err2, err, sizeof(h_err2), hipMemcpyDeviceToHost, s), "read err");
     TRY(hipStreamSynchronize(s), "sync");
+    if (h_err2[1] && !h_err2[0]) {
+        // more tile exits than one workgroup ranks: plain pointer jumping
+        TRY(dd::launch_rank_chains(g, succ, nxt, nxt2, rank2, err, s), "rank chains");
+        TRY(hipMemcpyAsync(h_err2, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "read err");
+        TRY(hipStreamSynchronize(s), "sync");
+    }
+    h_err = h_err2[0];
     if (h_err) { st = map_err_bits(h_err); goto fail_out; }
     TRY(dd::dalloc_n(&g->thread_base, (size_t)n_threads + 1, s), "alloc");
     TRY(dd::dalloc_n(&len, (size_t)n_threads + 1, s), "alloc");
     TRY(dd::dalloc_n(&g->order, N1, s), "alloc");
     TRY(dd::launch_build_order(g, succ, len, s), "order");
     TRY(dd::dalloc_n(&g->xin_ptr, N1, s), "alloc");
-    TRY(dd::dalloc_n(&cnt, N1, s), "alloc");
     if (n > 0) {
         TRY(dd::launch_cross_edges(g, d_in_ptr, d_in_src, edge_cls ? d_ecls : nullptr, cnt, err, stats, s), "cross edges");
     } else {

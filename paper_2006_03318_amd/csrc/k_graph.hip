@@ -217,6 +217,128 @@ __global__ __launch_bounds__(kBS) void k_rank_check(int32_t n, const int32_t *__
     if (__any(bad) && (threadIdx.x & 63) == 0) atomicOr(err, ERR_CHAIN_CYCLE);
 }
 
+// Chain ranking in two levels.  Tasks of a thread are mostly close in id
+// (traces interleave a few threads), so a tile of kRankTile consecutive ids
+// resolves most of each chain with pointer jumping in LDS: every task gets
+// d (predecessors up to and including the first one outside the tile) and
+// e (that outside task, -1 if the chain starts in the tile), so that
+// rank(u) = d + rank(e).  The outside tasks named as e (the tile exits) are
+// then ranked by one workgroup, again by pointer jumping in LDS, and every
+// task adds its exit's rank.  A thread order that loops inside a tile or
+// across exits is reported like the plain pointer jumping does.
+constexpr int kRankTile = 1024;
+constexpr int kRankXMax = 8192;     // tile exits ranked in LDS at most
+
+__global__ __launch_bounds__(kRankTile) void k_rank_tile(int32_t n, const int32_t *__restrict__ prev,
+                                                         int32_t *__restrict__ dloc,
+                                                         int32_t *__restrict__ ext,
+                                                         int64_t *__restrict__ xflag,
+                                                         uint32_t *__restrict__ err) {
+    __shared__ int32_t sn[2][kRankTile], sd[2][kRankTile], se[2][kRankTile];
+    const int64_t b0 = (int64_t)blockIdx.x * kRankTile;
+    const int i = threadIdx.x;
+    const int64_t u = b0 + i;
+    const bool ok = u < n;
+    const int32_t p = ok ? prev[u] : -1;
+    const bool in = p >= b0 && p < b0 + kRankTile && p < n;
+    int nn = in ? (int)(p - b0) : -1;
+    int d = p >= 0 ? 1 : 0;
+    int e = in ? -1 : p;
+    int buf = 0;
+    sn[0][i] = nn; sd[0][i] = d; se[0][i] = e;
+    __syncthreads();
+    for (int it = 0; it < 11; it++) {        // 2^10 = kRankTile: every in-tile chain ends
+        if (nn >= 0) {
+            const int j = nn;
+            d += sd[buf][j];
+            e = se[buf][j];
+            nn = sn[buf][j];
+        }
+        buf ^= 1;
+        sn[buf][i] = nn; sd[buf][i] = d; se[buf][i] = e;
+        __syncthreads();
+    }
+    if (__any(ok && nn >= 0) && (i & 63) == 0) atomicOr(err, ERR_CHAIN_CYCLE);
+    if (ok) {
+        dloc[u] = d;
+        ext[u] = e;
+        if (e >= 0) xflag[e] = 1;
+    }
+}
+
+__global__ __launch_bounds__(kBS) void k_rank_xlist(int32_t n, const int64_t *__restrict__ xidx,
+                                                    int32_t *__restrict__ xlist) {
+    const int64_t u = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (u < n && xidx[u + 1] != xidx[u]) xlist[xidx[u]] = (int32_t)u;
+}
+
+// ranks of the tile exits (one workgroup); err[1] is set when there are more
+// than kRankXMax of them (the caller then ranks by plain pointer jumping)
+__global__ __launch_bounds__(1024) void k_rank_exits(int32_t n, const int64_t *__restrict__ xidx,
+                                                     const int32_t *__restrict__ xlist,
+                                                     const int32_t *__restrict__ dloc,
+                                                     const int32_t *__restrict__ ext,
+                                                     int32_t *__restrict__ rank,
+                                                     uint32_t *__restrict__ err) {
+    __shared__ int32_t sn[2][kRankXMax], sd[2][kRankXMax];
+    const int64_t nx = xidx[n];
+    if (nx > kRankXMax) {
+        if (threadIdx.x == 0) err[1] = 1u;
+        return;
+    }
+    constexpr int PER = kRankXMax / 1024;
+    int nn[PER], d[PER];
+#pragma unroll
+    for (int k = 0; k < PER; k++) {
+        const int x = threadIdx.x + k * 1024;
+        nn[k] = -1; d[k] = 0;
+        if (x < nx) {
+            const int32_t u = xlist[x];
+            const int32_t e = ext[u];
+            d[k] = dloc[u];
+            nn[k] = e >= 0 ? (int)xidx[e] : -1;
+        }
+        sn[0][x] = nn[k]; sd[0][x] = d[k];
+    }
+    __syncthreads();
+    int buf = 0;
+    for (int it = 0; it < 14; it++) {        // 2^13 = kRankXMax: every exit chain ends
+#pragma unroll
+        for (int k = 0; k < PER; k++) {
+            if (nn[k] >= 0) {
+                const int j = nn[k];
+                d[k] += sd[buf][j];
+                nn[k] = sn[buf][j];
+            }
+        }
+        buf ^= 1;
+#pragma unroll
+        for (int k = 0; k < PER; k++) {
+            const int x = threadIdx.x + k * 1024;
+            sn[buf][x] = nn[k]; sd[buf][x] = d[k];
+        }
+        __syncthreads();
+    }
+    bool bad = false;
+#pragma unroll
+    for (int k = 0; k < PER; k++) {
+        const int x = threadIdx.x + k * 1024;
+        bad |= x < nx && nn[k] >= 0;
+        if (x < nx) rank[xlist[x]] = d[k];
+    }
+    if (__any(bad) && (threadIdx.x & 63) == 0) atomicOr(err, ERR_CHAIN_CYCLE);
+}
+
+__global__ __launch_bounds__(kBS) void k_rank_final(int32_t n, const int32_t *__restrict__ dloc,
+                                                    const int32_t *__restrict__ ext,
+                                                    const int64_t *__restrict__ xidx,
+                                                    int32_t *__restrict__ rank) {
+    const int64_t u = (int64_t)blockIdx.x * kBS + threadIdx.x;
+    if (u >= n || xidx[u + 1] != xidx[u]) return;   // exits hold their rank already
+    const int32_t e = ext[u];
+    rank[u] = dloc[u] + (e >= 0 ? rank[e] : 0);
+}
+
 __global__ __launch_bounds__(kBS) void k_thread_len(int32_t n, const int32_t *__restrict__ succ,
                                                     const int32_t *__restrict__ tid,
                                                     const int32_t *__restrict__ rank,
@@ -300,6 +422,21 @@ hipError_t launch_validate_edges(const dd_graph *g, const int64_t *in_ptr, const
                                  hipStream_t s) {
     k_validate_edges<<<grid_for(g->n, kBS), kBS, 0, s>>>(g->n, in_ptr, in_src, edge_cls,
                                                          g->thread_prev, succ, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_rank_tiles(const dd_graph *g, int32_t *dloc, int32_t *ext, int32_t *xlist,
+                             int64_t *xidx, uint32_t *err, hipStream_t s) {
+    const int32_t n = g->n;
+    hipError_t e = hipMemsetAsync(xidx, 0, sizeof(int64_t) * ((size_t)n + 1), s);
+    if (e != hipSuccess) return e;
+    k_rank_tile<<<(unsigned)((n + kRankTile - 1) / kRankTile), kRankTile, 0, s>>>(n, g->thread_prev,
+                                                                               dloc, ext, xidx, err);
+    e = scan_exclusive(xidx, xidx, n, s);
+    if (e != hipSuccess) return e;
+    k_rank_xlist<<<grid_for(n, kBS), kBS, 0, s>>>(n, xidx, xlist);
+    k_rank_exits<<<1, 1024, 0, s>>>(n, xidx, xlist, dloc, ext, g->rank, err);
+    k_rank_final<<<grid_for(n, kBS), kBS, 0, s>>>(n, dloc, ext, xidx, g->rank);
     return hipGetLastError();
 }
 

@@ -65,6 +65,26 @@ def test_ping_pong_round_counts(n):
     assert np.array_equal(gp, ph)
 
 
+@pytest.mark.parametrize("seed", [0, 1])
+def test_many_threads_chain_ranks(seed):
+    """Thousands of threads spread over the task ids: more tile exits than
+    one workgroup ranks, so graph load falls back to plain pointer jumping;
+    the schedule still matches the oracle's."""
+    require_gpu()
+    rng = np.random.default_rng(50_000 + seed)
+    n, T = 30000, 3000
+    thread = rng.integers(0, T, n)
+    thread[:T] = np.arange(T)                       # every thread has a task
+    a = rng.integers(0, n - 1, 3000)
+    b = np.minimum(a + rng.integers(1, 500, 3000), n - 1)
+    edges = [(int(x), int(y)) for x, y in zip(a, b) if x < y]
+    g = H.graph(T, thread, edges, rng.integers(0, 100, n), rng.integers(0, 10, n))
+    lv, ph = O.steps(g, 1)
+    gp, nph, _ = _steps_gpu(g, 1, B.DD_PHASES)
+    say("many threads", seed, "phases", nph)
+    assert np.array_equal(gp, ph)
+
+
 @pytest.mark.parametrize("k", [1, 2, 3, 4])
 def test_config_steps(k):
     require_gpu()
@@ -123,6 +143,12 @@ def test_load_errors():
     # the same fork deep inside a long thread
     g = H.graph(1, [0] * 3000, [], [1] * 3000, [0] * 3000)
     g.thread_prev[2500] = 1700
+    _expect(B.DD_ECHAIN, lambda: _load(g))
+    # thread order loops across tiles of consecutive tasks, away from the
+    # thread's head (the loop is found among the tile exits)
+    n = 3000
+    g = H.graph(1, [0] * n, [], [1] * n, [0] * n)
+    g.thread_prev[2000] = n - 1
     _expect(B.DD_ECHAIN, lambda: _load(g))
     # thread order loops (plus a proper head elsewhere)
     g = H.graph(1, [0, 0, 0], [], [1, 2, 3], [0, 0, 0], thread_order=[[0]])

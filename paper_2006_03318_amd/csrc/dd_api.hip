@@ -243,10 +243,10 @@ dd_status dd_graph_load(int32_t n, int32_t n_threads, const int64_t *in_ptr, con
     TRY(copy_in(&heads, (const int32_t *)nullptr, (size_t)n_threads, s), "alloc");
     TRY(copy_in(&err, (const uint32_t *)nullptr, 2, s), "alloc");
     TRY(copy_in(&stats, (const dd::LoadStats *)nullptr, 1, s), "alloc");
+    // the edge pass and the chain ranking clamp every index they follow, so
+    // the per-task errors are read together with theirs (invalid-input bits
+    // take precedence in map_err_bits)
     if (n > 0) TRY(dd::launch_validate_nodes(g, d_in_ptr, succ, heads, err, stats, s), "validate");
-    TRY(hipMemcpyAsync(&h_err, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "read err");
-    TRY(hipStreamSynchronize(s), "sync");
-    if (h_err) { st = map_err_bits(h_err); goto fail_out; }
     if (n > 0) TRY(dd::launch_validate_edges(g, d_in_ptr, d_in_src, edge_cls ? d_ecls : nullptr, succ, err, s), "validate edges");
     TRY(dd::dalloc_n(&g->rank, N1, s), "alloc rank");
     TRY(dd::dalloc_n(&nxt, N1, s), "alloc");

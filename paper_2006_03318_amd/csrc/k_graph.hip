@@ -157,9 +157,11 @@ __global__ __launch_bounds__(kBS) void k_validate_nodes(
     }
 }
 
-// (runs once the per-task fields are valid: also reports a task named as
-// previous task by two tasks, which left only one of them in succ)
-__global__ __launch_bounds__(kBS) void k_validate_edges(int32_t n, const int64_t *__restrict__ in_ptr,
+// (runs right after the per-task pass, before its errors are read, so every
+// index is clamped to its array; also reports a task named as previous task
+// by two tasks, which left only one of them in succ)
+__global__ __launch_bounds__(kBS) void k_validate_edges(int32_t n, int64_t E,
+                                                        const int64_t *__restrict__ in_ptr,
                                                         const int32_t *__restrict__ in_src,
                                                         const uint8_t *__restrict__ ecls,
                                                         const int32_t *__restrict__ prev,
@@ -169,8 +171,10 @@ __global__ __launch_bounds__(kBS) void k_validate_edges(int32_t n, const int64_t
     uint32_t e = 0;
     if (u < n) {
         const int32_t p = prev[u];
-        if (p >= 0 && succ[p] != (int32_t)u + 1) e |= ERR_SUCC;
-        for (int64_t k = in_ptr[u]; k < in_ptr[u + 1]; k++) {
+        if (p >= 0 && p < n && succ[p] != (int32_t)u + 1) e |= ERR_SUCC;
+        const int64_t k0 = in_ptr[u] > 0 ? in_ptr[u] : 0;
+        const int64_t k1 = in_ptr[u + 1] < E ? in_ptr[u + 1] : E;
+        for (int64_t k = k0; k < k1; k++) {
             const int32_t s = in_src[k];
             if (s < 0 || s >= n) e |= ERR_SRC_RANGE;
             else if (s == u) e |= ERR_SELF_LOOP;
@@ -239,7 +243,8 @@ __global__ __launch_bounds__(kRankTile) void k_rank_tile(int32_t n, const int32_
     const int i = threadIdx.x;
     const int64_t u = b0 + i;
     const bool ok = u < n;
-    const int32_t p = ok ? prev[u] : -1;
+    int32_t p = ok ? prev[u] : -1;
+    if (p < -1 || p >= n || p == u) p = -1;   // reported by the per-task pass
     const bool in = p >= b0 && p < b0 + kRankTile && p < n;
     int nn = in ? (int)(p - b0) : -1;
     int d = p >= 0 ? 1 : 0;
@@ -420,7 +425,7 @@ hipError_t launch_validate_nodes(const dd_graph *g, const int64_t *in_ptr, int32
 hipError_t launch_validate_edges(const dd_graph *g, const int64_t *in_ptr, const int32_t *in_src,
                                  const uint8_t *edge_cls, const int32_t *succ, uint32_t *err,
                                  hipStream_t s) {
-    k_validate_edges<<<grid_for(g->n, kBS), kBS, 0, s>>>(g->n, in_ptr, in_src, edge_cls,
+    k_validate_edges<<<grid_for(g->n, kBS), kBS, 0, s>>>(g->n, g->n_edges, in_ptr, in_src, edge_cls,
                                                          g->thread_prev, succ, err);
     return hipGetLastError();
 }

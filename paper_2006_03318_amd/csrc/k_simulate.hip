@@ -416,9 +416,10 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
 #pragma unroll
         for (int j = 0; j < VPL; j++) eon[j] = sEon[o0 + j];
         // next round's loads (records of k+1 are in LDS since round k-1): a
-        // small round issues them first; a big round after its walk, so the
-        // walk does not queue behind them and the two register sets are
-        // never live together
+        // small round issues them first; a big round right after its walk,
+        // so the walk does not queue behind them, the two register sets are
+        // never live together, and the address work fills the wait at the
+        // round's first barrier
         Dyn<K, VPL> DN;
         const int rn1 = m1rn;                     // round k+1 (this round if last)
         const int bN = k + 1 < nr ? b1 : b0;
@@ -757,6 +758,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 }
             }
         }
+        Dyn<K, VPL> DNb;
+        issue(next_small_tag, rn1, bN, r0, DNb);
         put_next();
         // slot summaries (variant-major); slot 0 absorbs the carry and
         // starts its variant (kHead); slots of idle waves are the identity
@@ -767,8 +770,6 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             sB[e] = slot == 0 ? max64(carry[j] + A[j], B[j]) : B[j];
         }
         __syncthreads();                                     // B1
-        Dyn<K, VPL> DNb;
-        issue(next_small_tag, rn1, bN, r0, DNb);
         // inclusive scan of slot summaries per variant: DPP within the wave,
         // then earlier 64-slot chunks of the same variant; chunks whose
         // slots all lie past the round's end are skipped

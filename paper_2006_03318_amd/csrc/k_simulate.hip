@@ -366,6 +366,22 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             }
         }
     };
+    // one position of the big layout (issue() does all K of them)
+    auto issue_big_at = [&](int rn, int b, int prev_r0, Dyn<K, VPL> &d, int i) {
+        const Rec *R = reinterpret_cast<const Rec *>(sRec[b]);
+        const int ke = per_slot(rn);
+        const int q = slot * ke + i;
+        const bool ok = i < ke && q < rn;
+        const int4 w1 = reinterpret_cast<const int4 *>(&R[q])[1];
+        const bool n0 = ok && w1.y >= 0 && w1.w < prev_r0;
+        const int64_t a0 = n0 ? w1.y : 0;
+        const Vals<VPL> f = *reinterpret_cast<const Vals<VPL> *>(a.finish + a0 * V + vvf);
+        const uint32_t r0 = a.rm[a0 * W + vw];
+        const int64_t gg = UNI ? 0 : a.gap[a0];
+        d.f0[i] = f;
+        d.r0w[i] = r0;
+        d.g0gap[i] = gg;
+    };
     // (start, size) of rounds k .. k+3, the last clamped to the final round:
     // each round loads the entry three rounds ahead, so no round waits for
     // a scalar load of its own bounds
@@ -416,10 +432,11 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
 #pragma unroll
         for (int j = 0; j < VPL; j++) eon[j] = sEon[o0 + j];
         // next round's loads (records of k+1 are in LDS since round k-1): a
-        // small round issues them first; a big round right after its walk,
-        // so the walk does not queue behind them, the two register sets are
-        // never live together, and the address work fills the wait at the
-        // round's first barrier
+        // small round issues them first; a big round during or right after
+        // its walk (a big next round's loads for position i go out after the
+        // walk's position i, whose prefetched registers they then reuse), so
+        // their record reads and address work fill the walk's stalls and the
+        // wait at the round's first barrier
         Dyn<K, VPL> DN;
         const int rn1 = m1rn;                     // round k+1 (this round if last)
         const int bN = k + 1 < nr ? b1 : b0;
@@ -619,10 +636,15 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         for (int i = 0; i < K; i++)
 #pragma unroll
             for (int j = 0; j < VPL; j++) nkh[i][j] = (uint32_t)((uint64_t)kHead >> 32);
-        if (wact) {
+        Dyn<K, VPL> DNb;
+        constexpr bool NEXT_BIG = !decltype(next_small_tag)::value;
+        {
 #pragma unroll
             for (int i = 0; i < K; i++) {
-                if (i >= ke) break;
+                // a big next round's loads go out position by position, between
+                // this round's positions
+                if (NEXT_BIG && i > 0) issue_big_at(rn1, bN, r0, DNb, i - 1);
+                if (!wact || i >= ke) continue;
                 const int q = slot * ke + i;
                 const bool ok = q < rn;
                 const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
@@ -758,8 +780,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 }
             }
         }
-        Dyn<K, VPL> DNb;
-        issue(next_small_tag, rn1, bN, r0, DNb);
+        if constexpr (NEXT_BIG) issue_big_at(rn1, bN, r0, DNb, K - 1);
+        else issue(next_small_tag, rn1, bN, r0, DNb);
         put_next();
         // slot summaries (variant-major); slot 0 absorbs the carry and
         // starts its variant (kHead); slots of idle waves are the identity

@@ -45,7 +45,7 @@ def kernel_source_digest():
     """sha256 over the sources the simulation kernel is compiled from."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("k_simulate.hip", "dd_internal.h", "dd_common.cuh"):
+    for f in ("k_simulate.hip", "dd_internal.h", "dd_common.h"):
         with open(os.path.join(ROOT, "paper_2006_03318_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
@@ -79,8 +79,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=5)
     ap.add_argument("--variants", type=int, default=None)
-    ap.add_argument("--cpu-sample", type=int, default=1024,
-                    help="variants the oracle runs for the CPU baseline (0 = skip)")
+    ap.add_argument("--cpu-sample", type=int, default=-1,
+                    help="variants the oracle runs for the CPU baseline (-1 = all, 0 = skip)")
+    ap.add_argument("--cpu-workers", type=int, default=16,
+                    help="oracle worker threads at most (the host share of one GPU is 16 "
+                         "cores)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device to device three times: the plain copy "
                          "whose byte counters scale the simulation kernel's")
@@ -126,6 +129,7 @@ def main():
     E = lambda: torch.cuda.Event(enable_timing=True)   # noqa: E731
     rows = {"load": [], "levelize": [], "transforms": [], "simulate": []}
     info = {}
+    binfo = [None] * len(di.batches)      # schedule shape of each batch
 
     def step(record):
         ev = [E() for _ in range(2 + 3 * len(di.batches))]
@@ -142,8 +146,10 @@ def main():
             fin, st, ms = outs[bi]
             B.dd_simulate_batch(gh, sch, var, fin, st, ms, stream)
             ev[k + 2].record(stream)
+            if binfo[bi] is None:
+                binfo[bi] = B.dd_sched_info(sch)
             if not info:
-                info.update(B.dd_sched_info(sch))
+                info.update(binfo[bi])
             hs.append((sch, var))
             k += 3
         for sch, var in hs:
@@ -179,31 +185,48 @@ def main():
     NV = g.n * vs.n_variants
     value = NV / (ms_per_step / 1e3)
 
+    # simulate time per step = sum over the batches' launches; bytes likewise
     sim_ms = float(np.mean(rows["simulate"]))
-    nbytes = algorithmic_bytes(g.n, vs.n_variants, info.get("n_gathers", 0), di.n_cls)
+    nbytes = sum(algorithmic_bytes(g.n, v1 - v0, bi_["n_gathers"], di.n_cls)
+                 for (v0, v1, *_r), bi_ in zip(di.batches, binfo))
     achieved = nbytes / (sim_ms / 1e3) / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": measured_traffic(args.config, g.n, vs.n_variants),
                 "kernel": "k_sim_pipe", "algorithmic_bytes_per_launch": int(nbytes),
-                "avg_launch_ms": round(sim_ms, 4)}
+                "avg_launch_ms": round(sim_ms / len(di.batches), 4),
+                "launches_per_step": len(di.batches)}
 
     # parity sample + CPU baseline: the oracle on the first variants
     cpu = None
     parity = None
-    if args.cpu_sample > 0:
+    if args.cpu_sample != 0:
         from oracle import oracle as O
         O.build(force=False)
-        ns = min(args.cpu_sample, vs.n_variants)
-        cores = max(1, min(len(os.sched_getaffinity(0)), 16))
+        ns = vs.n_variants if args.cpu_sample < 0 else min(args.cpu_sample, vs.n_variants)
+        avail = len(os.sched_getaffinity(0))
+        cores = max(1, min(avail, args.cpu_workers))
         t0 = time.perf_counter()
         _, _, oms, _ = O.run(g, vs, variants=range(ns), want_start=False, want_finish=False,
                              workers=cores)
         cpu_s = time.perf_counter() - t0
+        # one core: a bounded sample of about two seconds of oracle work
+        per_core = g.n * ns / cpu_s / cores          # rate estimate per worker
+        n1 = max(1, min(ns, int(2.0 * per_core / max(1, g.n))))
+        t1 = time.perf_counter()
+        O.run(g, vs, variants=range(n1), want_start=False, want_finish=False, workers=1)
+        one_s = time.perf_counter() - t1
         cpu = {"value": round(g.n * ns / cpu_s, 1), "unit": "node-variant updates/s",
                "cores": cores, "kind": "oracle",
-               "sample": "first %d of %d variants, all %d tasks (%.1f s wall)"
-                         % (ns, vs.n_variants, g.n, cpu_s)}
+               "sample": "%s%d of %d variants, all %d tasks (%.1f s wall on %d worker threads)"
+                         % ("" if ns == vs.n_variants else "first ", ns, vs.n_variants, g.n,
+                            cpu_s, cores),
+               "nproc": os.cpu_count(), "affinity_cpus": avail,
+               "worker_cap": "at most %d worker threads: the host share of one GPU"
+                             % args.cpu_workers,
+               "single_core_value": round(g.n * n1 / one_s, 1),
+               "single_core_sample": "first %d variants on 1 worker thread (%.2f s)"
+                                     % (n1, one_s)}
         gms = np.concatenate([m.cpu().numpy() for (_, _, m) in outs])[:ns]
         parity = bool(np.array_equal(gms, oms))
 

@@ -47,11 +47,15 @@
  *     caller; the library never frees them.
  *   - Handles are owned by the library until the matching *_free.  A handle
  *     keeps device memory, released on the stream it was created on, which
- *     must stay valid until the handle is freed.  Released device memory
- *     stays in a cache of the library, kept per device and stream, and is
- *     handed out again to later calls on that same stream (stream order
- *     makes the reuse safe); it returns to the device when an allocation
- *     would otherwise fail, or at process exit.
+ *     must stay valid until the handle is freed.  A handle may be used on
+ *     any stream: the library records an event after each use on a stream
+ *     other than the handle's own, and *_free makes the handle's stream wait
+ *     for those events before its memory can be handed out again.  Released
+ *     device memory stays in a cache of the library, kept per device and
+ *     stream, and is handed out again to later calls on that same stream
+ *     (stream order makes the reuse safe); it returns to the device when an
+ *     allocation would otherwise fail, on dd_release_cache(), or at process
+ *     exit.
  *   - `stream` is a hipStream_t (NULL = default stream).  Work is
  *     stream-ordered.  Input validation is synchronous: load, levelize and
  *     apply_transforms wait for their own device checks before returning.
@@ -161,6 +165,28 @@ dd_status dd_apply_transforms(const dd_graph *g, int32_t n_variants, int32_t n_c
 dd_status dd_simulate_batch(const dd_graph *g, const dd_sched *sched, const dd_variants *var,
                             int64_t *d_finish, int64_t *d_start, int64_t *d_makespan,
                             void *stream);
+
+/*
+ * dd_simulate_batch_vs -- dd_simulate_batch with an explicit launch shape.
+ *   variants_per_wg  variants that each workgroup owns for the whole
+ *                    schedule: 0 = chosen by the library (as
+ *                    dd_simulate_batch), or 1, 2, 4, 8, 16; any other value
+ *                    returns DD_EINVAL.
+ * The results do not depend on the shape (Algorithm 1 per variant, Sec. 4.1);
+ * only the number of workgroups and the kernel instance do.  For tuning, and
+ * for checking every compiled instance.
+ */
+dd_status dd_simulate_batch_vs(const dd_graph *g, const dd_sched *sched, const dd_variants *var,
+                               int64_t *d_finish, int64_t *d_start, int64_t *d_makespan,
+                               int32_t variants_per_wg, void *stream);
+
+/*
+ * dd_release_cache -- wait for all work on the current device, then return
+ * every block of the library's device-memory cache for that device to the
+ * device (hipFree).  Memory held by live handles is not touched.  For callers
+ * that share the GPU with another allocator (e.g. torch) and need the space.
+ */
+dd_status dd_release_cache(void);
 
 /* Step (level or phase) of every task: int32 [n], host or device pointer. */
 dd_status dd_sched_task_steps(const dd_sched *sched, int32_t *steps_out, void *stream);

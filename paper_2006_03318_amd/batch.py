@@ -50,8 +50,9 @@ def load_graph(di: DeviceInputs, stream=None):
 
 
 def simulate(di: DeviceInputs, mode=B.DD_PHASES, want_start=False, stream=None,
-             outputs: Optional[list] = None, keep_handles=False):
-    """Run every batch; returns a list of (v0, v1, finish[N][Vb], start, makespan[Vb])."""
+             outputs: Optional[list] = None, keep_handles=False, variants_per_wg: int = 0):
+    """Run every batch; returns a list of (v0, v1, finish[N][Vb], start, makespan[Vb]).
+    variants_per_wg: 0 = the library's launch shape, else 1/2/4/8/16."""
     import torch
     dev = di.tensors["dur"].device
     g = load_graph(di, stream)
@@ -68,7 +69,10 @@ def simulate(di: DeviceInputs, mode=B.DD_PHASES, want_start=False, stream=None,
                 fin = torch.empty((di.n, Vb), dtype=torch.int64, device=dev)
                 st = torch.empty((di.n, Vb), dtype=torch.int64, device=dev) if want_start else None
                 ms = torch.empty((Vb,), dtype=torch.int64, device=dev)
-            B.dd_simulate_batch(g, sch, var, fin, st, ms, stream)
+            if variants_per_wg:
+                B.dd_simulate_batch_vs(g, sch, var, fin, st, ms, variants_per_wg, stream)
+            else:
+                B.dd_simulate_batch(g, sch, var, fin, st, ms, stream)
             res.append((v0, v1, fin, st, ms))
             handles.append((sch, var))
     finally:

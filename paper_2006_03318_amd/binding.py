@@ -59,6 +59,8 @@ def lib():
         "dd_levelize": (_i32, [_vp, _u64, _i32, _vp, ctypes.POINTER(_vp), ctypes.POINTER(_i64)]),
         "dd_apply_transforms": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, ctypes.POINTER(_vp)]),
         "dd_simulate_batch": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _vp]),
+        "dd_simulate_batch_vs": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp]),
+        "dd_release_cache": (_i32, []),
         "dd_sched_task_steps": (_i32, [_vp, _vp, _vp]),
         "dd_sched_info": (_i32, [_vp, ctypes.POINTER(_i64), ctypes.POINTER(_i64),
                                  ctypes.POINTER(_i64), ctypes.POINTER(_i64)]),
@@ -156,6 +158,18 @@ def dd_simulate_batch(g, sched, var, d_finish, d_start, d_makespan, stream=None)
     rc = lib().dd_simulate_batch(g, sched, var, _ptr(d_finish, "int64"), _ptr(d_start, "int64"),
                                  _ptr(d_makespan, "int64"), _stream(stream))
     _check(rc)
+
+
+def dd_simulate_batch_vs(g, sched, var, d_finish, d_start, d_makespan, variants_per_wg,
+                         stream=None):
+    rc = lib().dd_simulate_batch_vs(g, sched, var, _ptr(d_finish, "int64"),
+                                    _ptr(d_start, "int64"), _ptr(d_makespan, "int64"),
+                                    int(variants_per_wg), _stream(stream))
+    _check(rc)
+
+
+def dd_release_cache():
+    _check(lib().dd_release_cache())
 
 
 def dd_sched_task_steps(sched, out, stream=None):

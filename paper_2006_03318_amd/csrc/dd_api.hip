@@ -68,6 +68,7 @@ hipError_t copy_in(T **dst, const T *src, size_t count, hipStream_t s) {
 
 void free_graph_arrays(dd_graph *g) {
     hipStream_t s = g->stream;
+    dd::join_uses(g->uses, s);
     dd::dfree(g->thread_prev, s); dd::dfree(g->thread_id, s); dd::dfree(g->dur, s);
     dd::dfree(g->gap, s); dd::dfree(g->cls, s); dd::dfree(g->rank, s);
     dd::dfree(g->thread_base, s); dd::dfree(g->order, s); dd::dfree(g->xin_ptr, s);
@@ -76,6 +77,7 @@ void free_graph_arrays(dd_graph *g) {
 
 void free_sched_arrays(dd_sched *x) {
     hipStream_t s = x->stream;
+    dd::join_uses(x->uses, s);
     dd::dfree(x->step_ptr, s); dd::dfree(x->pos_node, s); dd::dfree(x->pos_flags, s);
     dd::dfree(x->pos_dur, s); dd::dfree(x->pos_gap, s); dd::dfree(x->pos_cls, s);
     dd::dfree(x->gat_ptr, s); dd::dfree(x->gat_src, s); dd::dfree(x->gat_pos, s);
@@ -164,6 +166,39 @@ void dfree(void *p, hipStream_t s) {
     g_live.erase(it);
 }
 
+hipError_t release_cache() {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> lk(g_mu);
+    release_cached(dev);
+    return hipGetLastError();
+}
+
+hipError_t note_use(ForeignUses &u, hipStream_t own, hipStream_t s) {
+    if (s == own) return hipSuccess;
+    std::lock_guard<std::mutex> lk(u.mu);
+    hipEvent_t ev = nullptr;
+    for (auto &x : u.ev)
+        if (x.first == s) ev = x.second;
+    if (!ev) {
+        hipError_t e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+        if (e != hipSuccess) return e;
+        u.ev.emplace_back(s, ev);
+    }
+    // re-recording keeps the latest use: earlier work on s precedes it
+    return hipEventRecord(ev, s);
+}
+
+void join_uses(ForeignUses &u, hipStream_t own) {
+    std::lock_guard<std::mutex> lk(u.mu);
+    for (auto &x : u.ev) {
+        (void)hipStreamWaitEvent(own, x.second, 0);
+        (void)hipEventDestroy(x.second);
+    }
+    u.ev.clear();
+}
+
 }  // namespace dd
 
 #define TRY(x, what)                                           \
@@ -175,7 +210,10 @@ void dfree(void *p, hipStream_t s) {
 extern "C" {
 
 const char *dd_status_str(dd_status s) {
-    switch (s) {
+    // callers may pass any integer: read it as one, not as the enum
+    int code;
+    memcpy(&code, &s, sizeof(code));
+    switch (code) {
         case DD_OK: return "DD_OK";
         case DD_EINVAL: return "DD_EINVAL";
         case DD_ECYCLE: return "DD_ECYCLE";
@@ -333,6 +371,12 @@ dd_status dd_levelize(const dd_graph *g, uint64_t active_edge_classes, int32_t m
         delete x;
         return st;
     }
+    if (hipError_t e = dd::note_use(g->uses, g->stream, s)) {
+        st = hip_fail(e, "record stream use");
+        free_sched_arrays(x);
+        delete x;
+        return st;
+    }
     if (n_steps_out) *n_steps_out = x->n_steps;
     *out = x;
     return DD_OK;
@@ -407,6 +451,7 @@ dd_status dd_apply_transforms(const dd_graph *g, int32_t n_variants, int32_t n_c
         }
     }
     TRY(hipStreamSynchronize(s), "sync");
+    TRY(dd::note_use(g->uses, g->stream, s), "record stream use");
     free(h_on);
     dd::dfree(d_scale, s);
     dd::dfree(err, s);
@@ -422,9 +467,13 @@ fail_out:
     return st;
 }
 
-dd_status dd_simulate_batch(const dd_graph *g, const dd_sched *sched, const dd_variants *var,
-                            int64_t *d_finish, int64_t *d_start, int64_t *d_makespan, void *stream) {
-    g_err[0] = 0;
+}  // extern "C"
+
+namespace {
+
+dd_status simulate_impl(const dd_graph *g, const dd_sched *sched, const dd_variants *var,
+                        int64_t *d_finish, int64_t *d_start, int64_t *d_makespan, int vs,
+                        void *stream) {
     if (!g || !sched || !var) return fail(DD_EINVAL, "NULL handle");
     if (!d_makespan || (!d_finish && g->n > 0))
         return fail(DD_EINVAL, "d_finish and d_makespan are required");
@@ -434,11 +483,41 @@ dd_status dd_simulate_batch(const dd_graph *g, const dd_sched *sched, const dd_v
     if (missing)
         return fail(DD_EMISMATCH, "variants switch on edge classes 0x%llx that the schedule was not built for",
                     (unsigned long long)missing);
-    int vs = 0;
-    if (const char *e = getenv("DD_VS")) vs = atoi(e);
-    hipError_t e = dd::launch_simulate(g, sched, var, d_finish, d_start, d_makespan, vs,
-                                       (hipStream_t)stream);
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = dd::launch_simulate(g, sched, var, d_finish, d_start, d_makespan, vs, s);
     if (e != hipSuccess) return hip_fail(e, "simulate launch");
+    e = dd::note_use(g->uses, g->stream, s);
+    if (e == hipSuccess) e = dd::note_use(sched->uses, sched->stream, s);
+    if (e == hipSuccess) e = dd::note_use(var->uses, var->stream, s);
+    if (e != hipSuccess) return hip_fail(e, "record stream use");
+    return DD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+dd_status dd_simulate_batch(const dd_graph *g, const dd_sched *sched, const dd_variants *var,
+                            int64_t *d_finish, int64_t *d_start, int64_t *d_makespan, void *stream) {
+    g_err[0] = 0;
+    return simulate_impl(g, sched, var, d_finish, d_start, d_makespan, 0, stream);
+}
+
+dd_status dd_simulate_batch_vs(const dd_graph *g, const dd_sched *sched, const dd_variants *var,
+                               int64_t *d_finish, int64_t *d_start, int64_t *d_makespan,
+                               int32_t variants_per_wg, void *stream) {
+    g_err[0] = 0;
+    if (variants_per_wg != 0 && variants_per_wg != 1 && variants_per_wg != 2 &&
+        variants_per_wg != 4 && variants_per_wg != 8 && variants_per_wg != 16)
+        return fail(DD_EINVAL, "variants_per_wg must be 0, 1, 2, 4, 8 or 16 (got %d)",
+                    (int)variants_per_wg);
+    return simulate_impl(g, sched, var, d_finish, d_start, d_makespan, variants_per_wg, stream);
+}
+
+dd_status dd_release_cache(void) {
+    g_err[0] = 0;
+    hipError_t e = dd::release_cache();
+    if (e != hipSuccess) return hip_fail(e, "release cache");
     return DD_OK;
 }
 
@@ -480,6 +559,7 @@ void dd_sched_free(dd_sched *x) {
 void dd_variants_free(dd_variants *x) {
     if (!x) return;
     hipStream_t s = x->stream;
+    dd::join_uses(x->uses, s);
     dd::dfree(x->table, s);
     dd::dfree(x->rm_bits, s);
     dd::dfree(x->edge_on, s);

@@ -4,6 +4,10 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+#include <utility>
+#include <vector>
+
 #include "dd.h"
 
 namespace dd {
@@ -60,6 +64,19 @@ static_assert(sizeof(Rec) == 48, "record size");
 // LDS during the simulation instead of gathering the previous task of a run.
 constexpr int kMaxCarryThreads = 64;
 
+// Streams other than its own on which a handle's device memory was used.
+// A handle's blocks go back to the cache of the stream it was created on;
+// before that, its own stream waits for the last use on each other stream,
+// so a later allocation there cannot overwrite memory a kernel still reads.
+struct ForeignUses {
+    std::mutex mu;
+    std::vector<std::pair<hipStream_t, hipEvent_t>> ev;
+};
+// record the point after the work just queued on s (no-op when s == own)
+hipError_t note_use(ForeignUses &u, hipStream_t own, hipStream_t s);
+// make `own` wait for every recorded use; the events are released
+void join_uses(ForeignUses &u, hipStream_t own);
+
 // Statistics reduced on the device while loading (hi/lo split sums cannot
 // overflow for n < 2^31 values below 2^62).
 struct LoadStats {
@@ -90,6 +107,7 @@ struct dd_graph {
     int64_t *xin_ptr = nullptr;   // [n+1] cross-thread in-edges
     int32_t *xin_src = nullptr;
     uint8_t *xin_cls = nullptr;
+    mutable dd::ForeignUses uses;
 };
 
 struct dd_sched {
@@ -112,6 +130,7 @@ struct dd_sched {
     int32_t *node_step = nullptr; // [n]
     dd::Rec *rec = nullptr;       // [n] per position
     bool thread_carry = false;    // thread predecessors come from per-thread carries
+    mutable dd::ForeignUses uses;
 };
 
 struct dd_variants {
@@ -124,13 +143,16 @@ struct dd_variants {
     dd::ScaleEntry *table = nullptr;  // [n_cls][V]
     uint32_t *rm_bits = nullptr;      // [n][W]
     uint64_t *edge_on = nullptr;      // [V]
+    mutable dd::ForeignUses uses;
 };
 
 namespace dd {
 
-// device memory (stream-ordered pool)
+// device memory (cache of blocks kept per device and stream)
 hipError_t dalloc(void **p, size_t bytes, hipStream_t s);
 void dfree(void *p, hipStream_t s);
+// return every cached block of the current device (waits for the device)
+hipError_t release_cache();
 template <class T>
 hipError_t dalloc_n(T **p, size_t count, hipStream_t s) {
     return dalloc(reinterpret_cast<void **>(p), count * sizeof(T) + 16, s);

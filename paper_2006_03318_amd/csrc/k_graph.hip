@@ -10,7 +10,7 @@
 // times never decrease along a thread) and is dropped after checking that
 // it points forward.
 
-#include "dd_common.cuh"
+#include "dd_common.h"
 #include "dd_internal.h"
 
 namespace dd {

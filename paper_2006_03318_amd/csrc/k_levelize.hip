@@ -23,7 +23,7 @@
 // order.  Each position carries its "gathers": the cross-thread parents,
 // plus the previous task on the thread for the first task of a run.
 
-#include "dd_common.cuh"
+#include "dd_common.h"
 #include "dd_internal.h"
 
 #include <stdio.h>

@@ -32,7 +32,7 @@
 // release of each thread's latest task sits in LDS, so a run's first task
 // reads its thread predecessor there instead of gathering it.
 
-#include "dd_common.cuh"
+#include "dd_common.h"
 #include "dd_internal.h"
 
 #include <stdlib.h>

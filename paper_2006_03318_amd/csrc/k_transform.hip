@@ -9,7 +9,7 @@
 // using multiplication", PLDI 1994, Thm. 4.2 with N = 62); the load-time
 // range check guarantees d * p < 2^62.
 
-#include "dd_common.cuh"
+#include "dd_common.h"
 #include "dd_internal.h"
 
 namespace dd {

@@ -628,6 +628,42 @@ def random_graph(rng, n: int, n_threads: int, p_edge: float = 0.3, max_dur: int 
                      kind, np.full(n, -1, np.int32), np.full(n, -1, np.int64), "random")
 
 
+def random_graph_sparse(rng, n: int, n_threads: int, mean_in: float = 0.3,
+                        window: int = 64, n_edge_cls: int = 1, max_dur: int = 10**5,
+                        n_node_cls: int = 3, run_len: int = 1) -> TaskGraph:
+    """A larger random DAG built without a quadratic loop: task j gets
+    Poisson(mean_in) dependency edges from tasks drawn uniformly in
+    [j - window, j); tasks come in runs of `run_len` consecutive ids on one
+    random thread.  Ids are topological; thread order is id order."""
+    runs = (n + run_len - 1) // run_len
+    thread = np.repeat(rng.integers(0, n_threads, size=runs), run_len)[:n].astype(np.int32)
+    prev = np.full(n, -1, np.int32)
+    last = np.full(n_threads, -1, np.int64)
+    for i in range(n):           # O(n): previous task on the same thread
+        t = thread[i]
+        prev[i] = last[t]
+        last[t] = i
+    k = rng.poisson(mean_in, size=n).astype(np.int64)
+    k[0] = 0
+    dst = np.repeat(np.arange(n, dtype=np.int64), k)
+    lo = np.maximum(dst - window, 0)
+    src = lo + (rng.random(dst.shape[0]) * (dst - lo)).astype(np.int64)
+    ok = src < dst
+    src, dst = src[ok], dst[ok]
+    in_ptr = np.zeros(n + 1, np.int64)
+    np.add.at(in_ptr, dst + 1, 1)
+    in_ptr = np.cumsum(in_ptr)
+    dur = rng.integers(0, max_dur + 1, size=n).astype(np.int64)
+    dur[rng.random(n) < 0.1] = 0
+    gap = rng.integers(0, max_dur // 4 + 1, size=n).astype(np.int64)
+    gap[rng.random(n) < 0.5] = 0
+    cls = rng.integers(0, n_edge_cls, size=src.shape[0]).astype(np.uint8)
+    return TaskGraph(n, n_threads, in_ptr, src.astype(np.int32), cls, prev, thread, dur, gap,
+                     rng.integers(0, n_node_cls, size=n).astype(np.uint16), n_node_cls,
+                     n_edge_cls, np.zeros(n, np.uint8), np.full(n, -1, np.int32),
+                     np.full(n, -1, np.int64), "random-sparse")
+
+
 def random_variants(rng, g: TaskGraph, V: int, p_remove: float = 0.2,
                     qs=(1, 2, 3, 4, 5, 7, 8, 10)) -> VariantSet:
     C = g.n_node_cls

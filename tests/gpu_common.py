@@ -22,12 +22,12 @@ def say(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def gpu_run(g, vs, mode=B.DD_PHASES, want_start=True):
+def gpu_run(g, vs, mode=B.DD_PHASES, want_start=True, variants_per_wg=0):
     """All batches of a workload; returns host arrays start[V][N],
     finish[V][N], makespan[V] in variant order."""
     import torch
     di = BT.to_device(g, vs)
-    res = BT.simulate(di, mode=mode, want_start=want_start)
+    res = BT.simulate(di, mode=mode, want_start=want_start, variants_per_wg=variants_per_wg)
     torch.cuda.synchronize()
     V = vs.n_variants
     fin = np.zeros((V, g.n), np.int64)

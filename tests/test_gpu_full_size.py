@@ -1,9 +1,11 @@
 """Parity at full size: the 1,048,576-task x 2,048-variant transformer sweep
 (32 chained iterations) in the launch configuration the benchmark times (one
-batch, phase schedule, every variant in one dd_simulate_batch call).  The
-oracle checks a sample of variant columns exactly (finish of every task and
-the makespan); properties that hold for every variant are checked on all
-2,048 columns."""
+batch, phase schedule, every variant in one dd_simulate_batch call).  Every
+makespan and every finish column is compared exactly with the oracle; the
+finish array (16 GiB) stays on the GPU and is compared in chunks of 128
+variant columns."""
+import time
+
 import numpy as np
 import pytest
 
@@ -13,9 +15,9 @@ from paper_2006_03318_amd import binding as B
 from paper_2006_03318_amd import workloads as W
 from tests.gpu_common import assert_equal_arrays, require_gpu, say
 
-pytestmark = pytest.mark.gpu
+pytestmark = [pytest.mark.gpu, pytest.mark.timeout(1200)]
 
-SAMPLE = [0, 1, 2, 7, 8, 15, 16, 1023, 1024, 2046, 2047]
+CHUNK = 128
 
 
 @pytest.fixture(scope="module")
@@ -29,31 +31,29 @@ def config5():
     torch.cuda.synchronize()
     assert len(res) == 1
     v0, v1, fin, _, ms = res[0]
-    idx = torch.tensor(SAMPLE, device=fin.device)
-    cols = fin.index_select(1, idx).cpu().numpy().T          # [len(SAMPLE)][N]
-    last = fin.max(dim=0).values.cpu().numpy()               # max finish per variant
-    out = dict(g=g, vs=vs, cols=cols, ms=ms.cpu().numpy(), last=last)
-    del fin, res, di
+    del di
+    yield dict(g=g, vs=vs, fin=fin, ms=ms.cpu().numpy())
+    del fin, res
     torch.cuda.empty_cache()
-    return out
 
 
-def test_sampled_variants_bit_exact(config5):
+def test_every_makespan_bit_exact(config5):
     g, vs = config5["g"], config5["vs"]
-    _, oF, oM, _ = O.run(g, vs, variants=SAMPLE, want_start=False)
-    assert_equal_arrays("config 5 makespan", config5["ms"][SAMPLE], oM)
-    assert_equal_arrays("config 5 finish", config5["cols"], oF)
+    t0 = time.time()
+    _, _, oM, _ = O.run(g, vs, want_start=False, want_finish=False)
+    say("oracle: 2048 makespans in %.1f s" % (time.time() - t0))
+    assert config5["ms"].shape == (2048,)
+    assert_equal_arrays("config 5 makespan", config5["ms"], oM)
 
 
-def test_every_variant_properties(config5):
-    """Makespan = largest finish of a task kept in the variant; with removal
-    (finish of a removed task equals its start) the largest finish overall
-    can exceed it only through removed tasks, never fall below it."""
-    ms, last = config5["ms"], config5["last"]
-    assert ms.shape == (2048,)
-    assert (ms > 0).all()
-    assert (last >= ms).all()
-    # variant 0 is the untransformed graph: identity scales, nothing removed
-    _, _, o0, _ = O.run(config5["g"], config5["vs"], variants=[0], want_start=False,
-                        want_finish=False)
-    assert ms[0] == o0[0]
+def test_every_finish_column_bit_exact(config5):
+    g, vs, fin = config5["g"], config5["vs"], config5["fin"]
+    V = vs.n_variants
+    for c0 in range(0, V, CHUNK):
+        c1 = min(V, c0 + CHUNK)
+        t0 = time.time()
+        got = fin[:, c0:c1].t().contiguous().cpu().numpy()       # [c1-c0][N]
+        _, oF, _, _ = O.run(g, vs, variants=range(c0, c1), want_start=False)
+        assert_equal_arrays("config 5 finish, variants %d..%d" % (c0, c1 - 1), got, oF)
+        say("finish columns %d..%d equal (%.1f s)" % (c0, c1 - 1, time.time() - t0))
+        del got, oF

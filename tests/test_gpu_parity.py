@@ -15,9 +15,9 @@ from tests.gpu_common import assert_equal_arrays, gpu_run, require_gpu, say
 pytestmark = pytest.mark.gpu
 
 
-def _check(g, vs, mode=B.DD_PHASES, label=""):
-    say("parity", label, "n=%d V=%d mode=%d" % (g.n, vs.n_variants, mode))
-    S, F, M = gpu_run(g, vs, mode=mode)
+def _check(g, vs, mode=B.DD_PHASES, label="", variants_per_wg=0):
+    say("parity", label, "n=%d V=%d mode=%d vs=%d" % (g.n, vs.n_variants, mode, variants_per_wg))
+    S, F, M = gpu_run(g, vs, mode=mode, variants_per_wg=variants_per_wg)
     oS, oF, oM, _ = O.run(g, vs)
     assert_equal_arrays(label + " makespan", M, oM)
     assert_equal_arrays(label + " finish", F, oF)
@@ -71,27 +71,25 @@ def test_configs_levels_mode(k):
 
 
 @pytest.mark.parametrize("vs_width", [1, 2, 4, 8, 16])
-def test_every_variant_width(vs_width, monkeypatch):
+def test_every_variant_width(vs_width):
     """Each compiled variants-per-workgroup width gives the same answer,
     including a last workgroup that is only partly used."""
     require_gpu()
-    monkeypatch.setenv("DD_VS", str(vs_width))
     g, vs = W.config(1, variants=37)
-    _check(g, vs, B.DD_PHASES, "width%d" % vs_width)
+    _check(g, vs, B.DD_PHASES, "width%d" % vs_width, vs_width)
     rng = np.random.default_rng(33)
     g = W.random_graph(rng, 500, 3, p_edge=0.01, n_edge_cls=2, max_dur=1000)
     vs = W.random_variants(rng, g, 19, p_remove=0.3)
-    _check(g, vs, B.DD_PHASES, "width%d-random" % vs_width)
+    _check(g, vs, B.DD_PHASES, "width%d-random" % vs_width, vs_width)
 
 
 @pytest.mark.parametrize("vs_width", [1, 2, 4, 8, 16])
-def test_outputs_prefilled_with_sentinel(vs_width, monkeypatch):
+def test_outputs_prefilled_with_sentinel(vs_width):
     """Output buffers start full of a huge sentinel: a read of finish before
     its task is written, or any stale read, shows up as a wrong value.  Odd
     and even variant counts cover both lane layouts of every width."""
     import torch
     require_gpu()
-    monkeypatch.setenv("DD_VS", str(vs_width))
     sent = 1 << 61
     for V in (37, 38):
         g, vs = W.config(1, variants=V)
@@ -101,7 +99,7 @@ def test_outputs_prefilled_with_sentinel(vs_width, monkeypatch):
                  torch.full((v1 - v0,), sent, dtype=torch.int64, device="cuda"))
                 for (v0, v1, *_r) in di.batches]
         say("parity sentinel width%d V=%d" % (vs_width, V))
-        res = BT.simulate(di, want_start=True, outputs=outs)
+        res = BT.simulate(di, want_start=True, outputs=outs, variants_per_wg=vs_width)
         torch.cuda.synchronize()
         oS, oF, oM, _ = O.run(g, vs)
         for v0, v1, f, s_, m in res:

@@ -26,6 +26,10 @@ MUTANTS = {
                             "int64_t f = w->S[u] + w->dd[u] + w->gg[u];"),
     "wrong_variant_bit": ("return (int)((vs->rm_bits[(int64_t)u * W + v / 32] >> (v % 32)) & 1u);",
                           "return (int)((vs->rm_bits[(int64_t)u * W + v / 32] >> ((v + 1) % 32)) & 1u);"),
+    "removal_row_stride_slip": ("int32_t W = (vs->n_variants + 31) / 32;",
+                                "int32_t W = vs->n_variants / 32 + 1;"),
+    "removal_word_index_slip": ("return (int)((vs->rm_bits[(int64_t)u * W + v / 32] >> (v % 32)) & 1u);",
+                                "return (int)((vs->rm_bits[(int64_t)u * W + v / 33] >> (v % 32)) & 1u);"),
 }
 
 
@@ -71,6 +75,21 @@ def _pins_fail(m):
         except Exception:
             return True
         for v in range(vs.n_variants):
+            bS, bF, bms = P.brute_force(g, vs, v)
+            if list(S[v]) != bS or list(F[v]) != bF or ms[v] != bms:
+                return True
+    for seed in range(40):
+        rng = np.random.default_rng(50_000 + seed)
+        n = int(rng.integers(2, 9))
+        g = P.W.random_graph(rng, n, int(rng.integers(1, 4)), p_edge=float(rng.uniform(0.2, 0.6)),
+                             n_edge_cls=int(rng.integers(3, 5)))
+        V = int(rng.choice([33, 64, 65, 97]))
+        vs = P.W.random_variants(rng, g, V, p_remove=0.3)
+        try:
+            S, F, ms, _ = m.run(g, vs)
+        except Exception:
+            return True
+        for v in range(V):
             bS, bF, bms = P.brute_force(g, vs, v)
             if list(S[v]) != bS or list(F[v]) != bF or ms[v] != bms:
                 return True

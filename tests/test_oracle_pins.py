@@ -126,6 +126,33 @@ def test_oracle_equals_brute_force(oracle_mod, seed):
         assert ms[v] == bms
 
 
+@pytest.mark.parametrize("seed", range(40))
+def test_oracle_equals_brute_force_wide_variant_sets(oracle_mod, seed):
+    """Variant counts past one and two 32-bit removal words (33, 64, 65, 97)
+    and three or four edge classes: the removal bit of (task u, variant v)
+    sits in word v // 32 of a row of ceil(V / 32) words, and each variant
+    switches its own subset of edge classes on.  The brute force unpacks the
+    bits with the input module's own routine, not the oracle's indexing."""
+    rng = np.random.default_rng(50_000 + seed)
+    n = int(rng.integers(2, 9))
+    T = int(rng.integers(1, 4))
+    K = int(rng.integers(3, 5))
+    g = W.random_graph(rng, n, T, p_edge=float(rng.uniform(0.2, 0.6)), n_edge_cls=K)
+    V = int(rng.choice([33, 64, 65, 97]))
+    vs = W.random_variants(rng, g, V, p_remove=0.3)
+    S, F, ms, _ = oracle_mod.run(g, vs)
+    # each variant is also run on its own, alone in a set of one variant
+    for v in range(V):
+        bS, bF, bms = brute_force(g, vs, v)
+        assert list(S[v]) == bS, (v, V)
+        assert list(F[v]) == bF, (v, V)
+        assert ms[v] == bms, (v, V)
+    for v in (V - 1, 32, 31):
+        one = vs.subset(v, v + 1)
+        S1, F1, ms1, _ = oracle_mod.run(g, one)
+        assert list(S1[0]) == list(S[v]) and ms1[0] == ms[v]
+
+
 @pytest.mark.parametrize("seed", range(150, 230))
 def test_unlink_reading_equals_contracted_brute_force(oracle_mod, seed):
     g, vs = _random_case(seed)

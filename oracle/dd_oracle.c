@@ -376,10 +376,40 @@ static int run_variant(const ddo_graph *g, const ddo_struct *st, const ddo_varia
 }
 
 /* ------------------------------------------------------------------ */
+/* Runtime breakdown of the evaluation of AMP (Sec. 6.2, Fig. 6), from one
+ * variant's simulated schedule, by the paper's own rules for computing it:
+ *   total    = the iteration time (makespan);
+ *   CPU-only = total minus all GPU kernel runtime (the kernels' durations);
+ *   GPU-only = the time the CPU is blocked waiting for the GPU: for every
+ *              synchronization call and every device-to-host copy call, from
+ *              the moment its thread reached it (the release of the previous
+ *              task on the thread, 0 for the first) to the moment it starts
+ *              (the simulation starts it when the GPU work it waits on is done;
+ *              its own duration is the call's CPU time);
+ *   CPU+GPU parallel = total - CPU-only - GPU-only.
+ * role[u]: 1 = GPU kernel, 2 = CPU call that waits for the GPU, 0 = other. */
+static void breakdown(const ddo_graph *g, const uint8_t *role, const work *w, int64_t ms,
+                      int64_t *out) {
+    int64_t gpu = 0, wait = 0;
+    for (int32_t u = 0; u < g->n; u++) {
+        if (role[u] == 1) gpu += w->dd[u];
+        if (role[u] == 2) {
+            int32_t p = g->thread_prev[u];
+            int64_t reached = p >= 0 ? w->S[p] + w->dd[p] + w->gg[p] : 0;
+            wait += w->S[u] - reached;
+        }
+    }
+    out[0] = ms;
+    out[1] = ms - gpu;
+    out[2] = wait;
+    out[3] = ms - out[1] - out[2];
+}
+
 typedef struct {
     const ddo_graph *g; const ddo_struct *st; const ddo_variants *vs;
     const int32_t *vlist; int32_t n_list; int mode, tie;
     int64_t *start, *finish, *makespan, *bindings;
+    const uint8_t *role; int64_t *bd;        /* breakdown: role [n] in, [n_list][4] out */
     int32_t next; pthread_mutex_t mu; int rc;
 } job;
 
@@ -409,6 +439,8 @@ static void *worker(void *arg) {
             pthread_mutex_lock(&j->mu);
             if (j->rc == 0) j->rc = rc;
             pthread_mutex_unlock(&j->mu);
+        } else if (j->role) {
+            breakdown(j->g, j->role, &w, j->makespan[i], j->bd + (int64_t)i * 4);
         }
     }
     free(w.dd); free(w.gg); free(w.est); free(w.S); free(w.ref); free(w.rm); free(w.done);
@@ -435,10 +467,33 @@ static int check(const ddo_graph *g, const ddo_variants *vs) {
     return DDO_OK;
 }
 
+static int run_job(const ddo_graph *g, const ddo_variants *vs,
+                   const int32_t *vlist, int32_t n_list, int32_t mode, int32_t tie,
+                   int64_t *start, int64_t *finish, int64_t *makespan, int64_t *bindings,
+                   const uint8_t *role, int64_t *bd, int32_t n_workers);
+
 int ddo_run(const ddo_graph *g, const ddo_variants *vs,
             const int32_t *vlist, int32_t n_list, int32_t mode, int32_t tie,
             int64_t *start, int64_t *finish, int64_t *makespan, int64_t *bindings,
             int32_t n_workers) {
+    return run_job(g, vs, vlist, n_list, mode, tie, start, finish, makespan, bindings, NULL, NULL,
+                   n_workers);
+}
+
+/* The runtime breakdown (see breakdown()) of each listed variant after the
+ * simulation (mode 0): out [n_list][4] = total, CPU-only, GPU-only,
+ * CPU+GPU parallel. */
+int ddo_breakdown(const ddo_graph *g, const ddo_variants *vs, const uint8_t *role,
+                  const int32_t *vlist, int32_t n_list, int64_t *makespan, int64_t *out,
+                  int32_t n_workers) {
+    if (!role) return DDO_EINVAL;
+    return run_job(g, vs, vlist, n_list, 0, 0, NULL, NULL, makespan, NULL, role, out, n_workers);
+}
+
+static int run_job(const ddo_graph *g, const ddo_variants *vs,
+                   const int32_t *vlist, int32_t n_list, int32_t mode, int32_t tie,
+                   int64_t *start, int64_t *finish, int64_t *makespan, int64_t *bindings,
+                   const uint8_t *role, int64_t *bd, int32_t n_workers) {
     int rc = check(g, vs);
     if (rc) return rc;
     for (int32_t i = 0; i < n_list; i++)
@@ -451,7 +506,7 @@ int ddo_run(const ddo_graph *g, const ddo_variants *vs,
     memset(&j, 0, sizeof(j));
     j.g = g; j.st = &st; j.vs = vs; j.vlist = vlist; j.n_list = n_list;
     j.mode = mode; j.tie = tie; j.start = start; j.finish = finish;
-    j.makespan = makespan; j.bindings = bindings;
+    j.makespan = makespan; j.bindings = bindings; j.role = role; j.bd = bd;
     pthread_mutex_init(&j.mu, NULL);
     if (n_workers < 1) n_workers = 1;
     if (n_workers > n_list) n_workers = n_list > 0 ? n_list : 1;

@@ -61,6 +61,10 @@ def _load():
                                  ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                  ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32]
+        _lib.ddo_breakdown.restype = ctypes.c_int
+        _lib.ddo_breakdown.argtypes = [ctypes.POINTER(_Graph), ctypes.POINTER(_Variants),
+                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32]
         _lib.ddo_steps.restype = ctypes.c_int
         _lib.ddo_steps.argtypes = [ctypes.POINTER(_Graph), ctypes.c_uint64, ctypes.c_void_p,
                                    ctypes.c_void_p]
@@ -146,3 +150,32 @@ def run(g, vs, variants: Optional[Sequence[int]] = None, mode: int = 0, tie: int
     if rc != OK:
         raise OracleError(rc)
     return start, finish, ms, nb
+
+
+def breakdown(g, vs, role, variants: Optional[Sequence[int]] = None,
+              workers: Optional[int] = None):
+    """Runtime breakdown (Sec. 6.2, Fig. 6) of the listed variants from the
+    oracle's own simulation: int64 [len(variants)][4] = total, CPU-only,
+    GPU-only, CPU+GPU parallel.  role: uint8 [N], 1 = GPU kernel, 2 = CPU call
+    that waits for the GPU (synchronization, device-to-host copy), 0 = other."""
+    lib = _load()
+    gs, keep = _graph_struct(g)
+    scale = np.ascontiguousarray(vs.scale, np.int32)
+    rb = np.ascontiguousarray(vs.remove_bits, np.uint32)
+    eo = np.ascontiguousarray(vs.edge_on, np.uint64)
+    vv = _Variants(int(vs.n_variants), int(scale.shape[0]), _p(scale), _p(rb),
+                   int(eo.shape[1]), _p(eo))
+    if variants is None:
+        variants = range(vs.n_variants)
+    vl = np.ascontiguousarray(np.array(list(variants), np.int32))
+    rl = np.ascontiguousarray(role, np.uint8)
+    L = vl.shape[0]
+    ms = np.zeros(L, np.int64)
+    out = np.zeros((L, 4), np.int64)
+    if workers is None:
+        workers = max(1, min(len(os.sched_getaffinity(0)), 16))
+    rc = lib.ddo_breakdown(ctypes.byref(gs), ctypes.byref(vv), _p(rl), _p(vl), L, _p(ms),
+                           _p(out), int(workers))
+    if rc != OK:
+        raise OracleError(rc)
+    return out

@@ -34,7 +34,7 @@ MUTANTS = {
 
 
 def _build_mutant(name):
-    old, new = MUTANTS[name]
+    old, new = MUTANTS_ALL[name]
     src = open(SRC).read()
     assert src.count(old) >= 1, name
     src = src.replace(old, new, 1)
@@ -47,11 +47,24 @@ def _build_mutant(name):
     return so
 
 
+BREAKDOWN_MUTANTS = {
+    "bd_wait_until_finish": ("wait += w->S[u] - reached;", "wait += w->S[u] + w->dd[u] - reached;"),
+    "bd_reached_without_gap": ("int64_t reached = p >= 0 ? w->S[p] + w->dd[p] + w->gg[p] : 0;",
+                               "int64_t reached = p >= 0 ? w->S[p] + w->dd[p] : 0;"),
+    "bd_unscaled_kernel_time": ("if (role[u] == 1) gpu += w->dd[u];",
+                                "if (role[u] == 1) gpu += g->dur[u];"),
+    "bd_parallel_sign": ("out[3] = ms - out[1] - out[2];", "out[3] = ms - out[1] + out[2];"),
+}
+MUTANTS_ALL = dict(MUTANTS, **BREAKDOWN_MUTANTS)
+
+
 class _Mut:
     def __init__(self, so):
         lib = ctypes.CDLL(so)
         lib.ddo_run.restype = ctypes.c_int
         lib.ddo_run.argtypes = O._load().ddo_run.argtypes
+        lib.ddo_breakdown.restype = ctypes.c_int
+        lib.ddo_breakdown.argtypes = O._load().ddo_breakdown.argtypes
         self.lib = lib
         self.OracleError = O.OracleError
         self.ECYCLE = O.ECYCLE
@@ -61,6 +74,14 @@ class _Mut:
         O._lib = self.lib
         try:
             return O.run(*a, **k)
+        finally:
+            O._lib = saved
+
+    def breakdown(self, *a, **k):
+        saved = O._lib
+        O._lib = self.lib
+        try:
+            return O.breakdown(*a, **k)
         finally:
             O._lib = saved
 
@@ -106,3 +127,30 @@ def test_planted_mistake_is_caught(name):
     O.build(force=False)
     m = _Mut(_build_mutant(name))
     assert _pins_fail(m), "pins did not catch mutant " + name
+
+
+def _breakdown_pins_fail(m):
+    from tests import test_oracle_breakdown as BD
+    g, role, expect = BD._read_toy()
+    if list(m.breakdown(g, P.H.variants(g, V=1), role)[0]) != expect:
+        return True
+    for seed in range(60):
+        rng = np.random.default_rng(170_000 + seed)
+        g, role = BD._trace(rng, int(rng.integers(1, 6)), two_cpu=seed % 2 == 1)
+        V = 4
+        scales = [{}] + [{c: (int(rng.integers(0, 5)), int(rng.choice([1, 2, 3]))) for c in (0, 1)}
+                         for _ in range(V - 1)]
+        removed = [[]] + [[u for u in range(g.n) if rng.random() < 0.2] for _ in range(V - 1)]
+        vs = P.H.variants(g, scales=scales, removed=removed, V=V)
+        out = m.breakdown(g, vs, role)
+        for v in range(V):
+            if list(out[v]) != BD._stepwise(g, vs, v, role):
+                return True
+    return False
+
+
+@pytest.mark.parametrize("name", sorted(BREAKDOWN_MUTANTS))
+def test_planted_breakdown_mistake_is_caught(name):
+    O.build(force=False)
+    m = _Mut(_build_mutant(name))
+    assert _breakdown_pins_fail(m), "breakdown pins did not catch mutant " + name

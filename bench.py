@@ -41,6 +41,58 @@ def algorithmic_bytes(n, V, n_gathers, n_cls, want_start=False):
             + n_cls * V * 16.0)
 
 
+def breakdown_bytes(n_role, n_wait, n, V, n_cls):
+    """Bytes one runtime-breakdown call must move at minimum: the removal
+    bit of every (task with a role, variant); the finish of every waiting
+    call and of its thread predecessor per variant; per task the role and
+    class (counting sort) and, for tasks with a role, duration, class, role
+    and order entry; the scale table; the output."""
+    return (n_role * V / 8.0 + 2.0 * n_wait * V * 8.0 + n * 3.0 + n_role * 19.0
+            + n_cls * V * 16.0 + V * 32.0)
+
+
+def bench_breakdown(di, g, vs, stream, reps):
+    """Time dd_runtime_breakdown on one simulated batch (HIP events on the
+    launching stream)."""
+    import torch
+    from paper_2006_03318_amd import batch, binding as B, workloads as W
+    role = torch.from_numpy(W.task_roles(g)).to(di.tensors["dur"].device)
+    res, gh, handles = batch.simulate(di, stream=stream, keep_handles=True)
+    times = []
+    nbytes = 0.0
+    try:
+        outs = [torch.empty((v1 - v0, 4), dtype=torch.int64, device=fin.device)
+                for (v0, v1, fin, _s, _m) in res]
+        rn = W.task_roles(g)
+        n_role, n_wait = int((rn == 1).sum() + (rn == 2).sum()), int((rn == 2).sum())
+        for (v0, v1, *_r) in res:
+            nbytes += breakdown_bytes(n_role, n_wait, g.n, v1 - v0, di.n_cls)
+        for it in range(reps + 2):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for (v0, v1, fin, _s, ms), (_sch, var), out in zip(res, handles, outs):
+                B.dd_runtime_breakdown(gh, var, role, fin, ms, out, stream)
+            e1.record(stream)
+            stream.synchronize()
+            if it >= 2:
+                times.append(e0.elapsed_time(e1))
+    finally:
+        for sch, var in handles:
+            B.dd_sched_free(sch)
+            B.dd_variants_free(var)
+        B.dd_graph_free(gh)
+    ms_call = float(np.mean(times))
+    achieved = nbytes / (ms_call / 1e3) / 1e9
+    pairs = float(n_role) * vs.n_variants
+    return {"kernel": "k_bd_accum", "calls_timed": reps, "avg_call_ms": round(ms_call, 4),
+            "tasks_with_role": n_role, "waiting_calls": n_wait,
+            "task_variant_pairs_per_s": round(pairs / (ms_call / 1e3), 1),
+            "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                         "traffic": None, "algorithmic_bytes_per_call": int(nbytes)}}
+
+
 def kernel_source_digest():
     """sha256 over the sources the simulation kernel is compiled from."""
     import hashlib
@@ -84,6 +136,8 @@ def main():
     ap.add_argument("--cpu-workers", type=int, default=16,
                     help="oracle worker threads at most (the host share of one GPU is 16 "
                          "cores)")
+    ap.add_argument("--breakdown-reps", type=int, default=5,
+                    help="timed dd_runtime_breakdown calls after the steps (0 = skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device to device three times: the plain copy "
                          "whose byte counters scale the simulation kernel's")
@@ -197,6 +251,12 @@ def main():
                 "avg_launch_ms": round(sim_ms / len(di.batches), 4),
                 "launches_per_step": len(di.batches)}
 
+    # the runtime breakdown (CPU-only / GPU-only / CPU+GPU parallel) of every
+    # variant, after the timed steps
+    bd = None
+    if args.breakdown_reps > 0:
+        bd = bench_breakdown(di, g, vs, stream, args.breakdown_reps)
+
     # parity sample + CPU baseline: the oracle on the first variants
     cpu = None
     parity = None
@@ -252,6 +312,7 @@ def main():
         "simulate_only_updates_per_s": round(NV / (sim_ms / 1e3), 1),
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "runtime_breakdown": bd,
         "parity_sample_makespans_equal": parity,
     }
     print(json.dumps(out))

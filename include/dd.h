@@ -181,6 +181,33 @@ dd_status dd_simulate_batch_vs(const dd_graph *g, const dd_sched *sched, const d
                                int32_t variants_per_wg, void *stream);
 
 /*
+ * dd_runtime_breakdown -- where each variant's iteration time goes when the
+ * CPU and the GPU overlap: the breakdown the paper uses to explain the AMP
+ * speedups (Sec. 6.2, Fig. 6), computed by its own rules from a finished
+ * dd_simulate_batch of the same graph and variants:
+ *   total    = makespan;
+ *   CPU-only = total - all GPU kernel runtime (the sum of the scaled
+ *              durations of the kernels kept in the variant);
+ *   GPU-only = the time the CPU is blocked on the GPU: for every call that
+ *              waits for GPU work (synchronization, device-to-host copy), its
+ *              start minus the moment its thread reached it (the release
+ *              start + duration + gap of the previous task on the thread, 0
+ *              for the first task);
+ *   CPU+GPU parallel = total - CPU-only - GPU-only.
+ *   role        uint8 [n], host or device: 1 = GPU kernel, 2 = CPU call that
+ *               waits for GPU work, any other value = neither.
+ *   d_finish    device int64 [n][V], d_makespan device int64 [V]: the outputs
+ *               of dd_simulate_batch for (g, var), complete on `stream`.
+ *   d_out       device int64 [V][4]: total, CPU-only, GPU-only, CPU+GPU
+ *               parallel of each variant.
+ * Asynchronous like dd_simulate_batch.  DD_EMISMATCH if var comes from
+ * another graph.
+ */
+dd_status dd_runtime_breakdown(const dd_graph *g, const dd_variants *var, const uint8_t *role,
+                               const int64_t *d_finish, const int64_t *d_makespan,
+                               int64_t *d_out, void *stream);
+
+/*
  * dd_release_cache -- wait for all work on the current device, then return
  * every block of the library's device-memory cache for that device to the
  * device (hipFree).  Memory held by live handles is not touched.  For callers

@@ -7,4 +7,5 @@ from . import binding  # noqa: F401
 from .binding import (DD_LEVELS, DD_PHASES, DDError, dd_apply_transforms, dd_graph_free,  # noqa: F401
                       dd_graph_load, dd_last_error, dd_levelize, dd_release_cache,
                       dd_sched_free, dd_sched_info, dd_sched_task_steps, dd_simulate_batch,
-                      dd_simulate_batch_vs, dd_status_str, dd_variants_free)
+                      dd_runtime_breakdown, dd_simulate_batch_vs, dd_status_str,
+                      dd_variants_free)

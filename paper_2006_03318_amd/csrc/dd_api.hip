@@ -514,6 +514,33 @@ dd_status dd_simulate_batch_vs(const dd_graph *g, const dd_sched *sched, const d
     return simulate_impl(g, sched, var, d_finish, d_start, d_makespan, variants_per_wg, stream);
 }
 
+dd_status dd_runtime_breakdown(const dd_graph *g, const dd_variants *var, const uint8_t *role,
+                               const int64_t *d_finish, const int64_t *d_makespan,
+                               int64_t *d_out, void *stream) {
+    g_err[0] = 0;
+    if (!g || !var) return fail(DD_EINVAL, "NULL handle");
+    if (!d_makespan || !d_out || (g->n > 0 && (!d_finish || !role)))
+        return fail(DD_EINVAL, "role, d_finish, d_makespan and d_out are required");
+    if (var->graph_id != g->id) return fail(DD_EMISMATCH, "handles come from different graphs");
+    hipStream_t s = (hipStream_t)stream;
+    dd_status st = DD_OK;
+    uint8_t *d_role = nullptr;
+    int64_t *scratch = nullptr;
+    int32_t *order = nullptr;
+    TRY(copy_in(&d_role, role, (size_t)g->n, s), "copy role");
+    TRY(dd::dalloc_n(&scratch, 2 * (size_t)var->V + (size_t)var->n_cls + 1, s), "alloc");
+    TRY(dd::dalloc_n(&order, (size_t)g->n + 1, s), "alloc");
+    TRY(dd::launch_breakdown(g, var, d_role, d_finish, d_makespan, scratch, order, d_out, s),
+        "breakdown");
+    TRY(dd::note_use(g->uses, g->stream, s), "record stream use");
+    TRY(dd::note_use(var->uses, var->stream, s), "record stream use");
+fail_out:
+    dd::dfree(d_role, s);
+    dd::dfree(scratch, s);
+    dd::dfree(order, s);
+    return st;
+}
+
 dd_status dd_release_cache(void) {
     g_err[0] = 0;
     hipError_t e = dd::release_cache();

@@ -202,4 +202,12 @@ hipError_t launch_simulate(const dd_graph *g, const dd_sched *sch, const dd_vari
                            int64_t *finish, int64_t *start, int64_t *makespan, int vs_hint,
                            hipStream_t s);
 
+// runtime breakdown (k_breakdown.hip): scratch [2 * V + n_cls + 1] int64,
+// order [n] int32, out [V][4]
+hipError_t launch_breakdown(const dd_graph *g, const dd_variants *var, const uint8_t *role_dev,
+                            const int64_t *finish, const int64_t *makespan, int64_t *scratch,
+                            int32_t *order, int64_t *out, hipStream_t s);
+
+
+
 }  // namespace dd

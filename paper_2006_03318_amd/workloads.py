@@ -592,6 +592,16 @@ def _seq2seq_variants(rng, g: TaskGraph, L: int, V: int) -> VariantSet:
     return VariantSet(V, s, rb, eo, [(0, V, 1)])
 
 
+def task_roles(g: TaskGraph) -> np.ndarray:
+    """Roles for the runtime breakdown: 1 = GPU kernel, 2 = CPU call that
+    waits for GPU work (the synchronization tasks), 0 = anything else
+    (launch calls, memory copies, communication)."""
+    role = np.zeros(g.n, np.uint8)
+    role[np.isin(g.kind, GPU_KINDS)] = 1
+    role[g.kind == K_SYNC] = 2
+    return role
+
+
 # ---------------------------------------------------------------------------
 def random_graph(rng, n: int, n_threads: int, p_edge: float = 0.3, max_dur: int = 20,
                  zero_frac: float = 0.2, n_edge_cls: int = 1,

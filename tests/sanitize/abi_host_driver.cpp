@@ -36,6 +36,8 @@ hipError_t launch_build_scale_table(const dd_ratio *, int32_t, int32_t, ScaleEnt
                                     hipStream_t) { STUB; }
 hipError_t launch_simulate(const dd_graph *, const dd_sched *, const dd_variants *, int64_t *,
                            int64_t *, int64_t *, int, hipStream_t) { STUB; }
+hipError_t launch_breakdown(const dd_graph *, const dd_variants *, const uint8_t *, const int64_t *,
+                            const int64_t *, int64_t *, int32_t *, int64_t *, hipStream_t) { STUB; }
 }  // namespace dd
 
 static int g_bad = 0;
@@ -88,6 +90,7 @@ int main() {
     EXPECT(strstr(dd_last_error(), "variants_per_wg") != nullptr, "width message");
     EXPECT(dd_simulate_batch_vs(nullptr, nullptr, nullptr, dummy, nullptr, dummy, 32, nullptr) == DD_EINVAL, "width 32 rejected");
     EXPECT(dd_simulate_batch_vs(nullptr, nullptr, nullptr, dummy, nullptr, dummy, 16, nullptr) == DD_EINVAL, "width 16 NULL handles");
+    EXPECT(dd_runtime_breakdown(nullptr, nullptr, nullptr, dummy, dummy, dummy, nullptr) == DD_EINVAL, "breakdown NULL handles");
     EXPECT(strstr(dd_last_error(), "NULL handle") != nullptr, "NULL handle message");
     EXPECT(dd_sched_task_steps(nullptr, nullptr, nullptr) == DD_EINVAL, "steps NULL");
     int64_t a, b, c, d;

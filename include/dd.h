@@ -181,6 +181,28 @@ dd_status dd_simulate_batch_vs(const dd_graph *g, const dd_sched *sched, const d
                                int32_t variants_per_wg, void *stream);
 
 /*
+ * dd_simulate_batch_noalloc -- dd_simulate_batch for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, results and errors as
+ * dd_simulate_batch (default launch shape); it calls no hipMalloc, hipFree
+ * or other allocating routine and records no events.
+ *   Its working memory (round table, scan sums, per-position removal bits)
+ *   lives in one array of 64 MiB per GPU inside the library, held until the
+ *   process ends.  A batch needs about n*V/8 + 16*n_steps + 4*n/64 bytes of
+ *   it (n*V up to about 5 * 10^8 task-variant pairs); a larger one returns
+ *   DD_EINVAL with the size in dd_last_error() and launches nothing.
+ *   Every call on one GPU uses that GPU's array: calls that overlap on one
+ *   GPU (on different streams, or from several host threads) race and give
+ *   wrong results.  The array keeps the last call's contents; nothing in it
+ *   needs to start at zero.
+ *   Handles used here on a stream other than their own are not tracked (no
+ *   event is recorded): free them only after that stream's work is done.
+ */
+dd_status dd_simulate_batch_noalloc(const dd_graph *g, const dd_sched *sched, const dd_variants *var,
+                                    int64_t *d_finish, int64_t *d_start, int64_t *d_makespan,
+                                    void *stream);
+
+/*
  * dd_runtime_breakdown -- where each variant's iteration time goes when the
  * CPU and the GPU overlap: the breakdown the paper uses to explain the AMP
  * speedups (Sec. 6.2, Fig. 6), computed by its own rules from a finished

@@ -61,6 +61,7 @@ def lib():
         "dd_simulate_batch": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _vp]),
         "dd_simulate_batch_vs": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp]),
         "dd_release_cache": (_i32, []),
+        "dd_simulate_batch_noalloc": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _vp]),
         "dd_runtime_breakdown": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _vp]),
         "dd_sched_task_steps": (_i32, [_vp, _vp, _vp]),
         "dd_sched_info": (_i32, [_vp, ctypes.POINTER(_i64), ctypes.POINTER(_i64),
@@ -173,6 +174,13 @@ def dd_runtime_breakdown(g, var, role, d_finish, d_makespan, d_out, stream=None)
     rc = lib().dd_runtime_breakdown(g, var, _ptr(role, "uint8"), _ptr(d_finish, "int64"),
                                     _ptr(d_makespan, "int64"), _ptr(d_out, "int64"),
                                     _stream(stream))
+    _check(rc)
+
+
+def dd_simulate_batch_noalloc(g, sched, var, d_finish, d_start, d_makespan, stream=None):
+    rc = lib().dd_simulate_batch_noalloc(g, sched, var, _ptr(d_finish, "int64"),
+                                         _ptr(d_start, "int64"), _ptr(d_makespan, "int64"),
+                                         _stream(stream))
     _check(rc)
 
 

@@ -541,6 +541,29 @@ fail_out:
     return st;
 }
 
+dd_status dd_simulate_batch_noalloc(const dd_graph *g, const dd_sched *sched, const dd_variants *var,
+                                    int64_t *d_finish, int64_t *d_start, int64_t *d_makespan,
+                                    void *stream) {
+    g_err[0] = 0;
+    if (!g || !sched || !var) return fail(DD_EINVAL, "NULL handle");
+    if (!d_makespan || (!d_finish && g->n > 0))
+        return fail(DD_EINVAL, "d_finish and d_makespan are required");
+    if (sched->graph_id != g->id || var->graph_id != g->id)
+        return fail(DD_EMISMATCH, "handles come from different graphs");
+    const uint64_t missing = var->used_mask & g->cross_mask & ~sched->mask;
+    if (missing)
+        return fail(DD_EMISMATCH, "variants switch on edge classes 0x%llx that the schedule was not built for",
+                    (unsigned long long)missing);
+    size_t need = 0, limit = 0;
+    hipError_t e = dd::simulate_noalloc(g, sched, var, d_finish, d_start, d_makespan,
+                                        (hipStream_t)stream, &need, &limit);
+    if (need > limit)
+        return fail(DD_EINVAL, "this batch needs %zu bytes of scratch; the allocation-free entry "
+                               "point has %zu (use dd_simulate_batch)", need, limit);
+    if (e != hipSuccess) return hip_fail(e, "simulate launch");
+    return DD_OK;
+}
+
 dd_status dd_release_cache(void) {
     g_err[0] = 0;
     hipError_t e = dd::release_cache();

@@ -160,6 +160,10 @@ hipError_t dalloc_n(T **p, size_t count, hipStream_t s) {
 
 // exclusive prefix sum: out[i] = sum_{j<i} in[j] for i in [0, n]; in/out may alias
 hipError_t scan_exclusive(const int64_t *in, int64_t *out, int64_t n, hipStream_t s);
+// the same with the caller's temporaries: tmp holds scan_temp_count(n) int64
+int64_t scan_temp_count(int64_t n);
+hipError_t scan_exclusive_ws(const int64_t *in, int64_t *out, int64_t n, int64_t *tmp,
+                             hipStream_t s);
 
 inline int grid_for(int64_t n, int bs) {
     int64_t g = (n + bs - 1) / bs;
@@ -201,6 +205,12 @@ hipError_t launch_build_scale_table(const dd_ratio *scale_dev, int32_t n_cls, in
 hipError_t launch_simulate(const dd_graph *g, const dd_sched *sch, const dd_variants *var,
                            int64_t *finish, int64_t *start, int64_t *makespan, int vs_hint,
                            hipStream_t s);
+// the same in the library's per-GPU scratch array, allocating nothing:
+// *need = bytes this call needs, *limit = the array's size;
+// hipErrorInvalidValue when need > limit (nothing launched)
+hipError_t simulate_noalloc(const dd_graph *g, const dd_sched *sch, const dd_variants *var,
+                            int64_t *finish, int64_t *start, int64_t *makespan, hipStream_t s,
+                            size_t *need, size_t *limit);
 
 // runtime breakdown (k_breakdown.hip): scratch [2 * V + n_cls + 1] int64,
 // order [n] int32, out [V][4]

@@ -67,17 +67,27 @@ __global__ __launch_bounds__(kScanBS) void k_scan_apply(const int64_t *in, int64
 }
 }  // namespace
 
-hipError_t scan_exclusive(const int64_t *in, int64_t *out, int64_t n, hipStream_t s) {
-    int64_t nc = (n + kScanChunk - 1) / kScanChunk;
-    if (nc < 1) nc = 1;
-    int64_t *csum = nullptr;
-    hipError_t e = dalloc_n(&csum, (size_t)nc, s);
-    if (e != hipSuccess) return e;
+int64_t scan_temp_count(int64_t n) {
+    const int64_t nc = (n + kScanChunk - 1) / kScanChunk;
+    return nc < 1 ? 1 : nc;
+}
+
+hipError_t scan_exclusive_ws(const int64_t *in, int64_t *out, int64_t n, int64_t *csum,
+                             hipStream_t s) {
+    const int64_t nc = scan_temp_count(n);
     if (n > 0) k_scan_chunk_sums<<<(unsigned)nc, kScanBS, 0, s>>>(in, n, csum);
-    else (void)hipMemsetAsync(csum, 0, sizeof(int64_t), s);
-    k_scan_chunk_offsets<<<1, 1024, 0, s>>>(csum, n > 0 ? nc : 1, out + n);
+    // (with n == 0 the single chunk sum is never read: the offsets pass
+    // scans one chunk of zero tasks)
+    k_scan_chunk_offsets<<<1, 1024, 0, s>>>(csum, n > 0 ? nc : 0, out + n);
     if (n > 0) k_scan_apply<<<(unsigned)nc, kScanBS, 0, s>>>(in, n, csum, out);
-    e = hipGetLastError();
+    return hipGetLastError();
+}
+
+hipError_t scan_exclusive(const int64_t *in, int64_t *out, int64_t n, hipStream_t s) {
+    int64_t *csum = nullptr;
+    hipError_t e = dalloc_n(&csum, (size_t)scan_temp_count(n), s);
+    if (e != hipSuccess) return e;
+    e = scan_exclusive_ws(in, out, n, csum, s);
     dfree(csum, s);
     return e;
 }

@@ -37,6 +37,7 @@
 
 #include <stdlib.h>
 
+#include <mutex>
 #include <type_traits>
 
 namespace dd {
@@ -1073,29 +1074,67 @@ bool table_fits(int32_t n_cls) {
     return at.sharedSizeBytes + (size_t)n_cls * VS * sizeof(uint64_t) <= kLdsBytes;
 }
 
+// Device memory one simulation call uses besides its inputs and outputs:
+// the round table (cnt, r0, rn), the scan's chunk sums, the removal bits per
+// schedule position of each workgroup's variants (rmp) and the target of
+// idle lanes' stores.  Laid out in one region, each piece 256-byte aligned.
+struct SimLayout {
+    size_t cnt, csum, r0, rn, dummy, rmp, bytes;
+};
+
+template <int LPS, int VPL, int K, int NT = kNT>
+SimLayout sim_layout(const dd_sched *sch, const dd_variants *var) {
+    constexpr int VS = LPS * VPL;
+    constexpr int RP = (NT / LPS) * K;
+    typedef typename std::conditional<(VS <= 8), uint8_t, uint16_t>::type RmT;
+    constexpr int64_t kPer = 16 / (int64_t)sizeof(RmT);
+    const int64_t ns = sch->n_steps;
+    const int64_t max_rounds = ns + (sch->n + RP - 1) / RP + 1;
+    const int64_t grid = (var->V + VS - 1) / VS;
+    const int64_t rstride = (sch->n + kPer - 1) / kPer * kPer;
+    SimLayout L{};
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off = (off + bytes + 255) & ~(size_t)255;
+        return at;
+    };
+    L.cnt = take(sizeof(int64_t) * (size_t)(ns + 2));
+    L.csum = take(sizeof(int64_t) * (size_t)scan_temp_count(ns));
+    L.r0 = take(sizeof(int32_t) * (size_t)max_rounds);
+    L.rn = take(sizeof(int32_t) * (size_t)max_rounds);
+    L.dummy = take(sizeof(int64_t) * 2 * NT);
+    L.rmp = take(sizeof(RmT) * (size_t)grid * (size_t)(rstride > 0 ? rstride : kPer));
+    L.bytes = off;
+    return L;
+}
+
+// region == nullptr: the call allocates its memory from the library's cache;
+// else it uses region (at least sim_layout().bytes), allocating nothing
 template <int LPS, int VPL, int K, int NT = kNT>
 hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants *var,
-                       int64_t *finish, int64_t *start, int64_t *makespan, hipStream_t s) {
+                       int64_t *finish, int64_t *start, int64_t *makespan, hipStream_t s,
+                       unsigned char *region) {
     constexpr int VS = LPS * VPL;
     constexpr int RP = (NT / LPS) * K;
     const int64_t ns = sch->n_steps;
-    const int64_t max_rounds = ns + (sch->n + RP - 1) / RP + 1;
     typedef typename std::conditional<(VS <= 8), uint8_t, uint16_t>::type RmT;
     const int grid = (var->V + VS - 1) / VS;
-    int64_t *cnt = nullptr, *dummy = nullptr;
-    int32_t *r0 = nullptr, *rn = nullptr;
-    RmT *rmp = nullptr;
     constexpr int64_t kPer = 16 / (int64_t)sizeof(RmT);
     const int64_t rstride = (sch->n + kPer - 1) / kPer * kPer;   // rmp row stride
-    hipError_t e = dalloc_n(&cnt, (size_t)ns + 2, s);
-    if (e == hipSuccess) e = dalloc_n(&rmp, (size_t)grid * (size_t)(rstride > 0 ? rstride : kPer), s);
-    if (e == hipSuccess) e = dalloc_n(&r0, (size_t)max_rounds, s);
-    if (e == hipSuccess) e = dalloc_n(&rn, (size_t)max_rounds, s);
-    if (e == hipSuccess) e = dalloc_n(&dummy, 2 * NT, s);
-    if (e != hipSuccess) {
-        dfree(cnt, s); dfree(r0, s); dfree(rn, s); dfree(dummy, s); dfree(rmp, s);
-        return e;
+    const SimLayout L = sim_layout<LPS, VPL, K, NT>(sch, var);
+    unsigned char *base = region;
+    hipError_t e = hipSuccess;
+    if (!region) {
+        e = dalloc(reinterpret_cast<void **>(&base), L.bytes, s);
+        if (e != hipSuccess) return e;
     }
+    int64_t *cnt = reinterpret_cast<int64_t *>(base + L.cnt);
+    int64_t *csum = reinterpret_cast<int64_t *>(base + L.csum);
+    int64_t *dummy = reinterpret_cast<int64_t *>(base + L.dummy);
+    int32_t *r0 = reinterpret_cast<int32_t *>(base + L.r0);
+    int32_t *rn = reinterpret_cast<int32_t *>(base + L.rn);
+    RmT *rmp = reinterpret_cast<RmT *>(base + L.rmp);
     if (sch->n > 0) {
         const dim3 tg((unsigned)((sch->n + 127) / 128), (unsigned)((var->W + 63) / 64));
         if (var->W % 4 == 0)
@@ -1106,7 +1145,7 @@ hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants
                                                         var->rm_bits, rmp);
     }
     if (ns > 0) k_round_count<<<grid_for(ns, 256), 256, 0, s>>>(ns, sch->step_ptr, RP, cnt);
-    e = scan_exclusive(cnt, cnt, ns, s);
+    e = scan_exclusive_ws(cnt, cnt, ns, csum, s);
     if (e == hipSuccess && ns > 0)
         k_round_fill<<<grid_for(ns, 256), 256, 0, s>>>(ns, sch->step_ptr, cnt, RP, r0, rn);
     const uint64_t cls_mask = sch->mask & g->cross_mask;
@@ -1130,36 +1169,94 @@ hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants
         else launch_one<LPS, VPL, K, false, false, false, NT>(grid, s, r0, rn, nrp, rc, args);
         e = hipGetLastError();
     }
-    dfree(cnt, s); dfree(r0, s); dfree(rn, s); dfree(dummy, s); dfree(rmp, s);
+    if (!region) dfree(base, s);
     return e;
 }
 
-}  // namespace
-
-hipError_t launch_simulate(const dd_graph *g, const dd_sched *sch, const dd_variants *var,
-                           int64_t *finish, int64_t *start, int64_t *makespan, int vs_hint,
-                           hipStream_t s) {
+// the kernel instance for a launch shape: <lanes per slot, variants per
+// lane, positions per slot>; a round holds at most 512 positions (LDS record
+// ring); two variants per lane when V is even (16 B loads and stores stay
+// inside a row).  f(instance) is called with the instance as template
+// arguments.
+template <class F>
+auto with_shape(const dd_variants *var, int vs_hint, F &&f) {
     int vs = vs_hint;
     if (vs <= 0) {
         // enough workgroups to cover the 256 compute units, then widest rows
         vs = 1;
         while (vs < 16 && (int64_t)var->V / (vs * 2) >= 256) vs *= 2;
     }
-    // <lanes per slot, variants per lane, positions per slot>: a round holds
-    // at most 512 positions (LDS record ring); two variants per lane when V
-    // is even (16 B loads and stores stay inside a row)
     const bool pair = (var->V % 2) == 0;
     switch (vs) {
-        case 1: return launch_pipe<1, 1, 1>(g, sch, var, finish, start, makespan, s);
-        case 2: return pair ? launch_pipe<1, 2, 1>(g, sch, var, finish, start, makespan, s)
-                            : launch_pipe<2, 1, 2>(g, sch, var, finish, start, makespan, s);
-        case 4: return pair ? launch_pipe<2, 2, 2>(g, sch, var, finish, start, makespan, s)
-                            : launch_pipe<4, 1, 4>(g, sch, var, finish, start, makespan, s);
-        case 8: return pair ? launch_pipe<4, 2, 4>(g, sch, var, finish, start, makespan, s)
-                            : launch_pipe<8, 1, 8>(g, sch, var, finish, start, makespan, s);
-        default: return pair ? launch_pipe<8, 2, 4>(g, sch, var, finish, start, makespan, s)
-                             : launch_pipe<16, 1, 8>(g, sch, var, finish, start, makespan, s);
+        case 1: return f(std::integral_constant<int, 1>{}, std::integral_constant<int, 1>{},
+                         std::integral_constant<int, 1>{});
+        case 2: return pair ? f(std::integral_constant<int, 1>{}, std::integral_constant<int, 2>{},
+                                std::integral_constant<int, 1>{})
+                            : f(std::integral_constant<int, 2>{}, std::integral_constant<int, 1>{},
+                                std::integral_constant<int, 2>{});
+        case 4: return pair ? f(std::integral_constant<int, 2>{}, std::integral_constant<int, 2>{},
+                                std::integral_constant<int, 2>{})
+                            : f(std::integral_constant<int, 4>{}, std::integral_constant<int, 1>{},
+                                std::integral_constant<int, 4>{});
+        case 8: return pair ? f(std::integral_constant<int, 4>{}, std::integral_constant<int, 2>{},
+                                std::integral_constant<int, 4>{})
+                            : f(std::integral_constant<int, 8>{}, std::integral_constant<int, 1>{},
+                                std::integral_constant<int, 8>{});
+        default: return pair ? f(std::integral_constant<int, 8>{}, std::integral_constant<int, 2>{},
+                                 std::integral_constant<int, 4>{})
+                             : f(std::integral_constant<int, 16>{}, std::integral_constant<int, 1>{},
+                                 std::integral_constant<int, 8>{});
     }
+}
+
+// Scratch of the allocation-free entry point: one array per GPU, held until
+// the process ends.  Host code takes its device address once per device
+// (hipGetSymbolAddress) and uses only that address.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+unsigned char *g_scratch_ptr[kMaxDevices];
+
+}  // namespace
+
+hipError_t launch_simulate(const dd_graph *g, const dd_sched *sch, const dd_variants *var,
+                           int64_t *finish, int64_t *start, int64_t *makespan, int vs_hint,
+                           hipStream_t s) {
+    return with_shape(var, vs_hint, [&](auto lps, auto vpl, auto k) {
+        return launch_pipe<decltype(lps)::value, decltype(vpl)::value, decltype(k)::value>(
+            g, sch, var, finish, start, makespan, s, nullptr);
+    });
+}
+
+hipError_t simulate_noalloc(const dd_graph *g, const dd_sched *sch, const dd_variants *var,
+                            int64_t *finish, int64_t *start, int64_t *makespan, hipStream_t s,
+                            size_t *need, size_t *limit) {
+    *limit = kScratchBytes;
+    *need = with_shape(var, 0, [&](auto lps, auto vpl, auto k) {
+        return sim_layout<decltype(lps)::value, decltype(vpl)::value, decltype(k)::value>(sch, var)
+            .bytes;
+    });
+    if (*need > kScratchBytes) return hipErrorInvalidValue;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    unsigned char *ptr = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(g_scratch_mu);
+        if (!g_scratch_ptr[dev]) {
+            void *p = nullptr;
+            e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+            if (e != hipSuccess) return e;
+            g_scratch_ptr[dev] = static_cast<unsigned char *>(p);
+        }
+        ptr = g_scratch_ptr[dev];
+    }
+    return with_shape(var, 0, [&](auto lps, auto vpl, auto k) {
+        return launch_pipe<decltype(lps)::value, decltype(vpl)::value, decltype(k)::value>(
+            g, sch, var, finish, start, makespan, s, ptr);
+    });
 }
 
 }  // namespace dd

@@ -36,6 +36,12 @@ hipError_t launch_build_scale_table(const dd_ratio *, int32_t, int32_t, ScaleEnt
                                     hipStream_t) { STUB; }
 hipError_t launch_simulate(const dd_graph *, const dd_sched *, const dd_variants *, int64_t *,
                            int64_t *, int64_t *, int, hipStream_t) { STUB; }
+hipError_t simulate_noalloc(const dd_graph *, const dd_sched *, const dd_variants *, int64_t *,
+                            int64_t *, int64_t *, hipStream_t, size_t *need, size_t *limit) {
+    *need = 0;
+    *limit = 0;
+    STUB;
+}
 hipError_t launch_breakdown(const dd_graph *, const dd_variants *, const uint8_t *, const int64_t *,
                             const int64_t *, int64_t *, int32_t *, int64_t *, hipStream_t) { STUB; }
 }  // namespace dd
@@ -91,6 +97,7 @@ int main() {
     EXPECT(dd_simulate_batch_vs(nullptr, nullptr, nullptr, dummy, nullptr, dummy, 32, nullptr) == DD_EINVAL, "width 32 rejected");
     EXPECT(dd_simulate_batch_vs(nullptr, nullptr, nullptr, dummy, nullptr, dummy, 16, nullptr) == DD_EINVAL, "width 16 NULL handles");
     EXPECT(dd_runtime_breakdown(nullptr, nullptr, nullptr, dummy, dummy, dummy, nullptr) == DD_EINVAL, "breakdown NULL handles");
+    EXPECT(dd_simulate_batch_noalloc(nullptr, nullptr, nullptr, dummy, nullptr, dummy, nullptr) == DD_EINVAL, "no-alloc NULL handles");
     EXPECT(strstr(dd_last_error(), "NULL handle") != nullptr, "NULL handle message");
     EXPECT(dd_sched_task_steps(nullptr, nullptr, nullptr) == DD_EINVAL, "steps NULL");
     int64_t a, b, c, d;

@@ -29,6 +29,8 @@ import numpy as np
 # task kinds (metadata only; the simulation sees threads, edges, classes)
 K_LAUNCH, K_SYNC, K_GEMM, K_ELEM, K_AUX, K_WU, K_MEMCPY, K_COMM, K_CONV, \
     K_GPU_OTHER, K_OPT, K_EMB = range(12)
+# operator tags of CNN kernels (the layer types the batchnorm recipe selects)
+OP_NONE, OP_CONV, OP_BN, OP_RELU, OP_OTHER = range(5)
 N_KINDS = 12
 GPU_KINDS = (K_GEMM, K_ELEM, K_AUX, K_WU, K_CONV, K_GPU_OTHER, K_OPT, K_EMB)
 CPU_KINDS = (K_LAUNCH, K_SYNC)
@@ -61,6 +63,8 @@ class TaskGraph:
     layer: np.ndarray
     launch_of: np.ndarray          # for device tasks: the CPU call that issued it, else -1
     name: str = ""
+    op: Optional[np.ndarray] = None         # operator tag of GPU kernels (OP_*), 0 = none
+    iteration: Optional[np.ndarray] = None  # training iteration of each task
 
     @property
     def n_edges(self) -> int:
@@ -138,17 +142,19 @@ class _Builder:
         self.layer: List[int] = []
         self.launch_of: List[int] = []
         self.cls_override: List[int] = []
+        self.op: List[int] = []
         self.edges: List[Tuple[int, int, int]] = []
         self.last: dict = {}
 
     def task(self, thread: int, kind: int, layer: int, launch_of: int = -1,
-             cls_override: int = -1) -> int:
+             cls_override: int = -1, op: int = OP_NONE) -> int:
         i = len(self.thread)
         self.thread.append(thread)
         self.kind.append(kind)
         self.layer.append(layer)
         self.launch_of.append(launch_of)
         self.cls_override.append(cls_override)
+        self.op.append(op)
         self.last[thread] = i
         return i
 
@@ -156,11 +162,11 @@ class _Builder:
         self.edges.append((src, dst, ecls))
 
     def launch(self, cpu: int, stream: int, kind: int, layer: int,
-               cls_override: int = -1) -> Tuple[int, int]:
+               cls_override: int = -1, op: int = OP_NONE) -> Tuple[int, int]:
         """A CPU launch call followed by the device task it issues
         (correlation dependency, Sec. 4.2.2)."""
         l = self.task(cpu, K_LAUNCH, layer)
-        k = self.task(stream, kind, layer, launch_of=l, cls_override=cls_override)
+        k = self.task(stream, kind, layer, launch_of=l, cls_override=cls_override, op=op)
         self.edge(l, k)
         return l, k
 
@@ -180,6 +186,7 @@ class _Template:
     layer: np.ndarray
     launch_of: np.ndarray
     cls_override: np.ndarray
+    op: np.ndarray
     esrc: np.ndarray
     edst: np.ndarray
     ecls: np.ndarray
@@ -191,7 +198,7 @@ def _template(b: _Builder, n_layers: int) -> _Template:
     e = np.array(b.edges, dtype=np.int64).reshape(-1, 3)
     return _Template(np.array(b.thread, np.int32), np.array(b.kind, np.uint8),
                      np.array(b.layer, np.int32), np.array(b.launch_of, np.int64),
-                     np.array(b.cls_override, np.int32),
+                     np.array(b.cls_override, np.int32), np.array(b.op, np.uint8),
                      e[:, 0], e[:, 1], e[:, 2].astype(np.uint8), b.n_threads, n_layers)
 
 
@@ -258,7 +265,9 @@ def _tile(t: _Template, iters: int, rng, medians, memcpy_range, name: str,
     n_cls = int(L1 * N_KINDS + max(0, int(t.cls_override.max()) + 1))
     return TaskGraph(N, t.n_threads, in_ptr, esrc.astype(np.int32), ecls.astype(np.uint8),
                      prev, thread.astype(np.int32), dur, gap, node_cls.astype(np.uint16),
-                     n_cls, int(ecls.max()) + 1 if ecls.size else 1, kind, layer, lo, name)
+                     n_cls, int(ecls.max()) + 1 if ecls.size else 1, kind, layer, lo, name,
+                     op=np.tile(t.op, iters),
+                     iteration=np.repeat(np.arange(iters, dtype=np.int32), n1))
 
 
 # ---------------------------------------------------------------------------
@@ -273,15 +282,17 @@ def _cnn_iteration(n_layers=20) -> _Template:
     b = _Builder(3)
     _, mc = b.launch(CPU, MEMCPY_S, K_MEMCPY, -1)
     first = True
+    fwd_ops = (OP_CONV, OP_BN, OP_RELU)
+    bwd_ops = (OP_CONV, OP_CONV, OP_RELU, OP_BN, OP_OTHER, OP_OTHER)   # data and weight grads first
     for l in range(n_layers):
         for j in range(3):
-            _, k = b.launch(CPU, S0, K_CONV if j == 0 else K_GPU_OTHER, l)
+            _, k = b.launch(CPU, S0, K_CONV if j == 0 else K_GPU_OTHER, l, op=fwd_ops[j])
             if first:
                 b.edge(mc, k)   # input batch must arrive before the first kernel
                 first = False
     for l in reversed(range(n_layers)):
         for j in range(6):
-            b.launch(CPU, S0, K_CONV if j < 2 else K_GPU_OTHER, l)
+            b.launch(CPU, S0, K_CONV if bwd_ops[j] == OP_CONV else K_GPU_OTHER, l, op=bwd_ops[j])
     for l in range(n_layers):
         b.launch(CPU, S0, K_OPT, l)
     b.sync(CPU, [S0, MEMCPY_S], -1)
@@ -434,7 +445,7 @@ def config(k: int, seed: Optional[int] = None, variants: Optional[int] = None,
         t = _cnn_iteration()
         g = _tile(t, iters or 4, rng, _KERNEL_MEDIAN_NS, (500_000, 2_000_000), "cnn")
         V = variants or 8
-        vs = _cnn_variants(rng, g, t.n_layers, V)
+        g, vs = _cnn_recipes(rng, g, t.n_layers, V)
     elif k in (2, 5):
         t, _ = _transformer_iteration()
         it = iters or (1 if k == 2 else 32)
@@ -442,7 +453,7 @@ def config(k: int, seed: Optional[int] = None, variants: Optional[int] = None,
                   "transformer" if k == 2 else "transformer-x%d" % it)
         V = variants or (256 if k == 2 else 2048)
         if k == 2:
-            vs = _transformer_variants(rng, g, t.n_layers, V, qs=(1, 2, 3, 4, 8))
+            g, vs = _transformer_recipes(rng, g, t.n_layers, V)
         else:
             vs = _transformer_variants(rng, g, t.n_layers, V, qs=(1, 2, 4, 8))
     elif k == 3:
@@ -455,43 +466,108 @@ def config(k: int, seed: Optional[int] = None, variants: Optional[int] = None,
                   "transformer+allreduce", comm_ns=comm_ns)
         V = variants or 1024
         # order edges between all-reduce channels live in classes 1..4
-        g, vs = _comm_variants(rng, g, t, [ar for ar, _ in comm], V)
+        g, vs = _comm_recipes(rng, g, t, [ar for ar, _ in comm], V)
     elif k == 4:
         t = _seq2seq_iteration()
         g = _tile(t, iters or 9, rng, {K_GEMM: 15_000, K_ELEM: 15_000, K_OPT: 15_000},
                   (100_000, 400_000), "seq2seq")
         V = variants or 64
-        vs = _seq2seq_variants(rng, g, t.n_layers, V)
+        g, vs = _seq2seq_recipes(rng, g, t.n_layers, V)
     else:
         raise ValueError("config must be 1..5")
     return g, vs
 
 
-def _cnn_variants(rng, g: TaskGraph, L: int, V: int) -> VariantSet:
-    C = g.n_node_cls
-    s = _identity_scale(C, V)
-    gpu_cls = [_cls_of(l, kd, L) for l in list(range(L)) + [-1] for kd in GPU_KINDS + (K_MEMCPY,)]
-    conv_cls = [_cls_of(l, K_CONV, L) for l in range(L)]
-    launch_cls = [_cls_of(l, K_LAUNCH, L) for l in list(range(L)) + [-1]]
+# ---------------------------------------------------------------------------
+# variant sweeps written as what-if recipes (recipes.py)
+def _cnn_recipes(rng, g: TaskGraph, L: int, V: int):
+    """CNN sweep: baseline, AMP, restructured batchnorm, both, free launch
+    calls, a 2x faster GPU, and layer substitutions (scale or remove)."""
+    from . import recipes as R
+    sweep = []
     for v in range(V):
         kind = v % 8
-        if kind == 1:
-            for c in gpu_cls:
-                s[c, v] = (2, 1)
+        if kind == 0:
+            r = []
+        elif kind == 1:
+            r = [R.AMP()]
         elif kind == 2:
-            for c in conv_cls:
-                s[c, v] = (1, 2)
+            r = [R.RestructureBatchnorm()]
         elif kind == 3:
-            for c in launch_cls:
-                s[c, v] = (0, 1)
-        elif kind >= 4:
-            for l in range(L):
-                if rng.random() < 0.5:
-                    for kd in (K_CONV, K_GPU_OTHER, K_OPT):
-                        s[_cls_of(l, kd, L), v] = _random_pq(rng, (2, 4, 8), 2, 1)
-    rb = np.zeros((g.n, (V + 31) // 32), np.uint32)
-    eo = np.ones((V, 1), np.uint64)
-    return VariantSet(V, s, rb, eo, [(0, V, 1)])
+            r = [R.AMP(), R.RestructureBatchnorm()]
+        elif kind == 4:
+            r = [R.ScaleLaunch(0, 1)]
+        elif kind == 5:
+            r = [R.ScaleKernels(1, 2)]
+        elif kind == 6:
+            layers = [l for l in range(L) if rng.random() < 0.5]
+            p, q = _random_pq(rng, (2, 4, 8), 2, 1)
+            r = [R.ScaleLayers(layers, p, q)]
+        else:
+            layers = [int(x) for x in rng.choice(L, size=2, replace=False)]
+            r = [R.RemoveLayers(layers), R.AMP()]
+        sweep.append(r)
+    return R.compile_sweep(g, sweep)
+
+
+def _transformer_recipes(rng, g: TaskGraph, L: int, V: int):
+    """Transformer sweep: random combinations of element-wise kernel fusion,
+    a fused optimizer, AMP and layer scaling (variant 0 is the baseline)."""
+    from . import recipes as R
+    sweep = [[]]
+    for v in range(1, V):
+        r = []
+        fused_adam = rng.random() < 0.5
+        if rng.random() < 0.7:
+            kinds = (K_ELEM, K_AUX) if fused_adam else (K_ELEM, K_AUX, K_WU)
+            r.append(R.FuseElementwise(float(rng.uniform(0.1, 0.5)), int(rng.integers(1 << 30)),
+                                       kinds))
+        if fused_adam:
+            r.append(R.FusedAdam())
+        if rng.random() < 0.5:
+            r.append(R.AMP())
+        if rng.random() < 0.5:
+            layers = [l for l in range(L) if rng.random() < 0.5]
+            p, q = _random_pq(rng, (1, 2, 3, 4, 8), 2, 0)
+            r.append(R.ScaleLayers(layers, p, q))
+        sweep.append(r)
+    return R.compile_sweep(g, sweep)
+
+
+def _comm_recipes(rng, g: TaskGraph, t: _Template, ars: List[int], V: int):
+    """Data-parallel sweep: four orders of the all-reduce channel (edge
+    classes 1..4) x link bandwidth 10, 25, 100 GB/s x gradient compression
+    of random buckets, some with AMP."""
+    from . import recipes as R
+    g = _with_channel_orders(rng, g, t, ars)
+    B = len(ars)
+    per = V // 4
+    sweep = []
+    for gi in range(4):
+        n_g = V - 3 * per if gi == 3 else per
+        for j in range(n_g):
+            r = [R.EdgeClasses(on=1 << (1 + gi)), R.Distributed([10, 25, 100][j % 3])]
+            if j >= 3:
+                r.append(R.CompressGradients(1, 4, [b for b in range(B) if rng.random() < 0.5]))
+            if j >= 6 and rng.random() < 0.5:
+                r.append(R.AMP())
+            sweep.append(r)
+    return R.compile_sweep(g, sweep, base_edge_mask=1)
+
+
+def _seq2seq_recipes(rng, g: TaskGraph, L: int, V: int):
+    """Seq2seq sweep: CPU launch cost x {1, 0, 1/4, 1/2, 2} with element-wise
+    fusion of U[0.1, 0.5] of the kernels (variant 0 is the baseline)."""
+    from . import recipes as R
+    lscales = [(1, 1), (0, 1), (1, 4), (1, 2), (2, 1)]
+    sweep = []
+    for v in range(V):
+        r = [R.ScaleLaunch(*lscales[v % 5])]
+        if v:
+            r.append(R.FuseElementwise(float(rng.uniform(0.1, 0.5)), int(rng.integers(1 << 30)),
+                                       (K_ELEM,)))
+        sweep.append(r)
+    return R.compile_sweep(g, sweep)
 
 
 def _removable(g: TaskGraph, kinds) -> Tuple[np.ndarray, np.ndarray]:
@@ -500,6 +576,11 @@ def _removable(g: TaskGraph, kinds) -> Tuple[np.ndarray, np.ndarray]:
 
 
 def _transformer_variants(rng, g: TaskGraph, L: int, V: int, qs) -> VariantSet:
+    """Stress sweep of the large transformer workload: every (layer, kind)
+    class draws its own ratio p/q (q in `qs`, p in [0, 2q]) with probability
+    1/2 per variant, and each variant removes element-wise, auxiliary and
+    weight-update kernels (with their launch calls) at a density drawn from
+    U[0.1, 0.5].  Variant 0 is the baseline."""
     C = g.n_node_cls
     s = _identity_scale(C, V)
     kinds = (K_GEMM, K_ELEM, K_AUX, K_WU, K_LAUNCH)
@@ -516,10 +597,9 @@ def _transformer_variants(rng, g: TaskGraph, L: int, V: int, qs) -> VariantSet:
     return VariantSet(V, s, rb, eo, [(0, V, 1)])
 
 
-def _comm_variants(rng, g: TaskGraph, t: _Template, ars: List[int], V: int):
-    """Four channel-order groups (ready order, reverse, front-layers-first,
-    seeded permutation) x bandwidth {10, 25, 100} GB/s x per-bucket 1/4
-    compression.  Order edges are added to the graph with classes 1..4."""
+def _with_channel_orders(rng, g: TaskGraph, t: _Template, ars: List[int]) -> TaskGraph:
+    """The all-reduce channel's four orders (ready order, reverse, interleaved
+    priority, seeded permutation) as order edges of classes 1..4."""
     n1 = t.thread.shape[0]
     iters = g.n // n1
     B = len(ars)
@@ -544,52 +624,8 @@ def _comm_variants(rng, g: TaskGraph, t: _Template, ars: List[int], V: int):
     in_ptr = np.zeros(g.n + 1, np.int64)
     np.add.at(in_ptr, dst + 1, 1)
     in_ptr = np.cumsum(in_ptr)
-    g = dataclasses.replace(g, in_ptr=in_ptr, in_src=src.astype(np.int32),
-                            edge_cls=cls.astype(np.uint8), n_edge_cls=5)
-    C = g.n_node_cls
-    L = t.n_layers
-    s = _identity_scale(C, V)
-    ar_cls0 = (L + 1) * N_KINDS
-    per = V // 4
-    eo = np.zeros((V, 1), np.uint64)
-    batches = []
-    for gi in range(4):
-        v0 = gi * per
-        v1 = V if gi == 3 else (gi + 1) * per
-        batches.append((v0, v1, 1 | (1 << (1 + gi))))
-        for v in range(v0, v1):
-            eo[v, 0] = np.uint64(1 | (1 << (1 + gi)))
-            j = v - v0
-            bw = j % 3
-            bwp, bwq = [(1, 1), (2, 5), (1, 10)][bw]
-            comp = rng.random(B) < 0.5 if j >= 3 else np.zeros(B, bool)
-            for b_ in range(B):
-                p, q = bwp, bwq * (4 if comp[b_] else 1)
-                gg = np.gcd(p, q)
-                s[ar_cls0 + b_, v] = (p // gg, q // gg)
-            if j >= 6 and rng.random() < 0.5:     # AMP-like GPU scaling on some variants
-                for l in range(L):
-                    s[_cls_of(l, K_GEMM, L), v] = (1, 3)
-                    s[_cls_of(l, K_ELEM, L), v] = (1, 2)
-    rb = np.zeros((g.n, (V + 31) // 32), np.uint32)
-    return g, VariantSet(V, s, rb, eo, batches)
-
-
-def _seq2seq_variants(rng, g: TaskGraph, L: int, V: int) -> VariantSet:
-    C = g.n_node_cls
-    s = _identity_scale(C, V)
-    lscales = [(1, 1), (0, 1), (1, 4), (1, 2), (2, 1)]
-    launch_cls = [_cls_of(l, K_LAUNCH, L) for l in list(range(L)) + [-1]]
-    for v in range(V):
-        p, q = lscales[v % 5]
-        for c in launch_cls:
-            s[c, v] = (p, q)
-    dens = rng.uniform(0.1, 0.5, size=V)
-    dens[0] = 0.0
-    kern, lau = _removable(g, (K_ELEM,))
-    rb = _removal_bits(rng, g.n, V, kern, lau, dens)
-    eo = np.ones((V, 1), np.uint64)
-    return VariantSet(V, s, rb, eo, [(0, V, 1)])
+    return dataclasses.replace(g, in_ptr=in_ptr, in_src=src.astype(np.int32),
+                               edge_cls=cls.astype(np.uint8), n_edge_cls=5)
 
 
 def task_roles(g: TaskGraph) -> np.ndarray:

@@ -49,15 +49,18 @@ def test_chains_and_edges(k):
     assert (g.gap[~np.isin(g.kind, W.CPU_KINDS)] == 0).all()
 
 
-@pytest.mark.parametrize("k", [2, 4])
-def test_removal_pairs(k):
+@pytest.mark.parametrize("k,hi", [(2, 0.75), (4, 0.5)])
+def test_removal_pairs(k, hi):
+    """Config 2's upper bound is higher: a fused optimizer removes all but
+    one of the 13,296 weight-update kernels (with their launch calls) of
+    the 32,768-task iteration in about half of the variants."""
     g, vs = W.config(k)
     bits = W.unpack_bits(vs.remove_bits, vs.n_variants)
     k_ids = np.nonzero(g.launch_of >= 0)[0]
     assert (bits[k_ids] == bits[g.launch_of[k_ids]]).all()   # kernel removed with its launch
     assert not bits[:, 0].any()                               # variant 0 is the identity
     dens = bits[:, 1:].mean()
-    assert 0.05 < dens < 0.5
+    assert 0.05 < dens < hi
 
 
 def test_comm_batches():

@@ -17,6 +17,10 @@
  * the order of consecutive tasks on one execution thread (also a dependency
  * type of Sec. 4.2.2).
  *
+ * A third entry point runs the same loop with an overridden schedule()
+ * (Sec. 4.4, "Schedule"; the appendix's P3 priority rule) on graphs whose
+ * threads may hold tasks with no order among them.
+ *
  * Removal has two readings, both implemented so tests can check that they
  * agree: mode 0 keeps a removed task with duration and gap 0 (a
  * pass-through); mode 1 unlinks it (Sec. 4.4, Insert/Remove: the task is
@@ -376,6 +380,109 @@ static int run_variant(const ddo_graph *g, const ddo_struct *st, const ddo_varia
 }
 
 /* ------------------------------------------------------------------ */
+/* The simulation under an overridden schedule() (Sec. 4.4, "Schedule"; the
+ * appendix's P3 model).  Same transformations and the same loop as above
+ * (removed tasks kept with zero duration and gap), but threads may hold
+ * tasks with no order among them (several chains on one thread, e.g. the
+ * push and pull slices on a communication channel), so which ready task runs
+ * next decides the result.  The frontier Q is kept in trace order (ascending
+ * task id); Q.first() is its lowest id.  schedule(Q) scans Q in that order
+ * with time(x) = max(P[x.thread], x.start):
+ *   policy 0 (the default rule): the first task of least time;
+ *   policy 1 (P3's priority rule): the same scan, where a later task of equal
+ *            time also replaces the current choice when both are push/pull
+ *            tasks (pp[] != 0) and its priority is strictly higher.
+ * A task is dispatched at max(P[t], start); its thread's progress becomes its
+ * start + duration + gap, and so does every child's start if larger. */
+static int run_variant_policy(const ddo_graph *g, const ddo_struct *st, const ddo_variants *vs,
+                              int32_t v, int policy, const uint8_t *pp, const int32_t *prio,
+                              work *w, int64_t *start_row, int64_t *finish_row,
+                              int64_t *makespan) {
+    const int32_t n = g->n;
+    const int32_t V = vs->n_variants;
+    int32_t *Q = (int32_t *)w->heapbuf;
+    int32_t qn = 0;
+    for (int32_t u = 0; u < n; u++) {
+        int r = is_removed(vs, u, v);
+        w->rm[u] = (uint8_t)r;
+        int32_t p = 1, q = 1;
+        if (vs->scale) {
+            int64_t o = ((int64_t)g->node_cls[u] * V + v) * 2;
+            p = vs->scale[o];
+            q = vs->scale[o + 1];
+        }
+        w->dd[u] = r ? 0 : scaled(g->dur[u], p, q);
+        w->gg[u] = r ? 0 : g->gap[u];
+    }
+    for (int32_t t = 0; t < g->n_threads; t++) w->P[t] = 0;
+    for (int32_t u = 0; u < n; u++) {
+        int32_t r = (g->thread_prev[u] >= 0) ? 1 : 0;
+        for (int64_t e = g->in_ptr[u]; e < g->in_ptr[u + 1]; e++) {
+            int c = g->edge_cls ? g->edge_cls[e] : 0;
+            if (edge_active(vs, v, c)) r++;
+        }
+        w->ref[u] = r;
+        w->est[u] = 0;
+        if (r == 0) Q[qn++] = u;                       /* ids ascending */
+    }
+    int32_t dispatched = 0;
+    while (qn > 0) {
+        /* u <- schedule(Q) */
+        int32_t bi = 0;
+        int32_t best = Q[0];
+        int64_t time = w->P[g->thread_id[best]] > w->est[best] ? w->P[g->thread_id[best]]
+                                                             : w->est[best];
+        for (int32_t i = 0; i < qn; i++) {
+            int32_t x = Q[i];
+            int64_t px = w->P[g->thread_id[x]];
+            int64_t tx = px > w->est[x] ? px : w->est[x];
+            if (tx < time) { time = tx; best = x; bi = i; }
+            if (policy == 1 && tx == time && pp[x] && pp[best] && prio[x] > prio[best]) {
+                best = x;
+                bi = i;
+            }
+        }
+        memmove(&Q[bi], &Q[bi + 1], (size_t)(qn - bi - 1) * sizeof(int32_t));
+        qn--;
+        int32_t u = best;
+        int32_t t = g->thread_id[u];
+        int64_t s = w->P[t] > w->est[u] ? w->P[t] : w->est[u];
+        w->S[u] = s;
+        int64_t rel = s + w->dd[u] + w->gg[u];
+        w->P[t] = rel;
+        dispatched++;
+        /* children: dependency out-edges, then the next task on the thread */
+        for (int64_t e = st->out_ptr[u]; e <= st->out_ptr[u + 1]; e++) {
+            int32_t c;
+            if (e < st->out_ptr[u + 1]) {
+                if (!edge_active(vs, v, st->out_cls[e])) continue;
+                c = st->out_dst[e];
+            } else {
+                c = st->thread_next[u];
+                if (c < 0) break;
+            }
+            if (rel > w->est[c]) w->est[c] = rel;
+            if (--w->ref[c] == 0) {                    /* insert, keeping Q in id order */
+                int32_t i = qn;
+                while (i > 0 && Q[i - 1] > c) { Q[i] = Q[i - 1]; i--; }
+                Q[i] = c;
+                qn++;
+            }
+        }
+    }
+    if (dispatched != n) return DDO_ECYCLE;
+    int64_t ms = 0;
+    for (int32_t u = 0; u < n; u++) {
+        int64_t f = w->S[u] + w->dd[u];
+        if (start_row) start_row[u] = w->S[u];
+        if (finish_row) finish_row[u] = f;
+        if (!w->rm[u] && f > ms) ms = f;
+    }
+    *makespan = ms;
+    return DDO_OK;
+}
+
+/* ------------------------------------------------------------------ */
 /* Runtime breakdown of the evaluation of AMP (Sec. 6.2, Fig. 6), from one
  * variant's simulated schedule, by the paper's own rules for computing it:
  *   total    = the iteration time (makespan);
@@ -410,6 +517,7 @@ typedef struct {
     const int32_t *vlist; int32_t n_list; int mode, tie;
     int64_t *start, *finish, *makespan, *bindings;
     const uint8_t *role; int64_t *bd;        /* breakdown: role [n] in, [n_list][4] out */
+    int policy; const uint8_t *pp; const int32_t *prio;   /* policy >= 0: run_variant_policy */
     int32_t next; pthread_mutex_t mu; int rc;
 } job;
 
@@ -431,10 +539,15 @@ static void *worker(void *arg) {
         pthread_mutex_unlock(&j->mu);
         if (i >= j->n_list || !ok) break;
         int32_t v = j->vlist[i];
-        int rc = run_variant(j->g, j->st, j->vs, v, j->mode, j->tie, &w,
-                             j->start ? j->start + (int64_t)i * n : NULL,
-                             j->finish ? j->finish + (int64_t)i * n : NULL,
-                             &j->makespan[i], j->bindings ? &j->bindings[i] : NULL);
+        int rc = j->policy >= 0
+            ? run_variant_policy(j->g, j->st, j->vs, v, j->policy, j->pp, j->prio, &w,
+                                 j->start ? j->start + (int64_t)i * n : NULL,
+                                 j->finish ? j->finish + (int64_t)i * n : NULL,
+                                 &j->makespan[i])
+            : run_variant(j->g, j->st, j->vs, v, j->mode, j->tie, &w,
+                          j->start ? j->start + (int64_t)i * n : NULL,
+                          j->finish ? j->finish + (int64_t)i * n : NULL,
+                          &j->makespan[i], j->bindings ? &j->bindings[i] : NULL);
         if (rc) {
             pthread_mutex_lock(&j->mu);
             if (j->rc == 0) j->rc = rc;
@@ -470,14 +583,26 @@ static int check(const ddo_graph *g, const ddo_variants *vs) {
 static int run_job(const ddo_graph *g, const ddo_variants *vs,
                    const int32_t *vlist, int32_t n_list, int32_t mode, int32_t tie,
                    int64_t *start, int64_t *finish, int64_t *makespan, int64_t *bindings,
-                   const uint8_t *role, int64_t *bd, int32_t n_workers);
+                   const uint8_t *role, int64_t *bd, int32_t n_workers,
+                   int policy, const uint8_t *pp, const int32_t *prio);
 
 int ddo_run(const ddo_graph *g, const ddo_variants *vs,
             const int32_t *vlist, int32_t n_list, int32_t mode, int32_t tie,
             int64_t *start, int64_t *finish, int64_t *makespan, int64_t *bindings,
             int32_t n_workers) {
     return run_job(g, vs, vlist, n_list, mode, tie, start, finish, makespan, bindings, NULL, NULL,
-                   n_workers);
+                   n_workers, -1, NULL, NULL);
+}
+
+/* The simulation of each listed variant under schedule policy 0 or 1 (see
+ * run_variant_policy); pp and prio [n] are read by policy 1 only. */
+int ddo_run_policy(const ddo_graph *g, const ddo_variants *vs, const int32_t *vlist,
+                   int32_t n_list, int32_t policy, const uint8_t *pp, const int32_t *prio,
+                   int64_t *start, int64_t *finish, int64_t *makespan, int32_t n_workers) {
+    if (policy != 0 && policy != 1) return DDO_EINVAL;
+    if (policy == 1 && (!pp || !prio)) return DDO_EINVAL;
+    return run_job(g, vs, vlist, n_list, 0, 0, start, finish, makespan, NULL, NULL, NULL,
+                   n_workers, policy, pp, prio);
 }
 
 /* The runtime breakdown (see breakdown()) of each listed variant after the
@@ -487,13 +612,15 @@ int ddo_breakdown(const ddo_graph *g, const ddo_variants *vs, const uint8_t *rol
                   const int32_t *vlist, int32_t n_list, int64_t *makespan, int64_t *out,
                   int32_t n_workers) {
     if (!role) return DDO_EINVAL;
-    return run_job(g, vs, vlist, n_list, 0, 0, NULL, NULL, makespan, NULL, role, out, n_workers);
+    return run_job(g, vs, vlist, n_list, 0, 0, NULL, NULL, makespan, NULL, role, out, n_workers,
+                   -1, NULL, NULL);
 }
 
 static int run_job(const ddo_graph *g, const ddo_variants *vs,
                    const int32_t *vlist, int32_t n_list, int32_t mode, int32_t tie,
                    int64_t *start, int64_t *finish, int64_t *makespan, int64_t *bindings,
-                   const uint8_t *role, int64_t *bd, int32_t n_workers) {
+                   const uint8_t *role, int64_t *bd, int32_t n_workers,
+                   int policy, const uint8_t *pp, const int32_t *prio) {
     int rc = check(g, vs);
     if (rc) return rc;
     for (int32_t i = 0; i < n_list; i++)
@@ -507,6 +634,7 @@ static int run_job(const ddo_graph *g, const ddo_variants *vs,
     j.g = g; j.st = &st; j.vs = vs; j.vlist = vlist; j.n_list = n_list;
     j.mode = mode; j.tie = tie; j.start = start; j.finish = finish;
     j.makespan = makespan; j.bindings = bindings; j.role = role; j.bd = bd;
+    j.policy = policy; j.pp = pp; j.prio = prio;
     pthread_mutex_init(&j.mu, NULL);
     if (n_workers < 1) n_workers = 1;
     if (n_workers > n_list) n_workers = n_list > 0 ? n_list : 1;

@@ -65,6 +65,11 @@ def _load():
         _lib.ddo_breakdown.argtypes = [ctypes.POINTER(_Graph), ctypes.POINTER(_Variants),
                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32]
+        _lib.ddo_run_policy.restype = ctypes.c_int
+        _lib.ddo_run_policy.argtypes = [ctypes.POINTER(_Graph), ctypes.POINTER(_Variants),
+                                        ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32]
         _lib.ddo_steps.restype = ctypes.c_int
         _lib.ddo_steps.argtypes = [ctypes.POINTER(_Graph), ctypes.c_uint64, ctypes.c_void_p,
                                    ctypes.c_void_p]
@@ -179,3 +184,39 @@ def breakdown(g, vs, role, variants: Optional[Sequence[int]] = None,
     if rc != OK:
         raise OracleError(rc)
     return out
+
+
+POLICY_EARLIEST, POLICY_PRIORITY = 0, 1
+
+
+def run_policy(g, vs, policy: int, pp=None, prio=None, variants: Optional[Sequence[int]] = None,
+               want_start: bool = True, want_finish: bool = True,
+               workers: Optional[int] = None):
+    """Simulate the listed variants with an overridden schedule() (Sec. 4.4,
+    "Schedule"); threads may hold several chains.  policy 0: earliest time
+    max(P[t], start), first in trace order among equals; policy 1: P3's
+    priority rule over push/pull tasks (pp[u] != 0) with priority prio[u].
+    Returns (start, finish, makespan) like run()."""
+    lib = _load()
+    gs, keep = _graph_struct(g)
+    scale = np.ascontiguousarray(vs.scale, np.int32)
+    rb = np.ascontiguousarray(vs.remove_bits, np.uint32)
+    eo = np.ascontiguousarray(vs.edge_on, np.uint64)
+    vv = _Variants(int(vs.n_variants), int(scale.shape[0]), _p(scale), _p(rb),
+                   int(eo.shape[1]), _p(eo))
+    if variants is None:
+        variants = range(vs.n_variants)
+    vl = np.ascontiguousarray(np.array(list(variants), np.int32))
+    L = vl.shape[0]
+    ppa = None if pp is None else np.ascontiguousarray(pp, np.uint8)
+    pra = None if prio is None else np.ascontiguousarray(prio, np.int32)
+    start = np.zeros((L, g.n), np.int64) if want_start else None
+    finish = np.zeros((L, g.n), np.int64) if want_finish else None
+    ms = np.zeros(L, np.int64)
+    if workers is None:
+        workers = max(1, min(len(os.sched_getaffinity(0)), 16))
+    rc = lib.ddo_run_policy(ctypes.byref(gs), ctypes.byref(vv), _p(vl), L, int(policy),
+                            _p(ppa), _p(pra), _p(start), _p(finish), _p(ms), int(workers))
+    if rc != OK:
+        raise OracleError(rc)
+    return start, finish, ms

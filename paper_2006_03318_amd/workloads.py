@@ -710,6 +710,62 @@ def random_graph_sparse(rng, n: int, n_threads: int, mean_in: float = 0.3,
                      np.full(n, -1, np.int64), "random-sparse")
 
 
+def random_shared_graph(rng, n: int, n_ordered: int, n_shared: int, mean_in: float = 1.5,
+                        window: int = 32, max_dur: int = 1000, zero_frac: float = 0.2,
+                        n_edge_cls: int = 1, chain_frac: float = 0.3, n_node_cls: int = 3,
+                        prio_range: int = 4):
+    """A random DAG whose last `n_shared` threads hold tasks with no order
+    among them (a schedule decides it), like the push/pull slices of a
+    communication channel.  Tasks on the first `n_ordered` threads form one
+    chain per thread (id order); a task on a shared thread starts a chain of
+    its own, or with probability `chain_frac` continues the tail of one of
+    that thread's chains.  Dependency edges: Poisson(mean_in) per task from
+    the previous `window` ids.  Returns (graph, pp, prio): pp = 1 on tasks of
+    shared threads (the push/pull tasks of the priority rule), prio drawn from
+    [-prio_range, prio_range] so that equal priorities occur."""
+    T = n_ordered + n_shared
+    thread = rng.integers(0, T, size=n).astype(np.int32)
+    prev = np.full(n, -1, np.int32)
+    last = np.full(T, -1, np.int64)
+    tails = [[] for _ in range(T)]
+    for i in range(n):
+        t = int(thread[i])
+        if t < n_ordered:
+            prev[i] = last[t]
+            last[t] = i
+        else:
+            if tails[t] and rng.random() < chain_frac:
+                k = int(rng.integers(0, len(tails[t])))
+                prev[i] = tails[t][k]
+                tails[t][k] = i
+            else:
+                tails[t].append(i)
+    k = rng.poisson(mean_in, size=n).astype(np.int64)
+    k[0] = 0
+    dst = np.repeat(np.arange(n, dtype=np.int64), k)
+    lo = np.maximum(dst - window, 0)
+    src = lo + (rng.random(dst.shape[0]) * (dst - lo)).astype(np.int64)
+    ok = src < dst
+    src, dst = src[ok], dst[ok]
+    o = np.argsort(dst, kind="stable")
+    src, dst = src[o], dst[o]
+    in_ptr = np.zeros(n + 1, np.int64)
+    np.add.at(in_ptr, dst + 1, 1)
+    in_ptr = np.cumsum(in_ptr)
+    dur = rng.integers(1, max_dur + 1, size=n).astype(np.int64)
+    dur[rng.random(n) < zero_frac] = 0
+    gap = rng.integers(0, max_dur // 4 + 1, size=n).astype(np.int64)
+    gap[rng.random(n) < 0.5] = 0
+    cls = rng.integers(0, n_edge_cls, size=src.shape[0]).astype(np.uint8)
+    g = TaskGraph(n, T, in_ptr, src.astype(np.int32), cls, prev, thread, dur, gap,
+                  rng.integers(0, n_node_cls, size=n).astype(np.uint16), n_node_cls,
+                  n_edge_cls, np.zeros(n, np.uint8), np.full(n, -1, np.int32),
+                  np.full(n, -1, np.int64), "random-shared")
+    pp = (thread >= n_ordered).astype(np.uint8)
+    prio = rng.integers(-prio_range, prio_range + 1, size=n).astype(np.int32)
+    return g, pp, prio
+
+
 def random_variants(rng, g: TaskGraph, V: int, p_remove: float = 0.2,
                     qs=(1, 2, 3, 4, 5, 7, 8, 10)) -> VariantSet:
     C = g.n_node_cls

@@ -55,7 +55,19 @@ BREAKDOWN_MUTANTS = {
                                 "if (role[u] == 1) gpu += g->dur[u];"),
     "bd_parallel_sign": ("out[3] = ms - out[1] - out[2];", "out[3] = ms - out[1] + out[2];"),
 }
-MUTANTS_ALL = dict(MUTANTS, **BREAKDOWN_MUTANTS)
+POLICY_MUTANTS = {
+    "policy_priority_ignored": ("if (policy == 1 && tx == time && pp[x] && pp[best] && prio[x] > prio[best]) {",
+                                "if (0) {"),
+    "policy_priority_reversed": ("if (policy == 1 && tx == time && pp[x] && pp[best] && prio[x] > prio[best]) {",
+                                 "if (policy == 1 && tx == time && pp[x] && pp[best] && prio[x] < prio[best]) {"),
+    "policy_time_without_progress": ("int64_t tx = px > w->est[x] ? px : w->est[x];",
+                                     "int64_t tx = w->est[x]; (void)px;"),
+    "policy_last_of_equals": ("if (tx < time) { time = tx; best = x; bi = i; }",
+                              "if (tx <= time) { time = tx; best = x; bi = i; }"),
+    "policy_child_release_without_gap": ("int64_t rel = s + w->dd[u] + w->gg[u];\n        w->P[t] = rel;\n        dispatched++;",
+                                         "int64_t rel = s + w->dd[u] + w->gg[u];\n        w->P[t] = rel;\n        rel -= w->gg[u];\n        dispatched++;"),
+}
+MUTANTS_ALL = dict(MUTANTS, **BREAKDOWN_MUTANTS, **POLICY_MUTANTS)
 
 
 class _Mut:
@@ -65,6 +77,8 @@ class _Mut:
         lib.ddo_run.argtypes = O._load().ddo_run.argtypes
         lib.ddo_breakdown.restype = ctypes.c_int
         lib.ddo_breakdown.argtypes = O._load().ddo_breakdown.argtypes
+        lib.ddo_run_policy.restype = ctypes.c_int
+        lib.ddo_run_policy.argtypes = O._load().ddo_run_policy.argtypes
         self.lib = lib
         self.OracleError = O.OracleError
         self.ECYCLE = O.ECYCLE
@@ -74,6 +88,14 @@ class _Mut:
         O._lib = self.lib
         try:
             return O.run(*a, **k)
+        finally:
+            O._lib = saved
+
+    def run_policy(self, *a, **k):
+        saved = O._lib
+        O._lib = self.lib
+        try:
+            return O.run_policy(*a, **k)
         finally:
             O._lib = saved
 
@@ -154,3 +176,35 @@ def test_planted_breakdown_mistake_is_caught(name):
     O.build(force=False)
     m = _Mut(_build_mutant(name))
     assert _breakdown_pins_fail(m), "breakdown pins did not catch mutant " + name
+
+
+def _policy_pins_fail(m):
+    from tests import test_oracle_schedule as SC
+    try:
+        for policy in (0, 1):
+            g, pp, prio, exp = SC.load_p3_toy()
+            S, _, M = m.run_policy(g, P.H.variants(g, V=1), policy, pp, prio)
+            if S[0].tolist() != exp["start%d" % policy] or M[0] != exp["makespan%d" % policy][0]:
+                return True
+        for seed in range(25):
+            g, vs, pp, prio = SC._shared_case(seed)
+            for policy in (0, 1):
+                S, _, _ = m.run_policy(g, vs, policy, pp, prio)
+                for v in range(vs.n_variants):
+                    SC._check_valid_run(g, vs, v, S[v], pp, prio, policy)
+        for seed in range(10):
+            g, vs, pp, prio = SC._chain_case(seed)
+            S0, _, M0, _ = O.run(g, vs)
+            s1, _, m1 = m.run_policy(g, vs, 1, pp, prio)
+            if not (np.array_equal(S0, s1) and np.array_equal(M0, m1)):
+                return True
+    except AssertionError:
+        return True
+    return False
+
+
+@pytest.mark.parametrize("name", sorted(POLICY_MUTANTS))
+def test_planted_policy_mistake_is_caught(name):
+    O.build(force=False)
+    m = _Mut(_build_mutant(name))
+    assert _policy_pins_fail(m), "schedule pins did not catch mutant " + name

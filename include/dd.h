@@ -81,8 +81,9 @@ typedef enum {
     DD_ERANGE = 4,     /* scaled times could overflow int64 */
     DD_ENOMEM = 5,     /* device allocation failed */
     DD_EHIP = 6,       /* HIP runtime error */
-    DD_EMISMATCH = 7   /* handles from different graphs, or a variant uses an
+    DD_EMISMATCH = 7,  /* handles from different graphs, or a variant uses an
                           edge class the schedule was not built for */
+    DD_ELIMIT = 8      /* a fixed capacity of a device path was exceeded */
 } dd_status;
 
 typedef struct dd_graph dd_graph;
@@ -122,6 +123,27 @@ dd_status dd_graph_load(int32_t n, int32_t n_threads,
                         const int32_t *thread_prev, const int32_t *thread_id,
                         const int64_t *dur_ns, const int64_t *gap_ns, const uint16_t *node_cls,
                         void *stream, dd_graph **out);
+
+/*
+ * dd_graph_load_ex -- dd_graph_load with flags.
+ *   DD_LOAD_SHARED_THREADS  a thread may hold several chains: tasks with
+ *       thread_prev == -1 other than the first, and chains that share a
+ *       thread, have no recorded order among themselves (for example the
+ *       push and pull slices a what-if recipe inserts on a communication
+ *       channel, Sec. 5.1 P3).  Their order is decided while simulating, by
+ *       the schedule() rule of Sec. 4.4 ("Schedule"), so such a graph is
+ *       simulated only by dd_simulate_policy; dd_levelize and
+ *       dd_runtime_breakdown return DD_EINVAL for it.  Each task still has at
+ *       most one thread successor (DD_ECHAIN otherwise), and dependencies
+ *       between tasks of one thread are kept (no thread order implies them).
+ * flags == 0 is dd_graph_load.  Unknown flag bits: DD_EINVAL.
+ */
+#define DD_LOAD_SHARED_THREADS 1u
+dd_status dd_graph_load_ex(int32_t n, int32_t n_threads,
+                           const int64_t *in_ptr, const int32_t *in_src, const uint8_t *edge_cls,
+                           const int32_t *thread_prev, const int32_t *thread_id,
+                           const int64_t *dur_ns, const int64_t *gap_ns, const uint16_t *node_cls,
+                           uint32_t flags, void *stream, dd_graph **out);
 
 /*
  * dd_levelize -- topological schedule of the graph restricted to the edge
@@ -228,6 +250,40 @@ dd_status dd_simulate_batch_noalloc(const dd_graph *g, const dd_sched *sched, co
 dd_status dd_runtime_breakdown(const dd_graph *g, const dd_variants *var, const uint8_t *role,
                                const int64_t *d_finish, const int64_t *d_makespan,
                                int64_t *d_out, void *stream);
+
+/*
+ * dd_simulate_policy -- simulate every variant with an overridden schedule()
+ * (Sec. 4.4, "Schedule"): Algorithm 1 task by task, where schedule() picks
+ * the next task from the frontier Q of ready tasks, kept in trace order
+ * (ascending task id).  With time(x) = max(P[x's thread], x's start):
+ *   DD_POLICY_EARLIEST  the first task of least time (the default rule);
+ *   DD_POLICY_PRIORITY  P3's rule (the appendix's P3 model, its Schedule
+ *                       function): scanning Q in order, a task of least time
+ *                       is chosen, and a later task of equal time replaces
+ *                       the choice when both are push/pull tasks (pp != 0)
+ *                       and its priority is strictly higher.
+ * On graphs whose threads are single chains every rule gives the result of
+ * dd_simulate_batch.  Transformations as above (removed tasks run with zero
+ * duration and gap); every variant's own edge classes apply, so one call
+ * covers all variants of `var` without a schedule handle.
+ *   pp, prio    uint8 [n] and int32 [n], host or device, read by
+ *               DD_POLICY_PRIORITY (may be NULL for DD_POLICY_EARLIEST).
+ *   d_finish    device int64 [n][V] (task-major, variant-minor), required
+ *               unless n == 0.   d_start: the same or NULL.
+ *   d_makespan  device int64 [V], required.
+ * Limits: n < 2^22, n_threads <= 4096, in_ptr[n] + n < 2^31, and at most
+ * 1024 tasks ready at once in any variant (DD_ELIMIT beyond, outputs
+ * undefined).
+ * Synchronous: returns when the simulation is done, with DD_ECYCLE if some
+ * variant's active dependencies and thread chains contain a cycle.  Working
+ * memory: 12 * n * V bytes of device memory for the call.
+ */
+#define DD_POLICY_EARLIEST 0
+#define DD_POLICY_PRIORITY 1
+dd_status dd_simulate_policy(const dd_graph *g, const dd_variants *var, int32_t policy,
+                             const uint8_t *pp, const int32_t *prio,
+                             int64_t *d_finish, int64_t *d_start, int64_t *d_makespan,
+                             void *stream);
 
 /*
  * dd_release_cache -- wait for all work on the current device, then return

@@ -84,3 +84,38 @@ def simulate(di: DeviceInputs, mode=B.DD_PHASES, want_start=False, stream=None,
     if keep_handles:
         return res, g, handles
     return res
+
+
+def simulate_policy(g, vs, policy, pp=None, prio=None, shared=True, want_start=False,
+                    stream=None, device="cuda"):
+    """All variants under a schedule rule (dd_simulate_policy): the graph is
+    loaded with DD_LOAD_SHARED_THREADS when `shared`, the full variant table
+    goes in one handle.  Returns (finish[N][V], start or None, makespan[V])."""
+    import torch
+
+    def t(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(device)
+    gl = B.dd_graph_load_ex(g.n, g.n_threads, t(g.in_ptr.astype(np.int64)),
+                            t(g.in_src.astype(np.int32)), t(g.edge_cls.astype(np.uint8)),
+                            t(g.thread_prev.astype(np.int32)), t(g.thread_id.astype(np.int32)),
+                            t(g.dur.astype(np.int64)), t(g.gap.astype(np.int64)),
+                            t(g.node_cls.astype(np.uint16)),
+                            B.DD_LOAD_SHARED_THREADS if shared else 0, stream)
+    var = None
+    try:
+        V = vs.n_variants
+        var = B.dd_apply_transforms(gl, V, int(vs.scale.shape[0]), t(vs.scale.astype(np.int32)),
+                                    t(vs.remove_bits.astype(np.uint32)),
+                                    t(vs.edge_on[:, 0].astype(np.uint64)), stream)
+        fin = torch.empty((g.n, V), dtype=torch.int64, device=device)
+        st = torch.empty((g.n, V), dtype=torch.int64, device=device) if want_start else None
+        ms = torch.empty((V,), dtype=torch.int64, device=device)
+        B.dd_simulate_policy(gl, var, policy,
+                             None if pp is None else t(np.asarray(pp, np.uint8)),
+                             None if prio is None else t(np.asarray(prio, np.int32)),
+                             fin, st, ms, stream)
+    finally:
+        if var is not None:
+            B.dd_variants_free(var)
+        B.dd_graph_free(gl)
+    return fin, st, ms

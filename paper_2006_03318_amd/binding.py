@@ -16,15 +16,19 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libdd.so")
 HEADER = os.path.join(os.path.dirname(PKG), "include", "dd.h")
 
-DD_OK, DD_EINVAL, DD_ECYCLE, DD_ECHAIN, DD_ERANGE, DD_ENOMEM, DD_EHIP, DD_EMISMATCH = range(8)
+DD_OK, DD_EINVAL, DD_ECYCLE, DD_ECHAIN, DD_ERANGE, DD_ENOMEM, DD_EHIP, DD_EMISMATCH, \
+    DD_ELIMIT = range(9)
 DD_LEVELS, DD_PHASES = 0, 1
+DD_LOAD_SHARED_THREADS = 1
+DD_POLICY_EARLIEST, DD_POLICY_PRIORITY = 0, 1
 STATUS_NAMES = ["DD_OK", "DD_EINVAL", "DD_ECYCLE", "DD_ECHAIN", "DD_ERANGE", "DD_ENOMEM",
-                "DD_EHIP", "DD_EMISMATCH"]
+                "DD_EHIP", "DD_EMISMATCH", "DD_ELIMIT"]
 
 
 class DDError(RuntimeError):
     def __init__(self, code: int, msg: str):
-        super().__init__("%s: %s" % (STATUS_NAMES[code] if 0 <= code < 8 else code, msg))
+        super().__init__("%s: %s" % (STATUS_NAMES[code] if 0 <= code < len(STATUS_NAMES)
+                                     else code, msg))
         self.code = code
         self.msg = msg
 
@@ -56,7 +60,10 @@ def lib():
     sig = {
         "dd_graph_load": (_i32, [_i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                  ctypes.POINTER(_vp)]),
+        "dd_graph_load_ex": (_i32, [_i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                    ctypes.c_uint32, _vp, ctypes.POINTER(_vp)]),
         "dd_levelize": (_i32, [_vp, _u64, _i32, _vp, ctypes.POINTER(_vp), ctypes.POINTER(_i64)]),
+        "dd_simulate_policy": (_i32, [_vp, _vp, _i32, _vp, _vp, _vp, _vp, _vp, _vp]),
         "dd_apply_transforms": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, ctypes.POINTER(_vp)]),
         "dd_simulate_batch": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _vp]),
         "dd_simulate_batch_vs": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp]),
@@ -136,6 +143,26 @@ def dd_graph_load(n, n_threads, in_ptr, in_src, edge_cls, thread_prev, thread_id
                              _ptr(node_cls, "uint16", n), _stream(stream), ctypes.byref(out))
     _check(rc)
     return out
+
+
+def dd_graph_load_ex(n, n_threads, in_ptr, in_src, edge_cls, thread_prev, thread_id, dur_ns,
+                     gap_ns, node_cls, flags, stream=None):
+    out = _vp()
+    rc = lib().dd_graph_load_ex(int(n), int(n_threads), _ptr(in_ptr, "int64", n + 1),
+                                _ptr(in_src, "int32"), _ptr(edge_cls, "uint8"),
+                                _ptr(thread_prev, "int32", n), _ptr(thread_id, "int32", n),
+                                _ptr(dur_ns, "int64", n), _ptr(gap_ns, "int64", n),
+                                _ptr(node_cls, "uint16", n), ctypes.c_uint32(int(flags)),
+                                _stream(stream), ctypes.byref(out))
+    _check(rc)
+    return out
+
+
+def dd_simulate_policy(g, var, policy, pp, prio, d_finish, d_start, d_makespan, stream=None):
+    rc = lib().dd_simulate_policy(g, var, int(policy), _ptr(pp, "uint8"), _ptr(prio, "int32"),
+                                  _ptr(d_finish, "int64"), _ptr(d_start, "int64"),
+                                  _ptr(d_makespan, "int64"), _stream(stream))
+    _check(rc)
 
 
 def dd_levelize(g, active_edge_classes: int, mode: int, stream=None) -> Tuple[object, int]:

@@ -73,6 +73,7 @@ void free_graph_arrays(dd_graph *g) {
     dd::dfree(g->gap, s); dd::dfree(g->cls, s); dd::dfree(g->rank, s);
     dd::dfree(g->thread_base, s); dd::dfree(g->order, s); dd::dfree(g->xin_ptr, s);
     dd::dfree(g->xin_src, s); dd::dfree(g->xin_cls, s);
+    dd::free_event_lists(&g->ev, s);
 }
 
 void free_sched_arrays(dd_sched *x) {
@@ -222,6 +223,7 @@ const char *dd_status_str(dd_status s) {
         case DD_ENOMEM: return "DD_ENOMEM";
         case DD_EHIP: return "DD_EHIP";
         case DD_EMISMATCH: return "DD_EMISMATCH";
+        case DD_ELIMIT: return "DD_ELIMIT";
     }
     return "DD_UNKNOWN";
 }
@@ -232,9 +234,19 @@ dd_status dd_graph_load(int32_t n, int32_t n_threads, const int64_t *in_ptr, con
                         const uint8_t *edge_cls, const int32_t *thread_prev,
                         const int32_t *thread_id, const int64_t *dur_ns, const int64_t *gap_ns,
                         const uint16_t *node_cls, void *stream, dd_graph **out) {
+    return dd_graph_load_ex(n, n_threads, in_ptr, in_src, edge_cls, thread_prev, thread_id,
+                            dur_ns, gap_ns, node_cls, 0u, stream, out);
+}
+
+dd_status dd_graph_load_ex(int32_t n, int32_t n_threads, const int64_t *in_ptr,
+                           const int32_t *in_src, const uint8_t *edge_cls,
+                           const int32_t *thread_prev, const int32_t *thread_id,
+                           const int64_t *dur_ns, const int64_t *gap_ns, const uint16_t *node_cls,
+                           uint32_t flags, void *stream, dd_graph **out) {
     g_err[0] = 0;
     if (!out) return fail(DD_EINVAL, "out is NULL");
     *out = nullptr;
+    if (flags & ~DD_LOAD_SHARED_THREADS) return fail(DD_EINVAL, "unknown load flags 0x%x", flags);
     if (n < 0) return fail(DD_EINVAL, "n < 0");
     if (n_threads < 1) return fail(DD_EINVAL, "n_threads < 1");
     if (!in_ptr) return fail(DD_EINVAL, "in_ptr is NULL");
@@ -245,6 +257,7 @@ dd_status dd_graph_load(int32_t n, int32_t n_threads, const int64_t *in_ptr, con
     dd_graph *g = new dd_graph();
     g->n = n;
     g->n_threads = n_threads;
+    g->shared = (flags & DD_LOAD_SHARED_THREADS) != 0;
     g->stream = s;
     g->id = g_next_id.fetch_add(1);
     (void)hipGetDevice(&g->device);
@@ -302,25 +315,36 @@ dd_status dd_graph_load(int32_t n, int32_t n_threads, const int64_t *in_ptr, con
     }
     h_err = h_err2[0];
     if (h_err) { st = map_err_bits(h_err); goto fail_out; }
-    TRY(dd::dalloc_n(&g->thread_base, (size_t)n_threads + 1, s), "alloc");
-    TRY(dd::dalloc_n(&len, (size_t)n_threads + 1, s), "alloc");
-    TRY(dd::dalloc_n(&g->order, N1, s), "alloc");
-    TRY(dd::launch_build_order(g, succ, len, s), "order");
-    TRY(dd::dalloc_n(&g->xin_ptr, N1, s), "alloc");
-    if (n > 0) {
-        TRY(dd::launch_cross_edges(g, d_in_ptr, d_in_src, edge_cls ? d_ecls : nullptr, cnt, err, stats, s), "cross edges");
+    if (g->shared) {
+        // several chains per thread: no thread-major order and no dropped
+        // edges; every dependency edge stays for the schedule-rule path
+        g->xin_ptr = d_in_ptr; d_in_ptr = nullptr;
+        g->xin_src = d_in_src; d_in_src = nullptr;
+        g->xin_cls = d_ecls; d_ecls = nullptr;
+        g->n_cross = E;
+        TRY(hipMemcpyAsync(&hs, stats, sizeof(hs), hipMemcpyDeviceToHost, s), "read stats");
+        TRY(hipStreamSynchronize(s), "sync");
     } else {
-        TRY(hipMemsetAsync(g->xin_ptr, 0, sizeof(int64_t), s), "memset");
+        TRY(dd::dalloc_n(&g->thread_base, (size_t)n_threads + 1, s), "alloc");
+        TRY(dd::dalloc_n(&len, (size_t)n_threads + 1, s), "alloc");
+        TRY(dd::dalloc_n(&g->order, N1, s), "alloc");
+        TRY(dd::launch_build_order(g, succ, len, s), "order");
+        TRY(dd::dalloc_n(&g->xin_ptr, N1, s), "alloc");
+        if (n > 0) {
+            TRY(dd::launch_cross_edges(g, d_in_ptr, d_in_src, edge_cls ? d_ecls : nullptr, cnt, err, stats, s), "cross edges");
+        } else {
+            TRY(hipMemsetAsync(g->xin_ptr, 0, sizeof(int64_t), s), "memset");
+        }
+        // cross-edge lists sized by the edge count (an upper bound), so they are
+        // filled before the one read-back of the counts and error bits
+        TRY(dd::dalloc_n(&g->xin_src, (size_t)E + 1, s), "alloc");
+        TRY(dd::dalloc_n(&g->xin_cls, (size_t)E + 1, s), "alloc");
+        if (n > 0) TRY(dd::launch_cross_fill(g, d_in_ptr, d_in_src, edge_cls ? d_ecls : nullptr, s), "cross fill");
+        TRY(hipMemcpyAsync(&h_err, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "read err");
+        TRY(hipMemcpyAsync(&g->n_cross, g->xin_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s), "read");
+        TRY(hipMemcpyAsync(&hs, stats, sizeof(hs), hipMemcpyDeviceToHost, s), "read stats");
+        TRY(hipStreamSynchronize(s), "sync");
     }
-    // cross-edge lists sized by the edge count (an upper bound), so they are
-    // filled before the one read-back of the counts and error bits
-    TRY(dd::dalloc_n(&g->xin_src, (size_t)E + 1, s), "alloc");
-    TRY(dd::dalloc_n(&g->xin_cls, (size_t)E + 1, s), "alloc");
-    if (n > 0) TRY(dd::launch_cross_fill(g, d_in_ptr, d_in_src, edge_cls ? d_ecls : nullptr, s), "cross fill");
-    TRY(hipMemcpyAsync(&h_err, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "read err");
-    TRY(hipMemcpyAsync(&g->n_cross, g->xin_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s), "read");
-    TRY(hipMemcpyAsync(&hs, stats, sizeof(hs), hipMemcpyDeviceToHost, s), "read stats");
-    TRY(hipStreamSynchronize(s), "sync");
     if (h_err) { st = map_err_bits(h_err); goto fail_out; }
     g->dsum = ((__int128)hs.dsum_hi << 32) + (__int128)hs.dsum_lo;
     {
@@ -358,6 +382,8 @@ dd_status dd_levelize(const dd_graph *g, uint64_t active_edge_classes, int32_t m
     *out = nullptr;
     if (!g) return fail(DD_EINVAL, "graph is NULL");
     if (mode != DD_LEVELS && mode != DD_PHASES) return fail(DD_EINVAL, "mode must be DD_LEVELS or DD_PHASES");
+    if (g->shared)
+        return fail(DD_EINVAL, "the graph was loaded with shared threads: simulate it with dd_simulate_policy");
     hipStream_t s = (hipStream_t)stream;
     dd_sched *x = new dd_sched();
     x->graph_id = g->id;
@@ -522,6 +548,9 @@ dd_status dd_runtime_breakdown(const dd_graph *g, const dd_variants *var, const 
     if (!d_makespan || !d_out || (g->n > 0 && (!d_finish || !role)))
         return fail(DD_EINVAL, "role, d_finish, d_makespan and d_out are required");
     if (var->graph_id != g->id) return fail(DD_EMISMATCH, "handles come from different graphs");
+    if (g->shared)
+        return fail(DD_EINVAL, "the graph was loaded with shared threads: its thread order is "
+                               "decided by the schedule rule, not recorded");
     hipStream_t s = (hipStream_t)stream;
     dd_status st = DD_OK;
     uint8_t *d_role = nullptr;
@@ -538,6 +567,72 @@ fail_out:
     dd::dfree(d_role, s);
     dd::dfree(scratch, s);
     dd::dfree(order, s);
+    return st;
+}
+
+dd_status dd_simulate_policy(const dd_graph *g, const dd_variants *var, int32_t policy,
+                             const uint8_t *pp, const int32_t *prio, int64_t *d_finish,
+                             int64_t *d_start, int64_t *d_makespan, void *stream) {
+    g_err[0] = 0;
+    if (!g || !var) return fail(DD_EINVAL, "NULL handle");
+    if (policy != DD_POLICY_EARLIEST && policy != DD_POLICY_PRIORITY)
+        return fail(DD_EINVAL, "policy must be DD_POLICY_EARLIEST or DD_POLICY_PRIORITY");
+    if (policy == DD_POLICY_PRIORITY && g->n > 0 && (!pp || !prio))
+        return fail(DD_EINVAL, "DD_POLICY_PRIORITY needs pp and prio");
+    if (!d_makespan || (!d_finish && g->n > 0))
+        return fail(DD_EINVAL, "d_finish and d_makespan are required");
+    if (var->graph_id != g->id) return fail(DD_EMISMATCH, "handles come from different graphs");
+    if (g->n >= (1 << dd::kEventIdBits))
+        return fail(DD_ELIMIT, "the schedule-rule path takes n < 2^%d tasks", dd::kEventIdBits);
+    if (g->n_threads > dd::kEventMaxThreads)
+        return fail(DD_ELIMIT, "the schedule-rule path takes at most %d threads", dd::kEventMaxThreads);
+    if (g->n_cross + (int64_t)g->n >= (int64_t(1) << 31))
+        return fail(DD_ELIMIT, "too many edges for the schedule-rule path");
+    hipStream_t s = (hipStream_t)stream;
+    dd_status st = DD_OK;
+    uint8_t *d_pp = nullptr;
+    int32_t *d_prio = nullptr, *ref = nullptr;
+    int64_t *est = nullptr;
+    uint32_t *err = nullptr;
+    uint32_t h_err = 0;
+    const size_t nv = (size_t)g->n * (size_t)var->V;
+    {
+        std::lock_guard<std::mutex> lk(g->ev_mu);
+        if (!g->ev.rec) {
+            hipError_t e = dd::build_event_lists(g, &g->ev, s);
+            if (e != hipSuccess) {
+                dd::free_event_lists(&g->ev, s);
+                return hip_fail(e, "build out-edge lists");
+            }
+            // the lists belong to the graph and are released on its stream
+            e = dd::note_use(g->uses, g->stream, s);
+            if (e != hipSuccess) return hip_fail(e, "record stream use");
+        }
+    }
+    if (policy == DD_POLICY_PRIORITY) {
+        TRY(copy_in(&d_pp, pp, (size_t)g->n, s), "copy pp");
+        TRY(copy_in(&d_prio, prio, (size_t)g->n, s), "copy prio");
+    }
+    TRY(dd::dalloc_n(&ref, nv, s), "alloc reference counts");
+    TRY(dd::dalloc_n(&est, nv, s), "alloc start times");
+    TRY(copy_in(&err, (const uint32_t *)nullptr, 1, s), "alloc");
+    TRY(dd::launch_sim_event(g, g->ev, var, policy, d_pp, d_prio, ref, est, d_finish, d_start,
+                             d_makespan, err, s), "simulate");
+    TRY(hipMemcpyAsync(&h_err, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "read err");
+    TRY(hipStreamSynchronize(s), "sync");
+    TRY(dd::note_use(g->uses, g->stream, s), "record stream use");
+    TRY(dd::note_use(var->uses, var->stream, s), "record stream use");
+    if (h_err & 2u)
+        st = fail(DD_ELIMIT, "more than %d tasks were ready at once in some variant",
+                  dd::kEventQueue);
+    else if (h_err & 1u)
+        st = fail(DD_ECYCLE, "the active dependencies and thread chains contain a cycle");
+fail_out:
+    dd::dfree(d_pp, s);
+    dd::dfree(d_prio, s);
+    dd::dfree(ref, s);
+    dd::dfree(est, s);
+    dd::dfree(err, s);
     return st;
 }
 

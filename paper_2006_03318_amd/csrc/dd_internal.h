@@ -86,8 +86,23 @@ struct LoadStats {
 
 }  // namespace dd
 
+namespace dd {
+// Out-edge lists for the task-by-task simulation under a schedule rule:
+// every dependency edge and every thread-order link as (child << 8 | class),
+// class 255 for thread order (always present), grouped by parent.
+struct EventLists {
+    int4 *rec = nullptr;        // [n] {first out-edge, out-edge count, thread, task class}
+    uint4 *e4 = nullptr;        // [n] the first four out-edges (0 past the count)
+    uint32_t *edges = nullptr;  // [n_edges]
+    int64_t n_edges = 0;
+};
+constexpr uint32_t kEdgeAlways = 255;
+}  // namespace dd
+
 struct dd_graph {
     int32_t n = 0, n_threads = 0;
+    bool shared = false;          // threads may hold several chains (DD_LOAD_SHARED_THREADS);
+                                  // then xin_* hold every dependency edge
     int64_t n_edges = 0, n_cross = 0;
     int device = 0;
     hipStream_t stream = nullptr;
@@ -108,6 +123,8 @@ struct dd_graph {
     int32_t *xin_src = nullptr;
     uint8_t *xin_cls = nullptr;
     mutable dd::ForeignUses uses;
+    mutable std::mutex ev_mu;     // guards ev, built on first use
+    mutable dd::EventLists ev;
 };
 
 struct dd_sched {
@@ -217,6 +234,20 @@ hipError_t simulate_noalloc(const dd_graph *g, const dd_sched *sch, const dd_var
 hipError_t launch_breakdown(const dd_graph *g, const dd_variants *var, const uint8_t *role_dev,
                             const int64_t *finish, const int64_t *makespan, int64_t *scratch,
                             int32_t *order, int64_t *out, hipStream_t s);
+
+// simulation under a schedule rule (k_event.hip)
+// out-edge lists of g (dependencies in xin_*, thread order in thread_prev)
+hipError_t build_event_lists(const dd_graph *g, EventLists *ev, hipStream_t s);
+void free_event_lists(EventLists *ev, hipStream_t s);
+// ref: int32 [V][n], est: int64 [V][n] working memory; err: uint32, zeroed
+// by the caller (bit 0: a cycle, bit 1: frontier capacity exceeded)
+hipError_t launch_sim_event(const dd_graph *g, const EventLists &ev, const dd_variants *var,
+                            int32_t policy, const uint8_t *pp, const int32_t *prio, int32_t *ref,
+                            int64_t *est, int64_t *finish, int64_t *start, int64_t *makespan,
+                            uint32_t *err, hipStream_t s);
+constexpr int kEventQueue = 1024;      // ready tasks one variant may hold
+constexpr int kEventIdBits = 22;       // tasks: n < 2^22
+constexpr int kEventMaxThreads = 4096;
 
 
 

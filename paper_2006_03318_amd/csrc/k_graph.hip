@@ -104,7 +104,7 @@ __global__ __launch_bounds__(kBS) void k_validate_nodes(
     const int64_t *__restrict__ dur, const int64_t *__restrict__ gap,
     const uint16_t *__restrict__ cls, const int64_t *__restrict__ in_ptr,
     int32_t *__restrict__ succ, int32_t *__restrict__ heads, uint32_t *__restrict__ err,
-    LoadStats *__restrict__ st) {
+    LoadStats *__restrict__ st, bool one_head) {
     uint32_t e = 0;
     // sums split at bit 32 so that no partial sum can overflow
     int64_t dhi = 0, dlo = 0, ghi = 0, glo = 0, dm = 0, gm = 0, cm = 0;
@@ -119,7 +119,7 @@ __global__ __launch_bounds__(kBS) void k_validate_nodes(
         } else if (p >= 0) {
             if (tid[p] != t) e |= ERR_PREV_THREAD;
             else succ[p] = (int32_t)u + 1;   // one claimer wins; the others are found later
-        } else if (t_ok) {
+        } else if (t_ok && one_head) {
             if (atomicAdd(&heads[t], 1) != 0) e |= ERR_HEADS;
         }
         int64_t d = dur[u], g = gap[u];
@@ -428,7 +428,8 @@ hipError_t launch_validate_nodes(const dd_graph *g, const int64_t *in_ptr, int32
     if (blocks > kValBlocks) blocks = kValBlocks;
     k_validate_nodes<<<blocks, kBS, 0, s>>>(g->n, g->n_threads, g->thread_prev,
                                                          g->thread_id, g->dur, g->gap, g->cls,
-                                                         in_ptr, succ, heads, err, st);
+                                                         in_ptr, succ, heads, err, st,
+                                                         !g->shared);
     return hipGetLastError();
 }
 

@@ -44,6 +44,11 @@ hipError_t simulate_noalloc(const dd_graph *, const dd_sched *, const dd_variant
 }
 hipError_t launch_breakdown(const dd_graph *, const dd_variants *, const uint8_t *, const int64_t *,
                             const int64_t *, int64_t *, int32_t *, int64_t *, hipStream_t) { STUB; }
+hipError_t build_event_lists(const dd_graph *, EventLists *, hipStream_t) { STUB; }
+void free_event_lists(EventLists *ev, hipStream_t) { *ev = EventLists(); }
+hipError_t launch_sim_event(const dd_graph *, const EventLists &, const dd_variants *, int32_t,
+                            const uint8_t *, const int32_t *, int32_t *, int64_t *, int64_t *,
+                            int64_t *, int64_t *, uint32_t *, hipStream_t) { STUB; }
 }  // namespace dd
 
 static int g_bad = 0;
@@ -60,8 +65,8 @@ static bool has_msg() { return dd_last_error() && dd_last_error()[0] != 0; }
 int main() {
     // status names
     const char *names[] = {"DD_OK", "DD_EINVAL", "DD_ECYCLE", "DD_ECHAIN", "DD_ERANGE",
-                           "DD_ENOMEM", "DD_EHIP", "DD_EMISMATCH"};
-    for (int i = 0; i < 8; i++) EXPECT(strcmp(dd_status_str((dd_status)i), names[i]) == 0, "status name");
+                           "DD_ENOMEM", "DD_EHIP", "DD_EMISMATCH", "DD_ELIMIT"};
+    for (int i = 0; i < 9; i++) EXPECT(strcmp(dd_status_str((dd_status)i), names[i]) == 0, "status name");
     EXPECT(strcmp(dd_status_str((dd_status)99), "DD_UNKNOWN") == 0, "unknown status");
 
     // graph load: argument checks
@@ -82,6 +87,9 @@ int main() {
     EXPECT(g == nullptr && has_msg(), "no handle and a message after a failed load");
     st = dd_graph_load(0, 1, ptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, &g);
     EXPECT(st == DD_EHIP || st == DD_ENOMEM, "empty graph without device");
+    EXPECT(dd_graph_load_ex(3, 2, ptr, src, nullptr, prev, tid, dur, gap, nullptr, 2u, nullptr, &g) == DD_EINVAL && g == nullptr, "unknown load flag");
+    st = dd_graph_load_ex(3, 2, ptr, src, nullptr, prev, tid, dur, gap, nullptr, DD_LOAD_SHARED_THREADS, nullptr, &g);
+    EXPECT((st == DD_EHIP || st == DD_ENOMEM) && g == nullptr, "shared-thread load without device");
 
     // levelize / transforms / simulate argument checks
     dd_sched *sch = (dd_sched *)0x1;
@@ -98,6 +106,7 @@ int main() {
     EXPECT(dd_simulate_batch_vs(nullptr, nullptr, nullptr, dummy, nullptr, dummy, 16, nullptr) == DD_EINVAL, "width 16 NULL handles");
     EXPECT(dd_runtime_breakdown(nullptr, nullptr, nullptr, dummy, dummy, dummy, nullptr) == DD_EINVAL, "breakdown NULL handles");
     EXPECT(dd_simulate_batch_noalloc(nullptr, nullptr, nullptr, dummy, nullptr, dummy, nullptr) == DD_EINVAL, "no-alloc NULL handles");
+    EXPECT(dd_simulate_policy(nullptr, nullptr, 0, nullptr, nullptr, dummy, nullptr, dummy, nullptr) == DD_EINVAL, "policy NULL handles");
     EXPECT(strstr(dd_last_error(), "NULL handle") != nullptr, "NULL handle message");
     EXPECT(dd_sched_task_steps(nullptr, nullptr, nullptr) == DD_EINVAL, "steps NULL");
     int64_t a, b, c, d;

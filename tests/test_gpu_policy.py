@@ -1,0 +1,178 @@
+"""Parity of the schedule-rule path (dd_simulate_policy) with the oracle's
+simulation under the same rule: bit-exact start, finish and makespan.
+
+* graphs with shared threads (tasks of a channel with no recorded order),
+  both rules, with zero-length tasks, removals, scales and edge classes;
+* the hand-worked P3 example;
+* single-chain graphs, where both rules must give dd_simulate_batch's
+  result, loaded with and without the shared-threads flag;
+* the errors the path reports: a cycle, a frontier past its capacity, and a
+  shared-thread graph handed to the batch path.
+"""
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2006_03318_amd import batch as BT
+from paper_2006_03318_amd import binding as B
+from paper_2006_03318_amd import workloads as W
+from tests import helpers as H
+from tests.gpu_common import assert_equal_arrays, require_gpu, say
+from tests.test_oracle_schedule import load_p3_toy
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu(g, vs, policy, pp, prio, shared=True):
+    import torch
+    fin, st, ms = BT.simulate_policy(g, vs, policy, pp, prio, shared=shared, want_start=True)
+    torch.cuda.synchronize()
+    return st.cpu().numpy().T, fin.cpu().numpy().T, ms.cpu().numpy()
+
+
+def _check(g, vs, policy, pp, prio, label, shared=True):
+    say("policy", label, "n=%d V=%d T=%d rule=%d" % (g.n, vs.n_variants, g.n_threads, policy))
+    S, F, M = _gpu(g, vs, policy, pp, prio, shared)
+    oS, oF, oM = O.run_policy(g, vs, policy, pp, prio)
+    assert_equal_arrays(label + " makespan", M, oM)
+    assert_equal_arrays(label + " finish", F, oF)
+    assert_equal_arrays(label + " start", S, oS)
+
+
+def _shared(seed, n_lo=5, n_hi=400, V_hi=40):
+    rng = np.random.default_rng(8100 + seed)
+    n = int(rng.integers(n_lo, n_hi))
+    g, pp, prio = W.random_shared_graph(rng, n, int(rng.integers(1, 5)), int(rng.integers(1, 4)),
+                                        mean_in=float(rng.uniform(0.3, 2.5)),
+                                        window=int(rng.integers(4, 64)),
+                                        zero_frac=float(rng.uniform(0, 0.4)),
+                                        n_edge_cls=int(rng.integers(1, 4)),
+                                        chain_frac=float(rng.uniform(0, 0.6)),
+                                        max_dur=int(rng.choice([3, 1000, 10**6])))
+    pp[rng.random(n) < 0.1] = 0           # some tasks on channels are not push/pull tasks
+    vs = W.random_variants(rng, g, int(rng.integers(1, V_hi)), p_remove=float(rng.uniform(0, 0.4)))
+    return g, vs, pp, prio
+
+
+@pytest.mark.parametrize("seed", range(30))
+@pytest.mark.parametrize("policy", [0, 1])
+def test_shared_random(seed, policy):
+    require_gpu()
+    g, vs, pp, prio = _shared(seed)
+    _check(g, vs, policy, pp, prio, "shared%d" % seed)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_shared_larger(seed):
+    """Thousands of tasks, tens of variants, more than 64 out-edges on some
+    tasks (a sync-like fan-out) and more than 64 variants (two removal words)."""
+    require_gpu()
+    rng = np.random.default_rng(8300 + seed)
+    g, pp, prio = W.random_shared_graph(rng, 6000, 3, 2, mean_in=1.2, window=200,
+                                        zero_frac=0.1, n_edge_cls=2, chain_frac=0.4)
+    # task 0 gains 100 children (dependency edges from it), kept in id order
+    extra = sorted(int(x) for x in rng.choice(np.arange(1, g.n), 100, replace=False))
+    dst_old = np.repeat(np.arange(g.n, dtype=np.int64), np.diff(g.in_ptr))
+    src = np.concatenate([g.in_src.astype(np.int64), np.zeros(100, np.int64)])
+    dst = np.concatenate([dst_old, np.array(extra, np.int64)])
+    cls = np.concatenate([g.edge_cls, np.zeros(100, np.uint8)])
+    o = np.argsort(dst, kind="stable")
+    g.in_src = src[o].astype(np.int32)
+    g.edge_cls = cls[o]
+    g.in_ptr = np.concatenate([[0], np.cumsum(np.bincount(dst, minlength=g.n))]).astype(np.int64)
+    vs = W.random_variants(rng, g, 70, p_remove=0.2)
+    for policy in (0, 1):
+        _check(g, vs, policy, pp, prio, "larger%d" % seed)
+
+
+def test_p3_hand_example():
+    require_gpu()
+    g, pp, prio, exp = load_p3_toy()
+    for policy in (0, 1):
+        S, F, M = _gpu(g, H.variants(g, V=1), policy, pp, prio)
+        assert S[0].tolist() == exp["start%d" % policy]
+        assert M[0] == exp["makespan%d" % policy][0]
+
+
+@pytest.mark.parametrize("shared", [False, True])
+def test_single_chains_match_the_batch_path(shared):
+    require_gpu()
+    for k, V in ((1, 37), (2, 20)):
+        g, vs = W.config(k, variants=V)
+        oS, oF, oM, _ = O.run(g, vs)
+        rng = np.random.default_rng(k)
+        pp = (rng.random(g.n) < 0.5).astype(np.uint8)
+        prio = rng.integers(-3, 4, size=g.n).astype(np.int32)
+        for policy in (0, 1):
+            say("policy chains config%d shared=%d rule=%d" % (k, shared, policy))
+            S, F, M = _gpu(g, vs, policy, pp, prio, shared)
+            assert_equal_arrays("makespan", M, oM)
+            assert_equal_arrays("finish", F, oF)
+            assert_equal_arrays("start", S, oS)
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_single_chain_random(seed):
+    require_gpu()
+    rng = np.random.default_rng(8500 + seed)
+    n = int(rng.integers(1, 200))
+    g = W.random_graph(rng, n, int(rng.integers(1, 6)), p_edge=float(rng.uniform(0.01, 0.2)),
+                       n_edge_cls=int(rng.integers(1, 4)), max_dur=1000)
+    vs = W.random_variants(rng, g, int(rng.integers(1, 50)), p_remove=0.3)
+    oS, oF, oM, _ = O.run(g, vs)
+    say("policy chain-random%d n=%d" % (seed, n))
+    S, F, M = _gpu(g, vs, 0, None, None, shared=False)
+    assert_equal_arrays("makespan", M, oM)
+    assert_equal_arrays("start", S, oS)
+
+
+def test_cycle_is_reported():
+    require_gpu()
+    # 0 -> 1 -> 0 through dependencies on two channel tasks
+    g = H.graph(2, [0, 1], [(0, 1), (1, 0)], [5, 5], [0, 0], thread_order=[])
+    with pytest.raises(B.DDError) as ei:
+        _gpu(g, H.variants(g, V=2), 0, None, None)
+    assert ei.value.code == B.DD_ECYCLE
+
+
+def test_frontier_capacity_is_reported():
+    """1100 tasks ready at once exceed the 1024-entry frontier: an error,
+    not a wrong answer (the kernel drops the extra entries and every wave
+    ends)."""
+    require_gpu()
+    n = 1100
+    g = H.graph(1, [0] * n, [], [1] * n, [0] * n, thread_order=[])
+    g.thread_prev = np.full(n, -1, np.int32)
+    with pytest.raises(B.DDError) as ei:
+        _gpu(g, H.variants(g, V=3), 0, None, None)
+    assert ei.value.code == B.DD_ELIMIT
+    # 1024 is still fine
+    n = 1024
+    g = H.graph(1, [0] * n, [], [1] * n, [0] * n, thread_order=[])
+    g.thread_prev = np.full(n, -1, np.int32)
+    pp = np.ones(n, np.uint8)
+    prio = (np.arange(n) % 5).astype(np.int32)
+    _check(g, H.variants(g, V=3), 1, pp, prio, "capacity1024")
+
+
+def test_batch_path_refuses_shared_threads():
+    import torch
+    require_gpu()
+    g, pp, prio, _ = load_p3_toy()
+    di = BT.to_device(g, H.variants(g, V=1))
+    x = di.tensors
+    gl = B.dd_graph_load_ex(g.n, g.n_threads, x["in_ptr"], x["in_src"], x["edge_cls"],
+                            x["thread_prev"], x["thread_id"], x["dur"], x["gap"], x["node_cls"],
+                            B.DD_LOAD_SHARED_THREADS)
+    try:
+        with pytest.raises(B.DDError) as ei:
+            B.dd_levelize(gl, 1, B.DD_PHASES)
+        assert ei.value.code == B.DD_EINVAL
+    finally:
+        B.dd_graph_free(gl)
+    # without the flag the same graph is not one chain per thread
+    with pytest.raises(B.DDError) as ei:
+        B.dd_graph_load(g.n, g.n_threads, x["in_ptr"], x["in_src"], x["edge_cls"],
+                        x["thread_prev"], x["thread_id"], x["dur"], x["gap"], x["node_cls"])
+    assert ei.value.code == B.DD_ECHAIN
+    torch.cuda.synchronize()

@@ -93,6 +93,83 @@ def bench_breakdown(di, g, vs, stream, reps):
                          "traffic": None, "algorithmic_bytes_per_call": int(nbytes)}}
 
 
+def policy_bytes(n, V, n_edges_out):
+    """Bytes one schedule-rule call must move at minimum: per (task,
+    variant) the finish written (8 B), the reference count and start written
+    at set-up (12 B) and the task's frontier metadata read when it becomes
+    ready (thread 4, priority 4, push/pull flag 1, removal bit 1/8); per
+    (out-edge, variant) one read-modify-write of the child's count and start
+    (2 x 12 B); per task its record (32 B), duration and gap (16 B) and
+    out-edges (4 B each), read once per variant."""
+    per_tv = 8.0 + 12.0 + 9.0 + 1.0 / 8 + 48.0
+    return n * V * per_tv + n_edges_out * V * (24.0 + 4.0)
+
+
+def bench_policy(stream, reps, cpu_workers):
+    """Time dd_simulate_policy (both rules) on the VGG-19 parameter-server
+    workload with P3's sliced pushes and pulls, and time the oracle on the
+    same variants."""
+    import torch
+    from paper_2006_03318_amd import binding as B, workloads as W
+    from oracle import oracle as O
+    g, vs, pp, prio = W.p3_workload(iters=32, variants=2048)
+    dev = torch.device("cuda:0")
+
+    def t(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    gl = B.dd_graph_load_ex(g.n, g.n_threads, t(g.in_ptr), t(g.in_src), t(g.edge_cls),
+                            t(g.thread_prev), t(g.thread_id), t(g.dur), t(g.gap), t(g.node_cls),
+                            B.DD_LOAD_SHARED_THREADS, stream)
+    V = vs.n_variants
+    out = {}
+    try:
+        var = B.dd_apply_transforms(gl, V, int(vs.scale.shape[0]), t(vs.scale), t(vs.remove_bits),
+                                    t(vs.edge_on[:, 0]), stream)
+        fin = torch.empty((g.n, V), dtype=torch.int64, device=dev)
+        ms = torch.empty((V,), dtype=torch.int64, device=dev)
+        dpp, dprio = t(pp), t(prio)
+        for policy, name in ((B.DD_POLICY_EARLIEST, "earliest"), (B.DD_POLICY_PRIORITY, "p3")):
+            times = []
+            for it in range(reps + 1):
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                B.dd_simulate_policy(gl, var, policy, dpp, dprio, fin, None, ms, stream)
+                e1.record(stream)
+                stream.synchronize()
+                if it >= 1:
+                    times.append(e0.elapsed_time(e1))
+            out[name] = (float(np.mean(times)), ms.cpu().numpy().copy())
+        B.dd_variants_free(var)
+    finally:
+        B.dd_graph_free(gl)
+    cores = max(1, min(len(os.sched_getaffinity(0)), cpu_workers))
+    t0 = time.perf_counter()
+    _, _, oms = O.run_policy(g, vs, 1, pp, prio, want_start=False, want_finish=False,
+                             workers=cores)
+    cpu_s = time.perf_counter() - t0
+    ms_call, gms = out["p3"]
+    n_out = g.n_edges + int((g.thread_prev >= 0).sum())
+    nbytes = policy_bytes(g.n, V, n_out)
+    achieved = nbytes / (ms_call / 1e3) / 1e9
+    steps = float(g.n) * V
+    return {"kernel": "k_sim_event", "workload": "%s: %d tasks (%d push/pull slices on 2 "
+                                                 "shared channels) x %d variants" %
+                                                 (g.name, g.n, int(pp.sum()), V),
+            "calls_timed": reps,
+            "avg_call_ms": {"p3": round(ms_call, 3), "earliest": round(out["earliest"][0], 3)},
+            "task_variant_steps_per_s": round(steps / (ms_call / 1e3), 1),
+            "ns_per_step_per_variant": round(ms_call * 1e6 / g.n, 1),
+            "parity_all_makespans_equal": bool(np.array_equal(gms, oms)),
+            "p3_over_earliest_mean_makespan": round(float(np.mean(gms / out["earliest"][1])), 4),
+            "cpu_oracle": {"value": round(steps / cpu_s, 1), "unit": "task-variant steps/s",
+                           "cores": cores, "kind": "oracle",
+                           "sample": "all %d variants (%.2f s wall)" % (V, cpu_s)},
+            "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                         "traffic": None, "algorithmic_bytes_per_call": int(nbytes)}}
+
+
 def kernel_source_digest():
     """sha256 over the sources the simulation kernel is compiled from."""
     import hashlib
@@ -138,6 +215,8 @@ def main():
                          "cores)")
     ap.add_argument("--breakdown-reps", type=int, default=5,
                     help="timed dd_runtime_breakdown calls after the steps (0 = skip)")
+    ap.add_argument("--policy-reps", type=int, default=3,
+                    help="timed dd_simulate_policy calls per rule on the P3 workload (0 = skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device to device three times: the plain copy "
                          "whose byte counters scale the simulation kernel's")
@@ -257,6 +336,12 @@ def main():
     if args.breakdown_reps > 0:
         bd = bench_breakdown(di, g, vs, stream, args.breakdown_reps)
 
+    # the schedule-rule path (Sec. 4.4 "Schedule", the P3 model) on its own
+    # workload, after the timed steps
+    pol = None
+    if args.policy_reps > 0:
+        pol = bench_policy(stream, args.policy_reps, args.cpu_workers)
+
     # parity sample + CPU baseline: the oracle on the first variants
     cpu = None
     parity = None
@@ -313,6 +398,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "runtime_breakdown": bd,
+        "schedule_policy": pol,
         "parity_sample_makespans_equal": parity,
     }
     print(json.dumps(out))

@@ -45,28 +45,46 @@ __device__ __forceinline__ int64_t scaled(int64_t d, const ScaleEntry &se) {
     return (int64_t)(se.magic ? (__umul64hi(a, se.magic) >> se.shift) : (a >> se.shift));
 }
 
-__device__ __forceinline__ int64_t wave_min64(int64_t x) {
-    for (int o = 32; o > 0; o >>= 1) {
-        const int64_t y = shfl_xor64(x, o);
-        x = y < x ? y : x;
-    }
-    return x;
+// Wave-wide minima: butterflies inside each row of 16 lanes with DPP (quad
+// permutations, half-row and row mirrors), then the four row results read
+// into scalar registers.  All 64 lanes must be active.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp32(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xf, 0xf, false);
 }
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp64(uint64_t x) {
+    const uint32_t lo = dpp32<CTRL>((uint32_t)x);
+    const uint32_t hi = dpp32<CTRL>((uint32_t)(x >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t x, int l) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), l);
+    return ((uint64_t)hi << 32) | lo;
+}
+template <class T>
+__device__ __forceinline__ T tmin(T a, T b) { return b < a ? b : a; }
 
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t x) {
-    for (int o = 32; o > 0; o >>= 1) {
-        const uint64_t y = (uint64_t)shfl_xor64((int64_t)x, o);
-        x = y < x ? y : x;
-    }
-    return x;
+    x = tmin(x, dpp64<0xB1>(x));     // quad_perm [1,0,3,2]
+    x = tmin(x, dpp64<0x4E>(x));     // quad_perm [2,3,0,1]
+    x = tmin(x, dpp64<0x141>(x));    // row_half_mirror
+    x = tmin(x, dpp64<0x140>(x));    // row_mirror
+    return tmin(tmin(readlane_u64(x, 0), readlane_u64(x, 16)),
+                tmin(readlane_u64(x, 32), readlane_u64(x, 48)));
 }
 
 __device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
-    for (int o = 32; o > 0; o >>= 1) {
-        const uint32_t y = (uint32_t)__shfl_xor((int)x, o, 64);
-        x = y < x ? y : x;
-    }
-    return x;
+    x = tmin(x, dpp32<0xB1>(x));
+    x = tmin(x, dpp32<0x4E>(x));
+    x = tmin(x, dpp32<0x141>(x));
+    x = tmin(x, dpp32<0x140>(x));
+    const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)x, 0);
+    const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)x, 16);
+    const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)x, 32);
+    const uint32_t d = (uint32_t)__builtin_amdgcn_readlane((int)x, 48);
+    return tmin(tmin(a, b), tmin(c, d));
 }
 
 __device__ __forceinline__ uint32_t pick4(const uint4 &e, int k) {
@@ -221,46 +239,44 @@ __global__ __launch_bounds__(64) void k_sim_event(EvArgs a) {
     int64_t ms = 0;
     int32_t done = 0;
     while (qn > 0) {
-        // ---- schedule(Q): least (time, id) per lane, then over the wave ----
-        int64_t tb = INT64_MAX;
+        // ---- schedule(Q) ----
+        // One pass: per lane, the least time among its entries, the least
+        // (id, slot) among its entries of that time, and the best push/pull
+        // key (highest priority, then least id) among them.  Times are
+        // nonnegative, so they compare as unsigned.
+        uint64_t tb = ~0ull;
         uint32_t kb = 0xffffffffu;           // id << kSlotBits | slot
+        uint64_t pb = ~0ull;                 // ~priority << 32 | id << kSlotBits | slot
         for (int j = 0; j * 64 < qn; j++) {
             const int i = j * 64 + lane;
             if (i < qn) {
                 const int64_t p = sP[q.th[i]];
                 const int64_t e = q.est[i];
-                const int64_t t = p > e ? p : e;
-                const uint32_t k = ((q.a[i] & kIdMask) << kSlotBits) | (uint32_t)i;
-                if (t < tb || (t == tb && k < kb)) {
+                const uint64_t t = (uint64_t)(p > e ? p : e);
+                const uint32_t ai = q.a[i];
+                const uint32_t k = ((ai & kIdMask) << kSlotBits) | (uint32_t)i;
+                const uint64_t pk = (ai & kPPb)
+                    ? ((uint64_t)(~((uint32_t)q.pr[i] ^ 0x80000000u)) << 32) | k : ~0ull;
+                if (t < tb) {
                     tb = t;
                     kb = k;
+                    pb = pk;
+                } else if (t == tb) {
+                    kb = tmin(kb, k);
+                    pb = tmin(pb, pk);
                 }
             }
         }
-        const int64_t T0 = wave_min64(tb);
-        const uint32_t m1 = wave_min_u32(tb == T0 ? kb : 0xffffffffu);
+        const uint64_t T0 = wave_min_u64(tb);
+        const bool at = tb == T0;
+        const uint32_t m1 = wave_min_u32(at ? kb : 0xffffffffu);
         int32_t ws = (int32_t)(m1 & (uint32_t)(kQ - 1));
         if (a.policy == 1 && (q.a[ws] & kPPb)) {
             // the push/pull tasks of least time: highest priority, then least id
-            uint64_t pk = ~0ull;
-            for (int j = 0; j * 64 < qn; j++) {
-                const int i = j * 64 + lane;
-                if (i < qn && (q.a[i] & kPPb)) {
-                    const int64_t p = sP[q.th[i]];
-                    const int64_t e = q.est[i];
-                    if ((p > e ? p : e) == T0) {
-                        const uint32_t up = ~((uint32_t)q.pr[i] ^ 0x80000000u);
-                        const uint64_t k = ((uint64_t)up << 32) |
-                                           ((q.a[i] & kIdMask) << kSlotBits) | (uint32_t)i;
-                        pk = k < pk ? k : pk;
-                    }
-                }
-            }
-            pk = wave_min_u64(pk);
+            const uint64_t pk = wave_min_u64(at ? pb : ~0ull);
             ws = (int32_t)(pk & (uint64_t)(kQ - 1));
         }
         // ---- dispatch ----
-        ws = __builtin_amdgcn_readfirstlane(ws);
         const uint32_t wa = __builtin_amdgcn_readfirstlane(q.a[ws]);
         const int32_t th = __builtin_amdgcn_readfirstlane((int32_t)q.th[ws]);
         const int64_t eu = q.est[ws];
@@ -279,14 +295,13 @@ __global__ __launch_bounds__(64) void k_sim_event(EvArgs a) {
         const int64_t rel = f + gu;
         if (!rmv) ms = f > ms ? f : ms;
         const int32_t last = qn - 1;
-        if (ws != last) {
-            if (lane == 0) q.a[ws] = q.a[last];
-            if (lane == 1) q.th[ws] = q.th[last];
-            if (lane == 2) q.pr[ws] = q.pr[last];
-            if (lane == 3) q.est[ws] = q.est[last];
-        }
-        if (lane == 8) sP[th] = rel;
-        if (lane == 9) {
+        if (lane == 0) {
+            // the last entry fills the dispatched one's slot
+            q.a[ws] = q.a[last];
+            q.th[ws] = q.th[last];
+            q.pr[ws] = q.pr[last];
+            q.est[ws] = q.est[last];
+            sP[th] = rel;
             a.finish[(int64_t)u * V + v] = f;
             if (a.start) a.start[(int64_t)u * V + v] = s;
         }

@@ -31,9 +31,10 @@ K_LAUNCH, K_SYNC, K_GEMM, K_ELEM, K_AUX, K_WU, K_MEMCPY, K_COMM, K_CONV, \
     K_GPU_OTHER, K_OPT, K_EMB = range(12)
 # operator tags of CNN kernels (the layer types the batchnorm recipe selects)
 OP_NONE, OP_CONV, OP_BN, OP_RELU, OP_OTHER = range(5)
-N_KINDS = 12
+N_KINDS = 12          # kinds the synthetic generators emit (the class numbering uses it)
 GPU_KINDS = (K_GEMM, K_ELEM, K_AUX, K_WU, K_CONV, K_GPU_OTHER, K_OPT, K_EMB)
 CPU_KINDS = (K_LAUNCH, K_SYNC)
+K_API = 12            # a traced runtime call that neither issues nor waits for device work
 
 SEED_BASE = 2006033180
 
@@ -626,6 +627,131 @@ def _with_channel_orders(rng, g: TaskGraph, t: _Template, ars: List[int]) -> Tas
     in_ptr = np.cumsum(in_ptr)
     return dataclasses.replace(g, in_ptr=in_ptr, in_src=src.astype(np.int32),
                                edge_cls=cls.astype(np.uint8), n_edge_cls=5)
+
+
+# ---------------------------------------------------------------------------
+# parameter-server training with sliced gradient pushes and pulls (the P3
+# what-if of Sec. 5.1 and the appendix: every layer's gradient is cut into
+# slices; each slice is pushed after the backward kernel that produced it and
+# pulled back before the next iteration's forward kernel of that layer)
+SEND, RECV = 3, 4
+
+
+def vgg19_layer_params() -> Tuple[List[int], List[bool]]:
+    """Parameter counts of VGG-19's 19 weight layers (16 3x3 convolutions,
+    then three fully connected layers), from its layer shapes."""
+    chans = [64, 64, 128, 128, 256, 256, 256, 256, 512, 512, 512, 512, 512, 512, 512, 512]
+    params, fc = [], []
+    cin = 3
+    for c in chans:
+        params.append(9 * cin * c + c)
+        fc.append(False)
+        cin = c
+    for a, b in ((512 * 7 * 7, 4096), (4096, 4096), (4096, 1000)):
+        params.append(a * b + b)
+        fc.append(True)
+    return params, fc
+
+
+def _p3_iteration(params, fc, slice_bytes, servers):
+    """One iteration: forward (a convolution or GEMM and an element-wise
+    kernel per layer), loss, backward (data-gradient and weight-gradient
+    kernels per layer, in reverse), and for every layer's gradient its
+    slices: push on the send channel after the weight-gradient kernel, then
+    pull (on the send channel for slices kept by the first server, on the
+    receive channel otherwise).  Returns the template, the pull ids of each
+    layer, the first forward kernel of each layer and the slice sizes."""
+    L = len(params)
+    b = _Builder(5)
+    _, mc = b.launch(CPU, MEMCPY_S, K_MEMCPY, -1)
+    ff_first = []
+    for l in range(L):
+        _, k = b.launch(CPU, S0, K_GEMM if fc[l] else K_CONV, l,
+                        op=OP_OTHER if fc[l] else OP_CONV)
+        if l == 0:
+            b.edge(mc, k)
+        ff_first.append(k)
+        b.launch(CPU, S0, K_ELEM, l, op=OP_RELU)
+    b.launch(CPU, S0, K_ELEM, -1)                                   # loss
+    pulls = [[] for _ in range(L)]
+    sizes = []
+    n_slice = 0
+    for l in reversed(range(L)):
+        kind = K_GEMM if fc[l] else K_CONV
+        b.launch(CPU, S0, kind, l, op=OP_OTHER if fc[l] else OP_CONV)   # data gradient
+        _, u = b.launch(CPU, S0, kind, l, op=OP_OTHER if fc[l] else OP_CONV)   # weight gradient
+        left = 4 * params[l]
+        while left > 0:
+            sz = min(left, slice_bytes)
+            push = b.task(SEND, K_COMM, l)
+            pull = b.task(SEND if n_slice % servers == 0 else RECV, K_COMM, l)
+            b.edge(u, push)
+            b.edge(push, pull)
+            pulls[l].append(pull)
+            sizes += [sz, sz]
+            left -= sz
+            n_slice += 1
+    b.sync(CPU, [S0], -1)
+    return _template(b, L), pulls, ff_first, np.array(sizes, np.int64)
+
+
+def p3_workload(iters: int = 8, slice_bytes: int = 4 << 20, servers: int = 4, gbps: int = 10,
+                variants: int = 1024, seed: Optional[int] = None):
+    """VGG-19 data-parallel training on a parameter server with P3's sliced
+    pushes and pulls: `iters` chained iterations; the two channels (threads
+    SEND and RECV) hold the slices with no recorded order, so a schedule rule
+    orders them.  Slice durations are bytes at `gbps` Gbit/s; kernels are
+    lognormal (convolutions median 3 ms, GEMMs 1 ms, element-wise 0.3 ms).
+    Variants (through the recipe compiler): link bandwidth 1-40 Gbit/s, with
+    or without AMP, and some with cheaper launch calls.
+    Returns (graph, variants, pp, prio): pp = 1 on push/pull tasks, prio =
+    minus the layer index (layers nearer the input first)."""
+    from . import recipes as R
+    rng = np.random.default_rng(SEED_BASE + 6 if seed is None else seed)
+    params, fc = vgg19_layer_params()
+    t, pulls, ff_first, sizes = _p3_iteration(params, fc, slice_bytes, servers)
+    comm_ns = sizes * 8 // gbps
+    medians = {K_CONV: 3_000_000, K_GEMM: 1_000_000, K_ELEM: 300_000}
+    g = _tile(t, iters, rng, medians, (1_000_000, 4_000_000), "vgg19-p3", comm_ns=comm_ns)
+    n1 = t.thread.shape[0]
+    # the channels keep no recorded order: every slice task is a chain of its own
+    g.thread_prev[np.isin(g.thread_id, (SEND, RECV))] = -1
+    ch = np.isin(g.thread_id, (SEND, RECV))
+    nxt = np.full(g.n, -1, np.int64)
+    has = g.thread_prev >= 0
+    nxt[g.thread_prev[has]] = np.nonzero(has)[0]
+    assert not ch[nxt[nxt >= 0]].any()
+    # a layer's pulls come before the next iteration's forward kernel of it
+    xs, xd = [], []
+    for it in range(iters - 1):
+        for l, pl in enumerate(pulls):
+            for p_ in pl:
+                xs.append(it * n1 + p_)
+                xd.append((it + 1) * n1 + ff_first[l])
+    dst_old = np.repeat(np.arange(g.n, dtype=np.int64), np.diff(g.in_ptr))
+    src = np.concatenate([g.in_src.astype(np.int64), np.array(xs, np.int64)])
+    dst = np.concatenate([dst_old, np.array(xd, np.int64)])
+    cls = np.concatenate([g.edge_cls, np.zeros(len(xs), np.uint8)])
+    o = np.argsort(dst, kind="stable")
+    in_ptr = np.zeros(g.n + 1, np.int64)
+    np.add.at(in_ptr, dst + 1, 1)
+    g = dataclasses.replace(g, in_ptr=np.cumsum(in_ptr), in_src=src[o].astype(np.int32),
+                            edge_cls=cls[o].astype(np.uint8), n_threads=5)
+    pp = (g.kind == K_COMM).astype(np.uint8)
+    prio = np.where(g.kind == K_COMM, -g.layer, 0).astype(np.int32)
+    sweep = []
+    bws = (1, 2, 5, 10, 25, 40)
+    for v in range(variants):
+        r = [R.Distributed(bws[v % len(bws)], base_gbps=gbps)]
+        if (v // len(bws)) % 2:
+            r.append(R.AMP())
+        if (v // (2 * len(bws))) % 2:
+            r.append(R.ScaleLaunch(1, 2))
+        if v >= 4 * len(bws) and rng.random() < 0.5:
+            r.append(R.ScaleKernels(int(rng.integers(1, 4)), int(rng.integers(1, 4))))
+        sweep.append(r)
+    g, vs = R.compile_sweep(g, sweep)
+    return g, vs, pp, prio
 
 
 def task_roles(g: TaskGraph) -> np.ndarray:

@@ -176,3 +176,12 @@ def test_batch_path_refuses_shared_threads():
                         x["thread_prev"], x["thread_id"], x["dur"], x["gap"], x["node_cls"])
     assert ei.value.code == B.DD_ECHAIN
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("slice_mb", [1, 4])
+def test_p3_workload(slice_mb):
+    """The VGG-19 parameter-server sweep with P3's slices, both rules."""
+    require_gpu()
+    g, vs, pp, prio = W.p3_workload(iters=3, slice_bytes=slice_mb << 20, variants=48)
+    for policy in (0, 1):
+        _check(g, vs, policy, pp, prio, "p3-%dMB" % slice_mb)

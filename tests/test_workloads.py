@@ -81,3 +81,31 @@ def test_pack_roundtrip():
     for V in (1, 5, 31, 32, 33, 64, 100):
         b = rng.random((17, V)) < 0.3
         assert (W.unpack_bits(W.pack_bits(b), V) == b).all()
+
+
+def test_p3_workload_structure():
+    g, vs, pp, prio = W.p3_workload(iters=3, variants=12)
+    ch = np.isin(g.thread_id, (W.SEND, W.RECV))
+    assert (g.kind[ch] == W.K_COMM).all() and (pp == ch).all()
+    assert (g.thread_prev[ch] == -1).all()               # no recorded order on the channels
+    prev = g.thread_prev[g.thread_prev >= 0]
+    assert not ch[prev].any()
+    assert (prio[ch] == -g.layer[ch]).all() and (prio[~ch] == 0).all()
+    # every push follows the weight-gradient kernel of its layer, every pull its push
+    dst = np.repeat(np.arange(g.n), np.diff(g.in_ptr))
+    src = g.in_src
+    comm_dst = ch[dst]
+    assert (g.kind[src[comm_dst]] != W.K_LAUNCH).all()
+    # pulls of iteration i feed the forward kernel of their layer in iteration i+1
+    e = ch[src] & ~ch[dst]
+    assert e.any()
+    assert (g.layer[src[e]] == g.layer[dst[e]]).all()
+    assert (g.iteration[dst[e]] == g.iteration[src[e]] + 1).all()
+    # slice durations add up to each layer's gradient bytes at 10 Gbit/s
+    params, fc = W.vgg19_layer_params()
+    push = ch & (g.iteration == 0) & np.isin(np.arange(g.n), dst[ch[dst] & ~ch[src]])
+    for l in range(19):
+        tot = int(g.dur[push & (g.layer == l)].sum())
+        assert abs(tot - 4 * params[l] * 8 // 10) <= int((push & (g.layer == l)).sum())
+    assert len(params) == 19 and sum(params) > 140_000_000
+    assert vs.n_variants == 12 and len(vs.batches) == 1

@@ -538,21 +538,35 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                         X = on ? max64(X, rel) : X;
                     }
                     if (tcar) X = head ? max64(X, tcv) : X;
-                    if (extra) {
-                        const int64_t e1 = a.gat_ptr[r0 + q + 1];
-                        for (int64_t e = a.gat_ptr[r0 + q] + 2; e < e1; e++) {
-                            const uint8_t c = a.gat_cls[e];
-                            if (!cls_on(eo, c)) continue;
-                            const int32_t sp = a.gat_spos[e];
-                            int64_t rel;
-                            if (sp < prev_r0) {
-                                const int64_t sx = a.gat_src[e];
-                                const bool rs = (a.rm[sx * W + vwj] >> bit) & 1u;
-                                rel = a.finish[sx * V + vs_] + (rs ? 0 : a.gat_gap[e]);
-                            } else {
-                                rel = sR[(sp - prev_r0) * VS + os];
+                    if (__any(extra != 0u)) {
+                        // rare: wide fan-in.  The wave's lanes share each such
+                        // position's gathers beyond two (64 per pass, loads of
+                        // a pass in flight together), then a wave max hands
+                        // the result to the position's lane
+                        uint64_t todo = __ballot(extra != 0u);
+                        while (todo) {
+                            const int ld = __ffsll((unsigned long long)todo) - 1;
+                            todo &= todo - 1;
+                            const int64_t e0 = a.gat_ptr[r0 + ld] + 2, e1 = a.gat_ptr[r0 + ld + 1];
+                            int64_t mx = 0;
+                            for (int64_t eb = e0; eb < e1; eb += 64) {
+                                const int64_t e = eb + lane;
+                                if (e < e1) {
+                                    const uint8_t c = a.gat_cls[e];
+                                    const int32_t sp = a.gat_spos[e];
+                                    int64_t rel;
+                                    if (sp < prev_r0) {
+                                        const int64_t sx = a.gat_src[e];
+                                        const bool rs = (a.rm[sx * W + vwj] >> bit) & 1u;
+                                        rel = a.finish[sx * V + vs_] + (rs ? 0 : a.gat_gap[e]);
+                                    } else {
+                                        rel = sR[(sp - prev_r0) * VS + os];
+                                    }
+                                    if (cls_on(eo, c)) mx = max64(mx, rel);
+                                }
                             }
-                            X = max64(X, rel);
+                            mx = wave_max64(mx);
+                            if (lane == ld) X = max64(X, mx);
                         }
                     }
                     int64_t dp;
@@ -720,26 +734,51 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
 #pragma unroll
                     for (int j = 0; j < VPL; j++) X[j] = head ? max64(X[j], tc.x[j]) : X[j];
                 }
-                if (__any(extra != 0u) && extra) {             // rare: wide fan-in
-                    const int64_t e1 = a.gat_ptr[r0 + q + 1];
-                    for (int64_t e = a.gat_ptr[r0 + q] + 2; e < e1; e++) {
-                        const uint8_t c = a.gat_cls[e];
-                        const int32_t sp = a.gat_spos[e];
-                        Vals<VPL> rel;
-                        if (sp < prev_r0) {
-                            const int64_t sx = a.gat_src[e];
-                            const uint32_t rw = a.rm[sx * W + vw];
-                            const int64_t gg = a.gat_gap[e];
-                            const Vals<VPL> fx = *reinterpret_cast<const Vals<VPL> *>(a.finish + sx * V + vvf);
+                if (__any(extra != 0u)) {
+                    // rare: wide fan-in.  For each slot with such a position,
+                    // the wave's lanes share its gathers beyond two: lane l
+                    // takes gather l / LPS of a pass for its own variants (the
+                    // variants of lane l % LPS of every slot), then a max over
+                    // the lanes holding the same variants reaches the slot
+                    uint64_t todo = __ballot(extra != 0u && lis == 0);
+                    while (todo) {
+                        const int ld = __ffsll((unsigned long long)todo) - 1;
+                        todo &= todo - 1;
+                        const int qs = __shfl(q, ld, 64);
+                        const int64_t e0 = a.gat_ptr[r0 + qs] + 2, e1 = a.gat_ptr[r0 + qs + 1];
+                        int64_t mx[VPL];
 #pragma unroll
-                            for (int j = 0; j < VPL; j++)
-                                rel.x[j] = fx.x[j] + (((rw >> (vsh + j)) & 1u) ? 0 : gg);
-                        } else {
-                            rel = *reinterpret_cast<const Vals<VPL> *>(&sR[(sp - prev_r0) * VS + o0]);
+                        for (int j = 0; j < VPL; j++) mx[j] = 0;
+                        for (int64_t eb = e0; eb < e1; eb += 64 / LPS) {
+                            const int64_t e = eb + lane / LPS;
+                            if (e < e1) {
+                                const uint8_t c = a.gat_cls[e];
+                                const int32_t sp = a.gat_spos[e];
+                                Vals<VPL> rel;
+                                if (sp < prev_r0) {
+                                    const int64_t sx = a.gat_src[e];
+                                    const uint32_t rw = a.rm[sx * W + vw];
+                                    const int64_t gg = a.gat_gap[e];
+                                    const Vals<VPL> fx = *reinterpret_cast<const Vals<VPL> *>(a.finish + sx * V + vvf);
+#pragma unroll
+                                    for (int j = 0; j < VPL; j++)
+                                        rel.x[j] = fx.x[j] + (((rw >> (vsh + j)) & 1u) ? 0 : gg);
+                                } else {
+                                    rel = *reinterpret_cast<const Vals<VPL> *>(&sR[(sp - prev_r0) * VS + o0]);
+                                }
+#pragma unroll
+                                for (int j = 0; j < VPL; j++)
+                                    if (cls_on(eon[j], c)) mx[j] = max64(mx[j], rel.x[j]);
+                            }
                         }
+                        for (int o = LPS; o < 64; o <<= 1) {
 #pragma unroll
-                        for (int j = 0; j < VPL; j++)
-                            if (cls_on(eon[j], c)) X[j] = max64(X[j], rel.x[j]);
+                            for (int j = 0; j < VPL; j++) mx[j] = max64(mx[j], shfl_xor64(mx[j], o));
+                        }
+                        if (lane / LPS == ld / LPS) {
+#pragma unroll
+                            for (int j = 0; j < VPL; j++) X[j] = max64(X[j], mx[j]);
+                        }
                     }
                 }
                 if (anyh) {                                    // a run starts: reset the fold

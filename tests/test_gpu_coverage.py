@@ -137,3 +137,57 @@ def test_wide_fan_in_inside_big_round():
     _check(g, vs, B.DD_PHASES, "fan-in-200")
     for w in (1, 16):
         _check(g, vs, B.DD_PHASES, "fan-in-200-w%d" % w, w)
+
+
+def _multi_fan_in(rng, T=160, per=8, n_x=6, width=(70, 180), n_cls=3):
+    """Phase 0: runs of `per` tasks on T threads (several rounds, so a later
+    gather's source is in the previous round or older).  Phase 1: n_x tasks,
+    each on its own thread right after that thread's run, each waiting on
+    70-180 random phase-0 tasks through edges of random classes; the other
+    threads run two more tasks, so phase 1 has well over 64 positions and
+    several wide positions share a wave."""
+    thread, edges, ecls = [], [], []
+    for t in range(T):
+        thread += [t] * per
+    p0 = len(thread)
+    xs = []
+    for i in range(n_x):
+        x = len(thread)
+        thread.append(1 + i * 3)
+        xs.append(x)
+        k = int(rng.integers(width[0], width[1]))
+        for s in rng.choice(p0, size=k, replace=False):
+            if thread[int(s)] != thread[x]:
+                edges.append((int(s), x))
+                ecls.append(int(rng.integers(0, n_cls)))
+    for t in range(T):
+        if t % 3 == 1 and (t - 1) // 3 < n_x:
+            continue
+        a = len(thread)
+        thread += [t, t]
+        edges.append((int(rng.integers(0, p0)), a))
+        ecls.append(0)
+    n = len(thread)
+    g = H.graph(T, thread, edges, rng.integers(0, 10**6, n), rng.integers(0, 3000, n),
+                edge_cls=ecls, n_edge_cls=n_cls)
+    return g, xs
+
+
+@pytest.mark.parametrize("V", [37, 40])
+def test_several_wide_fan_ins_with_edge_classes(V):
+    """Wide positions (more than two gathers) several to a wave, sources
+    both in the previous round and older, edge classes switched per variant,
+    removals: every variants-per-workgroup width."""
+    require_gpu()
+    rng = np.random.default_rng(81_000 + V)
+    g, xs = _multi_fan_in(rng)
+    lv, ph = O.steps(g)
+    assert len(set(ph[xs].tolist())) == 1 and (ph == ph[xs[0]]).sum() > 64
+    assert min(int(g.in_ptr[x + 1] - g.in_ptr[x]) for x in xs) > 40
+    removed = [[int(u) for u in rng.choice(g.n, size=g.n // 5, replace=False)] if v else []
+               for v in range(V)]
+    masks = [1 | int(rng.integers(0, 8)) for _ in range(V)]
+    vs = H.variants(g, removed=removed, edge_on=masks, V=V)
+    vs.batches = [(0, V, 7)]
+    for w in (0, 1, 2, 4, 8, 16):
+        _check(g, vs, B.DD_PHASES, "multi-fan-in-V%d-w%d" % (V, w), w)

@@ -268,6 +268,28 @@ class CompressGradients(Recipe):
 
 
 @dataclasses.dataclass
+class ScaleCopies(Recipe):
+    """The offload and prefetch copies num/den as long (a faster or slower
+    host link)."""
+    num: int
+    den: int
+
+    def apply(self, g, plan):
+        scale_tasks(plan, (g.kind == W.K_MEMCPY) & np.isin(g.op, (W.OP_OFFLOAD, W.OP_PREFETCH)),
+                    self.num, self.den)
+
+
+@dataclasses.dataclass
+class RemoveOffload(Recipe):
+    """No memory offloading: the offload and prefetch copies are removed
+    with their launch calls."""
+
+    def apply(self, g, plan):
+        remove_tasks(plan, g, (g.kind == W.K_MEMCPY) & np.isin(g.op, (W.OP_OFFLOAD,
+                                                                      W.OP_PREFETCH)))
+
+
+@dataclasses.dataclass
 class EdgeClasses(Recipe):
     """Switch dependency classes on or off (Select plus re-route: for
     example one order of the communication channel)."""
@@ -280,11 +302,14 @@ class EdgeClasses(Recipe):
 
 # ---------------------------------------------------------------------------
 def compile_sweep(g: W.TaskGraph, variants: List[List[Recipe]],
-                  base_edge_mask: int = 1) -> Tuple[W.TaskGraph, W.VariantSet]:
+                  base_edge_mask: int = 1,
+                  one_batch_mask: Optional[int] = None) -> Tuple[W.TaskGraph, W.VariantSet]:
     """Run each variant's recipes and pack the result.  Returns the graph
     with one task class per distinct ratio column (and n_node_cls set) and
     the variant tables; batches are the runs of consecutive variants with
-    the same edge classes."""
+    the same edge classes, or, with `one_batch_mask`, one batch levelized
+    with those classes (the caller knows their union is acyclic; every
+    variant's classes must lie inside it)."""
     V = len(variants)
     if V < 1:
         raise ValueError("a sweep needs at least one variant")
@@ -306,11 +331,16 @@ def compile_sweep(g: W.TaskGraph, variants: List[List[Recipe]],
     scale = np.stack([P[:, rep].T, Q[:, rep].T], axis=2).astype(np.int32)   # [C][V][2]
     edge_on = np.array(masks, np.uint64).reshape(V, 1)
     batches = []
-    v0 = 0
-    for v in range(1, V + 1):
-        if v == V or masks[v] != masks[v0]:
-            batches.append((v0, v, int(masks[v0])))
-            v0 = v
+    if one_batch_mask is not None:
+        if any(m & ~one_batch_mask for m in masks):
+            raise ValueError("a variant switches on an edge class outside the batch's")
+        batches.append((0, V, int(one_batch_mask)))
+    else:
+        v0 = 0
+        for v in range(1, V + 1):
+            if v == V or masks[v] != masks[v0]:
+                batches.append((v0, v, int(masks[v0])))
+                v0 = v
     g2 = dataclasses.replace(g, node_cls=cls.astype(np.uint16), n_node_cls=int(C))
     return g2, W.VariantSet(V, scale, W.pack_bits(np.ascontiguousarray(R.T)), edge_on, batches)
 

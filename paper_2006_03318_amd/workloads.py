@@ -30,7 +30,8 @@ import numpy as np
 K_LAUNCH, K_SYNC, K_GEMM, K_ELEM, K_AUX, K_WU, K_MEMCPY, K_COMM, K_CONV, \
     K_GPU_OTHER, K_OPT, K_EMB = range(12)
 # operator tags of CNN kernels (the layer types the batchnorm recipe selects)
-OP_NONE, OP_CONV, OP_BN, OP_RELU, OP_OTHER = range(5)
+# and of the copies a memory-offloading recipe inserts
+OP_NONE, OP_CONV, OP_BN, OP_RELU, OP_OTHER, OP_OFFLOAD, OP_PREFETCH = range(7)
 N_KINDS = 12          # kinds the synthetic generators emit (the class numbering uses it)
 GPU_KINDS = (K_GEMM, K_ELEM, K_AUX, K_WU, K_CONV, K_GPU_OTHER, K_OPT, K_EMB)
 CPU_KINDS = (K_LAUNCH, K_SYNC)
@@ -752,6 +753,85 @@ def p3_workload(iters: int = 8, slice_bytes: int = 4 << 20, servers: int = 4, gb
         sweep.append(r)
     g, vs = R.compile_sweep(g, sweep)
     return g, vs, pp, prio
+
+
+# ---------------------------------------------------------------------------
+# memory offloading (vDNN, the appendix's model): each convolution's output is
+# copied to the host after the layer's forward pass and copied back before
+# its backward pass; when a copy back may start is the prefetch policy
+def _vdnn_iteration(n_layers=20, max_dist=3):
+    """One CNN iteration with vDNN's copies: after each layer's forward
+    kernels an offload copy (device to host) of its convolution output on the
+    copy stream; when the backward pass starts, one prefetch copy per layer
+    in backward order, each needed by the first backward kernel of its
+    layer.  Edge class d (1..max_dist) holds the prefetch policy "start the
+    copy back of layer l once the backward pass of layer l + d has begun"
+    (vDNN's choice of prefetch layer); with no class on, copies go back as
+    early as the copy stream allows."""
+    b = _Builder(3)
+    _, mc = b.launch(CPU, MEMCPY_S, K_MEMCPY, -1)
+    fwd_ops = (OP_CONV, OP_BN, OP_RELU)
+    bwd_ops = (OP_CONV, OP_CONV, OP_RELU, OP_BN, OP_OTHER, OP_OTHER)
+    first = True
+    for l in range(n_layers):
+        for j in range(3):
+            _, k = b.launch(CPU, S0, K_CONV if j == 0 else K_GPU_OTHER, l, op=fwd_ops[j])
+            if first:
+                b.edge(mc, k)
+                first = False
+            if j == 0:
+                conv = k
+        _, off = b.launch(CPU, MEMCPY_S, K_MEMCPY, l, op=OP_OFFLOAD)
+        b.edge(conv, off)                       # the feature map leaves once written
+    pf = {}
+    for l in reversed(range(n_layers)):
+        _, pf[l] = b.launch(CPU, MEMCPY_S, K_MEMCPY, l, op=OP_PREFETCH)
+    bwd_first = {}
+    for l in reversed(range(n_layers)):
+        for j in range(6):
+            _, k = b.launch(CPU, S0, K_CONV if bwd_ops[j] == OP_CONV else K_GPU_OTHER, l,
+                            op=bwd_ops[j])
+            if j == 0:
+                bwd_first[l] = k
+                b.edge(pf[l], k)                # the layer's backward needs its input back
+    for l in range(n_layers):
+        for d in range(1, max_dist + 1):
+            if l + d < n_layers:
+                b.edge(bwd_first[l + d], pf[l], d)
+    for l in range(n_layers):
+        b.launch(CPU, S0, K_OPT, l)
+    b.sync(CPU, [S0, MEMCPY_S], -1)
+    return _template(b, n_layers)
+
+
+def vdnn_workload(iters: int = 4, variants: int = 256, seed: Optional[int] = None):
+    """A 20-layer CNN trained with vDNN's offloading of convolution outputs
+    (the appendix's vDNN model), `iters` chained iterations.  Kernels are
+    lognormal (convolutions median 500 us, other kernels 100 us, optimizer
+    50 us); each copy takes U[100, 600] us (feature map over PCIe).
+    Variants (through the recipe compiler, one levelization for all: the
+    union of the policy classes is acyclic): no offloading, copies back as
+    early as possible, or prefetch 1, 2 or 3 layers ahead; PCIe 2x faster
+    or slower; with or without AMP."""
+    from . import recipes as R
+    rng = np.random.default_rng(SEED_BASE + 7 if seed is None else seed)
+    t = _vdnn_iteration()
+    g = _tile(t, iters, rng, {K_CONV: 500_000, K_GPU_OTHER: 100_000, K_OPT: 50_000},
+              (100_000, 600_000), "cnn-vdnn")
+    sweep = []
+    for v in range(variants):
+        pol = v % 5                       # 0: no offloading, 1: eager, 2-4: distance 1-3
+        r = [R.RemoveOffload()] if pol == 0 else (
+            [] if pol == 1 else [R.EdgeClasses(on=1 << (pol - 1))])
+        pcie = (v // 5) % 3
+        if pcie == 1:
+            r.append(R.ScaleCopies(1, 2))
+        elif pcie == 2:
+            r.append(R.ScaleCopies(2, 1))
+        if (v // 15) % 2:
+            r.append(R.AMP())
+        sweep.append(r)
+    return R.compile_sweep(g, sweep, one_batch_mask=0xF)
 
 
 def task_roles(g: TaskGraph) -> np.ndarray:

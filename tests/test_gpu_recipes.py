@@ -47,3 +47,11 @@ def test_random_recipe_mixes(seed):
         sweep = _random_sweep(rng, g, 70, L)
         g2, vs = R.compile_sweep(g, sweep)
         _check(g2, vs, "mix%d-config%d" % (seed, k))
+
+
+def test_vdnn_sweep():
+    """Memory offloading with the prefetch policies as edge classes, all in
+    one levelization."""
+    require_gpu()
+    g, vs = W.vdnn_workload(iters=3, variants=60)
+    _check(g, vs, "vdnn")

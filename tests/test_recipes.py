@@ -251,3 +251,50 @@ def test_class_grouping_against_row_sort():
         assert all((cls == cls[u]).tolist() == (inv == inv[u]).tolist() for u in range(min(N, 50)))
         assert (P[:, rep[cls]] == P).all() and (Q[:, rep[cls]] == Q).all()
         assert cls[0] == 0 and (np.diff(np.maximum.accumulate(cls)) <= 1).all()
+
+
+# --------------------------------------------------------------------------
+# memory offloading (vDNN)
+def test_vdnn_tables_and_structure():
+    g, vs = W.vdnn_workload(iters=2, variants=30)
+    copies = (g.kind == W.K_MEMCPY) & np.isin(g.op, (W.OP_OFFLOAD, W.OP_PREFETCH))
+    assert copies.sum() == 2 * 20 * 2                   # one out, one back per layer and iteration
+    bits = W.unpack_bits(vs.remove_bits, vs.n_variants)
+    launches = g.launch_of[copies]
+    for v in range(vs.n_variants):
+        p, q = R.task_ratios(vs, g, v)
+        if v % 5 == 0:                                  # no offloading: copies and launches gone
+            assert bits[copies, v].all() and bits[launches, v].all()
+            assert bits[:, v].sum() == 2 * copies.sum()
+        else:
+            assert not bits[:, v].any()
+        pcie = (v // 5) % 3
+        want = {0: (1, 1), 1: (1, 2), 2: (2, 1)}[pcie]
+        assert (p[copies] == want[0]).all() and (q[copies] == want[1]).all()
+        other = (g.kind == W.K_MEMCPY) & ~copies        # the input batch's copy keeps its time
+        assert (p[other] == 1).all() and (q[other] == 1).all()
+        pol = v % 5
+        assert int(vs.edge_on[v, 0]) == (1 | (1 << (pol - 1)) if pol >= 2 else 1)
+    assert vs.batches == [(0, 30, 0xF)]
+    # policy edges: class d goes from the backward pass of layer l + d to the copy back of l
+    dst = np.repeat(np.arange(g.n), np.diff(g.in_ptr))
+    for d in (1, 2, 3):
+        e = g.edge_cls == d
+        assert e.sum() == (20 - d) * 2
+        assert (g.op[dst[e]] == W.OP_PREFETCH).all()
+        assert (g.layer[g.in_src[e]] == g.layer[dst[e]] + d).all()
+    with pytest.raises(ValueError):
+        R.compile_sweep(g, [[R.EdgeClasses(on=1 << 5)]], one_batch_mask=0xF)
+
+
+def test_vdnn_policies_order(oracle_mod):
+    """Prefetching further ahead never lengthens the iteration: the copy back
+    of layer l waits for the backward pass of layer l + d, which starts no
+    later for larger d; eager copies wait for nothing, and no offloading
+    removes the copies altogether."""
+    g, vs = W.vdnn_workload(iters=2, variants=30)
+    _, _, M, _ = oracle_mod.run(g, vs, want_start=False, want_finish=False)
+    for base in range(0, 30, 5):
+        none, eager, d1, d2, d3 = M[base:base + 5]
+        assert none <= eager <= d3 <= d2 <= d1
+    assert M[2] > M[0]              # offloading costs something here

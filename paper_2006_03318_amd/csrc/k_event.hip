@@ -238,6 +238,8 @@ __global__ __launch_bounds__(64) void k_sim_event(EvArgs a) {
 
     int64_t ms = 0;
     int32_t done = 0;
+    int32_t bu = 0;                 // this lane's buffered result: task, finish, start
+    int64_t bf = 0, bs = 0;
     while (qn > 0) {
         // ---- schedule(Q) ----
         // One pass: per lane, the least time among its entries, the least
@@ -302,11 +304,21 @@ __global__ __launch_bounds__(64) void k_sim_event(EvArgs a) {
             q.pr[ws] = q.pr[last];
             q.est[ws] = q.est[last];
             sP[th] = rel;
-            a.finish[(int64_t)u * V + v] = f;
-            if (a.start) a.start[(int64_t)u * V + v] = s;
+        }
+        // results go out 64 at a time, one per lane: a store in every step
+        // would make each step's wait for its loads wait for the store too
+        // (vector memory operations complete in order)
+        if (lane == (done & 63)) {
+            bu = u;
+            bf = f;
+            bs = s;
         }
         qn = last;
         done++;
+        if ((done & 63) == 0) {
+            a.finish[(int64_t)bu * V + v] = bf;
+            if (a.start) a.start[(int64_t)bu * V + v] = bs;
+        }
         // ---- children ----
         for (int32_t base = 0; base < ur.y; base += 64) {
             const int32_t k = base + lane;
@@ -344,6 +356,10 @@ __global__ __launch_bounds__(64) void k_sim_event(EvArgs a) {
             qn += __popcll(b);
             if (qn > kQ) qn = kQ;
         }
+    }
+    if (lane < (done & 63)) {
+        a.finish[(int64_t)bu * V + v] = bf;
+        if (a.start) a.start[(int64_t)bu * V + v] = bs;
     }
     if (done != n) err |= 1u;
     for (int o = 32; o > 0; o >>= 1) err |= (uint32_t)__shfl_xor((int)err, o, 64);

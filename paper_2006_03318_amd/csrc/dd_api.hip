@@ -475,6 +475,10 @@ dd_status dd_apply_transforms(const dd_graph *g, int32_t n_variants, int32_t n_c
             st = fail(DD_ERANGE, "scaled durations could sum past 2^62 ns");
             goto fail_out;
         }
+        // every simulated time is a sum of weights along a path, so below
+        // the bound; 2^51 = 2.25e15 (a margin for rounding again)
+        x->f64_ok = bound < 2.0e15L &&
+                    (__int128)g->dmax * (__int128)pmax < ((__int128)1 << 53);
     }
     TRY(hipStreamSynchronize(s), "sync");
     TRY(dd::note_use(g->uses, g->stream, s), "record stream use");

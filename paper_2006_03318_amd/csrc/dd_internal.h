@@ -156,6 +156,8 @@ struct dd_variants {
     uint64_t used_mask = 0;       // OR of edge_on over all variants
     uint64_t all_mask = 0;        // AND of edge_on over all variants
     bool any_magic = false;       // some scale has q not a power of two
+    bool f64_ok = false;          // every simulated time below 2^51 and every d * p below
+                                  // 2^53: the double form of the time arithmetic is exact
     hipStream_t stream = nullptr;
     dd::ScaleEntry *table = nullptr;  // [n_cls][V]
     uint32_t *rm_bits = nullptr;      // [n][W]

@@ -140,17 +140,61 @@ __device__ __forceinline__ int64_t scaled8(int64_t d, uint64_t e, const ScaleEnt
 // a >= kHead, so no sum overflows.
 constexpr int64_t kHead = -(int64_t(1) << 62);
 
+// Time arithmetic.  Tm<false>: plain int64.  Tm<true>: every value is an
+// integer held in a double, which the hardware adds and compares in one
+// full-rate instruction each (int64 takes two to three).  Times are biased
+// by 2^52: the double of time t (0 <= t < 2^52) has the bit pattern
+// 0x4330000000000000 + t, so moving a time between HBM (int64) and a
+// register is one operation on its high word, and the bit patterns of
+// nonnegative doubles order as integers do.  Weights (durations, gaps and
+// their sums) stay unbiased, and a range holding a run head carries -inf,
+// which any sum keeps (c + -inf = -inf loses to every b in a max).  All of
+// it is exact while every simulated time stays below 2^51 and every
+// duration times the scale numerator below 2^53 (checked on the host; the
+// int64 form serves every other launch).  Values travel as int64 bit
+// patterns either way.
+template <bool FP> struct Tm;
+template <> struct Tm<false> {
+    static constexpr int64_t zero = 0;          // time 0
+    static constexpr int64_t head = kHead;      // weight sum of a range holding a run head
+    __device__ static __forceinline__ int64_t add(int64_t x, int64_t y) { return x + y; }
+    __device__ static __forceinline__ int64_t sub(int64_t x, int64_t y) { return x - y; }
+    __device__ static __forceinline__ int64_t mx(int64_t x, int64_t y) { return max64(x, y); }
+    __device__ static __forceinline__ int64_t from_time(int64_t t) { return t; }
+    __device__ static __forceinline__ int64_t to_time(int64_t x) { return x; }
+    __device__ static __forceinline__ int64_t w32(uint32_t w) { return (int64_t)w; }
+    __device__ static __forceinline__ double d(int64_t x) { return __longlong_as_double(x); }
+    __device__ static __forceinline__ int64_t i(double x) { return __double_as_longlong(x); }
+};
+template <> struct Tm<true> {
+    static constexpr int64_t zero = 0x4330000000000000ll;                    // 2^52
+    static constexpr int64_t head = (int64_t)0xFFF0000000000000ull;          // -inf
+    __device__ static __forceinline__ double d(int64_t x) { return __longlong_as_double(x); }
+    __device__ static __forceinline__ int64_t i(double x) { return __double_as_longlong(x); }
+    __device__ static __forceinline__ int64_t add(int64_t x, int64_t y) { return i(d(x) + d(y)); }
+    __device__ static __forceinline__ int64_t sub(int64_t x, int64_t y) { return i(d(x) - d(y)); }
+    __device__ static __forceinline__ int64_t mx(int64_t x, int64_t y) {
+        return i(__builtin_fmax(d(x), d(y)));
+    }
+    __device__ static __forceinline__ int64_t from_time(int64_t t) { return t | zero; }
+    __device__ static __forceinline__ int64_t to_time(int64_t x) { return x ^ zero; }
+    __device__ static __forceinline__ int64_t w32(uint32_t w) { return i((double)w); }
+};
+
 // (la, lb) then (a, b)
+template <bool FP = false>
 __device__ __forceinline__ void compose(int64_t la, int64_t lb, int64_t &a, int64_t &b) {
-    b = max64(lb + a, b);
-    a = a < 0 ? a : la + a;
+    b = Tm<FP>::mx(Tm<FP>::add(lb, a), b);
+    if (FP) a = Tm<FP>::add(la, a);
+    else a = a < 0 ? a : la + a;
 }
 
 // one Kogge-Stone step of the max-plus scan across the wave, the left
 // operand taken with a DPP lane shift (lanes without one see the identity
-// (0, 0), as b >= a).  Row shifts write every lane (bound control: 0 where
-// the source lies outside the row), so no lane needs its old value.
-template <int CTRL, int RMASK>
+// (0, 0), as b >= a; in the double form the bits 0 are 0.0, below every
+// biased time).  Row shifts write every lane (bound control: 0 where the
+// source lies outside the row), so no lane needs its old value.
+template <int CTRL, int RMASK, bool FP = false>
 __device__ __forceinline__ void scan_step(int64_t &a, int64_t &b) {
     constexpr bool BC = RMASK == 0xf;
     const int alo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)a, CTRL, RMASK, 0xf, BC);
@@ -159,7 +203,7 @@ __device__ __forceinline__ void scan_step(int64_t &a, int64_t &b) {
     const int bhi = __builtin_amdgcn_update_dpp(0, (int)((uint64_t)b >> 32), CTRL, RMASK, 0xf, BC);
     const int64_t la = join64(alo, ahi);
     const int64_t lb = join64(blo, bhi);
-    compose(la, lb, a, b);
+    compose<FP>(la, lb, a, b);
 }
 
 __device__ __forceinline__ int64_t readlane64(int64_t x, int l) {
@@ -169,13 +213,14 @@ __device__ __forceinline__ int64_t readlane64(int64_t x, int l) {
 }
 
 // inclusive scan over the 64 lanes of a wave
+template <bool FP = false>
 __device__ __forceinline__ void wave_scan(int64_t &a, int64_t &b) {
-    scan_step<0x111, 0xf>(a, b);   // row_shr:1
-    scan_step<0x112, 0xf>(a, b);   // row_shr:2
-    scan_step<0x114, 0xf>(a, b);   // row_shr:4
-    scan_step<0x118, 0xf>(a, b);   // row_shr:8
-    scan_step<0x142, 0xa>(a, b);   // row_bcast:15 into rows 1 and 3
-    scan_step<0x143, 0xc>(a, b);   // row_bcast:31 into rows 2 and 3
+    scan_step<0x111, 0xf, FP>(a, b);   // row_shr:1
+    scan_step<0x112, 0xf, FP>(a, b);   // row_shr:2
+    scan_step<0x114, 0xf, FP>(a, b);   // row_shr:4
+    scan_step<0x118, 0xf, FP>(a, b);   // row_shr:8
+    scan_step<0x142, 0xa, FP>(a, b);   // row_bcast:15 into rows 1 and 3
+    scan_step<0x143, 0xc, FP>(a, b);   // row_bcast:31 into rows 2 and 3
 }
 
 // Lane layout: slot = tid / LPS handles K consecutive positions; the LPS
@@ -190,9 +235,12 @@ __device__ __forceinline__ void wave_scan(int64_t &a, int64_t &b) {
 // end of a phase are ragged).
 //
 // UNI: every variant of the launch enables every edge class that the
-// schedule's gathers use, every scale is a power of two and every duration
-// and gap is below 2^32 (one 32x32 multiply and a shift per scaled
-// duration; a gather source's gap comes from the record).
+// schedule's gathers use, every scale is a power of two, every duration
+// and gap is below 2^32 (a gather source's gap comes from the record) and
+// the launch passes the bounds of the double form of the time arithmetic
+// (Tm<true>): the scaled duration is the floor of the duration times the
+// scale held as a double, and every sum and maximum of the walk, the scans
+// and the finalize is one double instruction.
 template <int LPS, int VPL, int K, bool TLDS, bool START, bool UNI, int NT>
 __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ round_r0,
                                                   const int32_t *__restrict__ round_rn,
@@ -201,6 +249,12 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
     constexpr int VS = LPS * VPL;
     constexpr int NS = NT / LPS;
     constexpr int RP = NS * K;
+    typedef Tm<UNI> TM;
+    // a gap read from memory as a weight (below 2^32 on the uniform path)
+    auto wt = [](int64_t g) -> int64_t {
+        if constexpr (UNI) return TM::w32((uint32_t)g);
+        else return g;
+    };
     // slot summaries, variant-major with a row stride of NSP: when a wave
     // scans whole variants, 4 entries of padding put the rows written by
     // one wave on different banks
@@ -274,13 +328,16 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             const ScaleEntry e = a.table[(int64_t)c * V + vx];
             const bool mg = e.magic != 0;
             any_magic |= mg;
-            sT[i] = (uint64_t)e.p | ((uint64_t)(e.shift & 0xff) << 32) | (mg ? (1ull << 40) : 0ull);
+            if (UNI)   // the scale p / 2^shift as a double (exact: p < 2^32)
+                sT[i] = (uint64_t)__double_as_longlong(__builtin_ldexp((double)e.p, -(int)(e.shift & 0xff)));
+            else
+                sT[i] = (uint64_t)e.p | ((uint64_t)(e.shift & 0xff) << 32) | (mg ? (1ull << 40) : 0ull);
         }
     }
-    for (int i = tid; i < kMaxCarryThreads * VS; i += NT) sTC[i] = 0;
+    for (int i = tid; i < kMaxCarryThreads * VS; i += NT) sTC[i] = TM::zero;
     if (tid < VS) {
         sMs[tid] = 0;
-        sCarry[tid] = 0;   // read by a first round that is small (finite, so heads ignore it)
+        sCarry[tid] = TM::zero;   // read by a first round that is small (finite, so heads ignore it)
         // per-variant values read inside the loop live in LDS: a register
         // loaded before the loop would make every round wait for all traffic
         sEon[tid] = a.edge_on[v0 + tid < a.V ? v0 + tid : 0];
@@ -414,8 +471,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         for (int j = 0; j < VPL; j++) asm volatile("" ::"v"(D.f0[i].x[j]));
     }
 
-    typename I64V<VPL>::T carry = 0, ms = 0;
-    int64_t msS0 = 0, msS1 = 0;               // small rounds: variants w and w + NW
+    typename I64V<VPL>::T carry = TM::zero, ms = TM::zero;
+    int64_t msS0 = TM::zero, msS1 = TM::zero;   // small rounds: variants w and w + NW
     int prev_r0 = 0;
     int b0 = 0, b1 = 1, b2 = 2;               // ring buffers of rounds k, k+1, k+2
     // Small and big rounds run as two inner loops rather than one loop with
@@ -480,7 +537,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
             const int4 w0 = r4[0], w1 = r4[1], w2 = r4[2];
             const int64_t dur = ((int64_t)(uint32_t)w0.y << 32) | (uint32_t)w0.x;
-            const int64_t gap = UNI ? (int64_t)(uint32_t)w0.z
+            const int64_t gap = UNI ? TM::w32((uint32_t)w0.z)
                                     : (((int64_t)(uint32_t)w0.w << 32) | (uint32_t)w0.z);
             const int32_t node = w1.x, s0 = w1.y, s1 = w1.z, p0 = w1.w, p1 = w2.x;
             const uint32_t cl = (uint32_t)w2.y;
@@ -498,6 +555,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             const bool any1 = __any(has1);
             const uint32_t extra = flags >> 8;
             const int tcx = ((flags >> 2) & 63u) * VS;
+            const int64_t g0w = UNI ? TM::w32((uint32_t)w2.w) : 0;   // first source's gap
             int64_t Fs[K], Ss[K];
             bool sts[K];
 #pragma unroll
@@ -520,24 +578,25 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     asm volatile("" : "+v"(yn), "+v"(tcv), "+v"(tev), "+v"(crv));
                     int64_t X;
                     {
-                        const int64_t g0g = UNI ? (int64_t)(uint32_t)w2.w : D.g0gap[jj];
-                        const int64_t ro = D.f0[jj].x[0] + (((D.r0w[jj] >> bit) & 1u) ? 0 : g0g);
+                        const int64_t g0g = UNI ? g0w : D.g0gap[jj];
+                        const int64_t ro = TM::add(TM::from_time(D.f0[jj].x[0]),
+                                                   ((D.r0w[jj] >> bit) & 1u) ? 0 : g0g);
                         const int64_t rel = old0 ? ro : yn;
                         const bool on = has0 && (all_on || cls_on(eo, c0));
-                        X = on ? rel : 0;
+                        X = on ? rel : TM::zero;
                     }
                     if (any1) {
                         int64_t ro = 0;
                         if (__any(has1 && old1)) {       // rare: loaded on demand
                             const int64_t a1 = has1 && old1 ? s1 : 0;
                             const bool r1 = (a.rm[a1 * W + vwj] >> bit) & 1u;
-                            ro = a.finish[a1 * V + vs_] + (r1 ? 0 : a.gap[a1]);
+                            ro = TM::add(TM::from_time(a.finish[a1 * V + vs_]), r1 ? 0 : wt(a.gap[a1]));
                         }
                         const int64_t rel = old1 ? ro : sR[i1 * VS + os];
                         const bool on = has1 && (all_on || cls_on(eo, c1));
-                        X = on ? max64(X, rel) : X;
+                        X = on ? TM::mx(X, rel) : X;
                     }
-                    if (tcar) X = head ? max64(X, tcv) : X;
+                    if (tcar) X = head ? TM::mx(X, tcv) : X;
                     if (__any(extra != 0u)) {
                         // rare: wide fan-in.  The wave's lanes share each such
                         // position's gathers beyond two (64 per pass, loads of
@@ -558,21 +617,22 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                                     if (sp < prev_r0) {
                                         const int64_t sx = a.gat_src[e];
                                         const bool rs = (a.rm[sx * W + vwj] >> bit) & 1u;
-                                        rel = a.finish[sx * V + vs_] + (rs ? 0 : a.gat_gap[e]);
+                                        rel = TM::add(TM::from_time(a.finish[sx * V + vs_]),
+                                                      rs ? 0 : wt(a.gat_gap[e]));
                                     } else {
                                         rel = sR[(sp - prev_r0) * VS + os];
                                     }
-                                    if (cls_on(eo, c)) mx = max64(mx, rel);
+                                    if (cls_on(eo, c)) mx = TM::mx(mx, rel);
                                 }
                             }
+                            // (bit patterns of nonnegative doubles order as integers)
                             mx = wave_max64(mx);
-                            if (lane == ld) X = max64(X, mx);
+                            if (lane == ld) X = TM::mx(X, mx);
                         }
                     }
                     int64_t dp;
                     if (UNI) {
-                        const uint64_t te = tev;
-                        dp = (int64_t)(((uint64_t)(uint32_t)dur * (uint32_t)te) >> ((uint32_t)(te >> 32) & 0xff));
+                        dp = TM::i(__builtin_floor((double)(uint32_t)dur * TM::d((int64_t)tev)));
                     } else if (TLDS) {
                         const uint64_t te = tev;
                         if (shift_only) {
@@ -587,20 +647,20 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     dp = live ? dp : 0;
                     const int64_t gp = live ? gap : 0;
                     // one position per lane: c -> max(c + A, B), a run head
-                    // written with kHead; the round's first position takes
-                    // the carry (no effect on a head)
-                    int64_t sa = ok ? (head ? kHead : dp + gp) : 0;
-                    int64_t sb = ok ? X + dp + gp : 0;
-                    if (q == 0 && ok) sb = max64(crv + sa, sb);
-                    wave_scan(sa, sb);
+                    // written with the head value; the round's first
+                    // position takes the carry (no effect on a head)
+                    int64_t sa = ok ? (head ? TM::head : TM::add(dp, gp)) : 0;
+                    int64_t sb = ok ? TM::add(TM::add(X, dp), gp) : 0;
+                    if (q == 0 && ok) sb = TM::mx(TM::add(crv, sa), sb);
+                    wave_scan<UNI>(sa, sb);
                     const int64_t Rv = sb;
-                    F = Rv - gp;
-                    S = F - dp;
+                    F = TM::sub(Rv, gp);
+                    S = TM::sub(F, dp);
                     if (ok) sR[q * VS + os] = Rv;
                     if (ok && tcar && (flags & 2u)) sTC[tcx + os] = Rv;
                     if (ok && !rmv) {
-                        if (jj == 0) msS0 = max64(msS0, F);
-                        else msS1 = max64(msS1, F);
+                        if (jj == 0) msS0 = TM::mx(msS0, F);
+                        else msS1 = TM::mx(msS1, F);
                     }
                     st = ok;
                 }
@@ -616,11 +676,11 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 const int64_t vs_ = vw_ok ? v0 + os : 0;
                 gi64 *o = sts[jj] ? (gi64 *)(a.finish + ((int64_t)node * V + vs_)) : dummy;
                 asm volatile("" : "+v"(o));  // one unconditional store per slot
-                *o = Fs[jj];
+                *o = TM::to_time(Fs[jj]);
                 if (START) {
                     gi64 *os2 = sts[jj] ? (gi64 *)(a.start + ((int64_t)node * V + vs_)) : dummy;
                     asm volatile("" : "+v"(os2));
-                    *os2 = Ss[jj];
+                    *os2 = TM::to_time(Ss[jj]);
                 }
             }
             DN = DNs;
@@ -645,12 +705,14 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
 #pragma unroll
         for (int j = 0; j < VPL; j++) { A[j] = 0; B[j] = 0; }
         // high word added to a position's finish before the makespan max:
-        // kHead for positions not kept (removed, or past the round's end)
+        // that of the head value for positions not kept (removed, or past
+        // the round's end; its low word is 0)
+        constexpr uint32_t kNk = (uint32_t)((uint64_t)TM::head >> 32);
         uint32_t nkh[K][VPL];
 #pragma unroll
         for (int i = 0; i < K; i++)
 #pragma unroll
-            for (int j = 0; j < VPL; j++) nkh[i][j] = (uint32_t)((uint64_t)kHead >> 32);
+            for (int j = 0; j < VPL; j++) nkh[i][j] = kNk;
         Dyn<K, VPL> DNb;
         constexpr bool NEXT_BIG = !decltype(next_small_tag)::value;
         {
@@ -665,7 +727,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
                 const int4 w0 = r4[0], w1 = r4[1], w2 = r4[2];
                 const int64_t dur = ((int64_t)(uint32_t)w0.y << 32) | (uint32_t)w0.x;
-                const int64_t gap = UNI ? (int64_t)(uint32_t)w0.z
+                const int64_t gap = UNI ? TM::w32((uint32_t)w0.z)
                                     : (((int64_t)(uint32_t)w0.w << 32) | (uint32_t)w0.z);
                 const int32_t node = w1.x, s0 = w1.y, s1 = w1.z, p0 = w1.w, p1 = w2.x;
                 // positions past the round's end hold stale LDS: nothing read
@@ -694,20 +756,21 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 // wave-uniform decision below is taken once for all VPL variants
                 int64_t X[VPL];
 #pragma unroll
-                for (int j = 0; j < VPL; j++) X[j] = 0;
+                for (int j = 0; j < VPL; j++) X[j] = TM::zero;
                 if (any0) {
                     Vals<VPL> yn = *reinterpret_cast<const Vals<VPL> *>(&sR[i0 * VS + o0]);
                     // read on every lane: the choice below stays a select
                     // instead of a branch that sinks half of the read
 #pragma unroll
                     for (int j = 0; j < VPL; j++) asm volatile("" : "+v"(yn.x[j]));
-                    const int64_t g0g = UNI ? (int64_t)(uint32_t)w2.w : D.g0gap[i];
+                    const int64_t g0g = UNI ? TM::w32((uint32_t)w2.w) : D.g0gap[i];
 #pragma unroll
                     for (int j = 0; j < VPL; j++) {
-                        const int64_t ro = D.f0[i].x[j] + (((D.r0w[i] >> (vsh + j)) & 1u) ? 0 : g0g);
+                        const int64_t ro = TM::add(TM::from_time(D.f0[i].x[j]),
+                                                   ((D.r0w[i] >> (vsh + j)) & 1u) ? 0 : g0g);
                         const int64_t rel = old0 ? ro : yn.x[j];
                         const bool on = has0 && (all_on || cls_on(eon[j], c0));
-                        X[j] = on ? rel : 0;
+                        X[j] = on ? rel : TM::zero;
                     }
                 }
                 if (any1) {
@@ -719,20 +782,21 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                         const Vals<VPL> f1 = *reinterpret_cast<const Vals<VPL> *>(a.finish + a1 * V + vvf);
 #pragma unroll
                         for (int j = 0; j < VPL; j++)
-                            ro.x[j] = f1.x[j] + (((r1w >> (vsh + j)) & 1u) ? 0 : g1);
+                            ro.x[j] = TM::add(TM::from_time(f1.x[j]),
+                                              ((r1w >> (vsh + j)) & 1u) ? 0 : wt(g1));
                     }
                     const Vals<VPL> yn = *reinterpret_cast<const Vals<VPL> *>(&sR[i1 * VS + o0]);
 #pragma unroll
                     for (int j = 0; j < VPL; j++) {
                         const int64_t rel = old1 ? ro.x[j] : yn.x[j];
                         const bool on = has1 && (all_on || cls_on(eon[j], c1));
-                        X[j] = on ? max64(X[j], rel) : X[j];
+                        X[j] = on ? TM::mx(X[j], rel) : X[j];
                     }
                 }
                 if (tcar && anyh) {                            // previous task of the thread
                     const Vals<VPL> tc = *reinterpret_cast<const Vals<VPL> *>(&sTC[tcx]);
 #pragma unroll
-                    for (int j = 0; j < VPL; j++) X[j] = head ? max64(X[j], tc.x[j]) : X[j];
+                    for (int j = 0; j < VPL; j++) X[j] = head ? TM::mx(X[j], tc.x[j]) : X[j];
                 }
                 if (__any(extra != 0u)) {
                     // rare: wide fan-in.  For each slot with such a position,
@@ -762,29 +826,31 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                                     const Vals<VPL> fx = *reinterpret_cast<const Vals<VPL> *>(a.finish + sx * V + vvf);
 #pragma unroll
                                     for (int j = 0; j < VPL; j++)
-                                        rel.x[j] = fx.x[j] + (((rw >> (vsh + j)) & 1u) ? 0 : gg);
+                                        rel.x[j] = TM::add(TM::from_time(fx.x[j]),
+                                                           ((rw >> (vsh + j)) & 1u) ? 0 : wt(gg));
                                 } else {
                                     rel = *reinterpret_cast<const Vals<VPL> *>(&sR[(sp - prev_r0) * VS + o0]);
                                 }
 #pragma unroll
                                 for (int j = 0; j < VPL; j++)
-                                    if (cls_on(eon[j], c)) mx[j] = max64(mx[j], rel.x[j]);
+                                    if (cls_on(eon[j], c)) mx[j] = TM::mx(mx[j], rel.x[j]);
                             }
                         }
+                        // (bit patterns of nonnegative doubles order as integers)
                         for (int o = LPS; o < 64; o <<= 1) {
 #pragma unroll
                             for (int j = 0; j < VPL; j++) mx[j] = max64(mx[j], shfl_xor64(mx[j], o));
                         }
                         if (lane / LPS == ld / LPS) {
 #pragma unroll
-                            for (int j = 0; j < VPL; j++) X[j] = max64(X[j], mx[j]);
+                            for (int j = 0; j < VPL; j++) X[j] = TM::mx(X[j], mx[j]);
                         }
                     }
                 }
                 if (anyh) {                                    // a run starts: reset the fold
 #pragma unroll
                     for (int j = 0; j < VPL; j++) {
-                        A[j] = head ? kHead : A[j];            // the carry no longer reaches it
+                        A[j] = head ? TM::head : A[j];          // the carry no longer reaches it
                         B[j] = head ? 0 : B[j];
                     }
                 }
@@ -795,8 +861,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     int64_t dp;
                     if (UNI) {
                         const uint64_t te = sT[cls * VS + o0 + j];
-                        const uint32_t pm = live ? (uint32_t)te : 0u;   // removed: zero duration
-                        dp = (int64_t)(((uint64_t)(uint32_t)dur * pm) >> ((uint32_t)(te >> 32) & 0xff));
+                        const uint32_t du = live ? (uint32_t)dur : 0u;   // removed: zero duration
+                        dp = TM::i(__builtin_floor((double)du * TM::d((int64_t)te)));
                     } else if (TLDS) {
                         const uint64_t te = sT[cls * VS + o0 + j];
                         if (shift_only) {
@@ -809,14 +875,14 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     }
                     if (!UNI) dp = live ? dp : 0;
                     const int64_t gp = live ? gap : 0;
-                    const int64_t F = max64(B[j], X[j]) + dp;
-                    Dp[i][j] = A[j] + dp;
-                    A[j] += dp + gp;
-                    B[j] = F + gp;
+                    const int64_t F = TM::add(TM::mx(B[j], X[j]), dp);
+                    Dp[i][j] = TM::add(A[j], dp);
+                    A[j] = TM::add(Dp[i][j], gp);
+                    B[j] = TM::add(F, gp);
                     Fl[i][j] = F;
                     if (START) Dd[i][j] = dp;
                     Gp[i][j] = gp;
-                    nkh[i][j] = live ? 0u : (uint32_t)((uint64_t)kHead >> 32);
+                    nkh[i][j] = live ? 0u : kNk;
                 }
             }
         }
@@ -828,8 +894,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
 #pragma unroll
         for (int j = 0; j < VPL; j++) {
             const int e = (o0 + j) * NSP + slot;
-            sA[e] = slot == 0 ? kHead : A[j];
-            sB[e] = slot == 0 ? max64(carry[j] + A[j], B[j]) : B[j];
+            sA[e] = slot == 0 ? TM::head : A[j];
+            sB[e] = slot == 0 ? TM::mx(TM::add(carry[j], A[j]), B[j]) : B[j];
         }
         __syncthreads();                                     // B1
         // inclusive scan of slot summaries per variant: DPP within the wave,
@@ -850,15 +916,15 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             for (int m = 0; m < VPL; m++) {
                 ta[m] = sA[e0 + m];
                 tb[m] = sB[e0 + m];
-                if (m > 0) compose(ta[m - 1], tb[m - 1], ta[m], tb[m]);
+                if (m > 0) compose<UNI>(ta[m - 1], tb[m - 1], ta[m], tb[m]);
             }
             int64_t pa = ta[VPL - 1], pb = tb[VPL - 1];
-            wave_scan(pa, pb);
+            wave_scan<UNI>(pa, pb);
             const int qlo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)pb, 0x138, 0xf, 0xf, true);   // wave_shr:1
             const int qhi = __builtin_amdgcn_update_dpp(0, (int)((uint64_t)pb >> 32), 0x138, 0xf, 0xf, true);
             const int64_t qb = join64(qlo, qhi);
 #pragma unroll
-            for (int m = 0; m < VPL; m++) sB[e0 + m] = max64(qb + ta[m], tb[m]);
+            for (int m = 0; m < VPL; m++) sB[e0 + m] = TM::mx(TM::add(qb, ta[m]), tb[m]);
         } else if (NS <= 64 * VPL) {
             // a wave scans whole variants (its VPL chunks hold them): the
             // chunks of one variant follow each other in the same wave
@@ -870,9 +936,9 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 xa[j] = 0; xb[j] = 0;
                 if (cact[j]) {
                     xa[j] = sA[e]; xb[j] = sB[e];
-                    wave_scan(xa[j], xb[j]);
+                    wave_scan<UNI>(xa[j], xb[j]);
                     // after the last chunk (a variant's first slot is a head)
-                    if (j > 0) compose(pa, pb, xa[j], xb[j]);
+                    if (j > 0) compose<UNI>(pa, pb, xa[j], xb[j]);
                     sB[e] = xb[j];
                 }
                 pa = readlane64(xa[j], 63);
@@ -886,7 +952,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 xa[j] = 0; xb[j] = 0;
                 if (cact[j]) {
                     xa[j] = sA[e]; xb[j] = sB[e];
-                    wave_scan(xa[j], xb[j]);
+                    wave_scan<UNI>(xa[j], xb[j]);
                 }
             }
 #pragma unroll
@@ -904,10 +970,10 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     int64_t qa = sTA[first], qb = sTB[first];
                     for (int c = 1; c < chunk; c++) {
                         int64_t ca = sTA[first + c], cb = sTB[first + c];
-                        compose(qa, qb, ca, cb);
+                        compose<UNI>(qa, qb, ca, cb);
                         qa = ca; qb = cb;
                     }
-                    compose(qa, qb, xa[j], xb[j]);
+                    compose<UNI>(qa, qb, xa[j], xb[j]);
                 }
             }
 #pragma unroll
@@ -944,13 +1010,17 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
 #pragma unroll
                 for (int j = 0; j < VPL; j++) {
                     // positions after a run head hold Dp <= kHead + weights: no effect
-                    const int64_t F = max64(cin[j] + Dp[i][j], Fl[i][j]);
-                    rv.x[j] = F + Gp[i][j];
-                    fv.x[j] = F;
-                    if (START) sv.x[j] = F - Dd[i][j];
+                    const int64_t F = TM::mx(TM::add(cin[j], Dp[i][j]), Fl[i][j]);
+                    rv.x[j] = TM::add(F, Gp[i][j]);
+                    fv.x[j] = TM::to_time(F);
+                    if (START) sv.x[j] = TM::to_time(TM::sub(F, Dd[i][j]));
                     // makespan over kept tasks (lanes past V never publish theirs)
                     // (positions past ke were not walked: no finish to take)
-                    if (i < ke) ms[j] = max64(ms[j], (int64_t)((uint64_t)F + ((uint64_t)nkh[i][j] << 32)));
+                    if (i < ke) {
+                        const int64_t nk = (int64_t)((uint64_t)nkh[i][j] << 32);
+                        if (UNI) ms[j] = TM::mx(ms[j], TM::add(F, nk));
+                        else ms[j] = max64(ms[j], (int64_t)((uint64_t)F + (uint64_t)nk));
+                    }
                 }
                 // positions past the round's end write their own unused slot
                 // (no young gather reads it); slots past ke would overlap the
@@ -999,7 +1069,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
     if (wv < VS) atomicMax(&sMs[wv], (unsigned long long)msS0);
     if (PS > 1 && wv + NW < VS) atomicMax(&sMs[wv + NW], (unsigned long long)msS1);
     __syncthreads();
-    if (tid < VS && v0 + tid < a.V) a.makespan[v0 + tid] = (int64_t)sMs[tid];
+    // (bit patterns of nonnegative doubles order as integers)
+    if (tid < VS && v0 + tid < a.V) a.makespan[v0 + tid] = TM::to_time((int64_t)sMs[tid]);
 }
 
 // Removal bits per schedule position for each workgroup's VS variants:
@@ -1195,9 +1266,11 @@ hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants
     const int64_t *nrp = cnt + ns;
     const bool tl = table_fits<LPS, VPL, K, NT>(var->n_cls);
     // uniform: every gather class on in every variant, shift-only scales,
-    // durations and gaps below 2^32 (a source's gap then rides in its record)
+    // durations and gaps below 2^32 (a source's gap then rides in its
+    // record), times within the bounds of the double arithmetic
     const bool uni = tl && (var->all_mask & cls_mask) == cls_mask && !var->any_magic &&
-                     g->dmax < (int64_t(1) << 32) && g->gmax < (int64_t(1) << 32);
+                     g->dmax < (int64_t(1) << 32) && g->gmax < (int64_t(1) << 32) &&
+                     var->f64_ok;
     const Rec *rc = sch->rec;
     if (e == hipSuccess) {
         if (uni && start) launch_one<LPS, VPL, K, true, true, true, NT>(grid, s, r0, rn, nrp, rc, args);

@@ -171,11 +171,12 @@ def bench_policy(stream, reps, cpu_workers):
 
 
 def kernel_source_digest():
-    """sha256 over the sources the simulation kernel is compiled from."""
+    """sha256 over the sources the simulation kernel is compiled from and
+    the build script (it holds the kernel's compile flags)."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("k_simulate.hip", "dd_internal.h", "dd_common.h"):
-        with open(os.path.join(ROOT, "paper_2006_03318_amd", "csrc", f), "rb") as fh:
+    for f in ("csrc/k_simulate.hip", "csrc/dd_internal.h", "csrc/dd_common.h", "build.py"):
+        with open(os.path.join(ROOT, "paper_2006_03318_amd", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
 

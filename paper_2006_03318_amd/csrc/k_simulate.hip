@@ -370,17 +370,27 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
     // before the round that issues these loads)
     // (the layout is a compile-time choice: with a run-time branch between the
     // two layouts, the compiler would make each wait for the other's loads)
+    // word k of the record of position q in ring buffer b (indexing the LDS
+    // array keeps the address arithmetic in 32 bits)
+    auto rec_w = [&](int b, int q, int k) -> int4 {
+        const uint4 u = sRec[b][q * 3 + k];
+        return make_int4((int)u.x, (int)u.y, (int)u.z, (int)u.w);
+    };
+    // offset of row `row` (nonnegative, 32 bits) of a row-major array
+    // `width` wide: one 32x32 -> 64 multiply
+    auto rowoff = [](int64_t row, int64_t width) -> int64_t {
+        return (int64_t)((uint64_t)(uint32_t)row * (uint64_t)(uint32_t)width);
+    };
     auto issue = [&](auto small_tag, int rn, int b, int prev_r0, Dyn<K, VPL> &d) {
         constexpr bool SMALL_LAYOUT = decltype(small_tag)::value;
         const int ke = per_slot(rn);
-        const Rec *R = reinterpret_cast<const Rec *>(sRec[b]);
         if constexpr (SMALL_LAYOUT) {
             // small layout: position = lane; slot jj of the load registers
             // holds variant w + 8 jj of this wave
             const int q = lane;
             const bool ok = q < rn;
-            const int4 w1 = reinterpret_cast<const int4 *>(&R[q])[1];
-            const bool n0 = ok && w1.y >= 0 && w1.w < prev_r0;
+            const int4 w1 = rec_w(b, q, 1);
+            const bool n0 = ok & (w1.y >= 0) & (w1.w < prev_r0);
             const int64_t a0 = n0 ? w1.y : 0;
 #pragma unroll
             for (int jj = 0; jj < K; jj++) {
@@ -398,8 +408,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                     // issued on every path (row 0 when unused): with a known
                     // count of loads, the ring refill waits for the record
                     // loads only
-                    f.x[0] = a.finish[a0 * V + vs_];
-                    r0 = a.rm[a0 * W + vwj];
+                    f.x[0] = a.finish[rowoff(a0, V) + vs_];
+                    r0 = a.rm[rowoff(a0, W) + vwj];
                     if (!UNI) gg = a.gap[a0];
                 }
                 d.f0[jj] = f;
@@ -411,12 +421,12 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             for (int i = 0; i < K; i++) {
                 const int q = slot * ke + i;
                 const bool ok = i < ke && q < rn;
-                const int4 w1 = reinterpret_cast<const int4 *>(&R[q])[1];   // node, g0_src, g1_src, g0_spos
-                const bool n0 = ok && w1.y >= 0 && w1.w < prev_r0;
+                const int4 w1 = rec_w(b, q, 1);   // node, g0_src, g1_src, g0_spos
+                const bool n0 = ok & (w1.y >= 0) & (w1.w < prev_r0);
                 const int64_t a0 = n0 ? w1.y : 0;
                 // issued on every path (row 0 when unused), like the small layout
-                const Vals<VPL> f = *reinterpret_cast<const Vals<VPL> *>(a.finish + a0 * V + vvf);
-                const uint32_t r0 = a.rm[a0 * W + vw];
+                const Vals<VPL> f = *reinterpret_cast<const Vals<VPL> *>(a.finish + rowoff(a0, V) + vvf);
+                const uint32_t r0 = a.rm[rowoff(a0, W) + vw];
                 const int64_t gg = UNI ? 0 : a.gap[a0];
                 d.f0[i] = f;
                 d.r0w[i] = r0;
@@ -425,16 +435,15 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         }
     };
     // one position of the big layout (issue() does all K of them)
-    auto issue_big_at = [&](int rn, int b, int prev_r0, Dyn<K, VPL> &d, int i) {
-        const Rec *R = reinterpret_cast<const Rec *>(sRec[b]);
-        const int ke = per_slot(rn);
-        const int q = slot * ke + i;
+    // (qs = slot * positions per slot of that round)
+    auto issue_big_at = [&](int rn, int ke, int qs, int b, int prev_r0, Dyn<K, VPL> &d, int i) {
+        const int q = qs + i;
         const bool ok = i < ke && q < rn;
-        const int4 w1 = reinterpret_cast<const int4 *>(&R[q])[1];
-        const bool n0 = ok && w1.y >= 0 && w1.w < prev_r0;
+        const int4 w1 = rec_w(b, q, 1);
+        const bool n0 = ok & (w1.y >= 0) & (w1.w < prev_r0);
         const int64_t a0 = n0 ? w1.y : 0;
-        const Vals<VPL> f = *reinterpret_cast<const Vals<VPL> *>(a.finish + a0 * V + vvf);
-        const uint32_t r0 = a.rm[a0 * W + vw];
+        const Vals<VPL> f = *reinterpret_cast<const Vals<VPL> *>(a.finish + rowoff(a0, V) + vvf);
+        const uint32_t r0 = a.rm[rowoff(a0, W) + vw];
         const int64_t gg = UNI ? 0 : a.gap[a0];
         d.f0[i] = f;
         d.r0w[i] = r0;
@@ -485,7 +494,6 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         const int r0 = m0r0, rn = m0rn;
         int m4r0, m4rn;                           // round k+4, used from the next round on
         if (nr > 0) rmeta(k + 4, m4r0, m4rn);
-        const Rec *R = reinterpret_cast<const Rec *>(sRec[b0]);
         uint64_t eon[VPL];
 #pragma unroll
         for (int j = 0; j < VPL; j++) eon[j] = sEon[o0 + j];
@@ -534,8 +542,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             issue(next_small_tag, rn1, bN, r0, DNs);
             const int q = lane;
             const bool ok = q < rn;
-            const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
-            const int4 w0 = r4[0], w1 = r4[1], w2 = r4[2];
+            const int4 w0 = rec_w(b0, q, 0), w1 = rec_w(b0, q, 1), w2 = rec_w(b0, q, 2);
             const int64_t dur = ((int64_t)(uint32_t)w0.y << 32) | (uint32_t)w0.x;
             const int64_t gap = UNI ? TM::w32((uint32_t)w0.z)
                                     : (((int64_t)(uint32_t)w0.w << 32) | (uint32_t)w0.z);
@@ -544,7 +551,9 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             const int cls = ok ? (int)(cl & 0xffff) : 0;
             const uint8_t c0 = (cl >> 16) & 0xff, c1 = cl >> 24;
             const uint32_t flags = ok ? (uint32_t)w2.z : 0u;
-            const uint32_t rb = ok ? (uint32_t)sRm[b0][q] : 0u;   // removal bits of the task
+            uint32_t rbq = sRm[b0][q];            // read on every lane: a select, not a masked read
+            asm volatile("" : "+v"(rbq));
+            const uint32_t rb = ok ? rbq : 0u;    // removal bits of the task
             const bool head = flags & 1u;
             const bool old0 = p0 < prev_r0, old1 = p1 < prev_r0;
             int i0 = p0 - prev_r0, i1 = p1 - prev_r0;
@@ -674,11 +683,18 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 const int os = wv + NW * jj;
                 const bool vw_ok = os < VS && v0 + os < a.V;
                 const int64_t vs_ = vw_ok ? v0 + os : 0;
-                gi64 *o = sts[jj] ? (gi64 *)(a.finish + ((int64_t)node * V + vs_)) : dummy;
+                // formed on every lane (lanes past the round's end store to
+                // the dummy), so the choice is a select
+                const int64_t off = rowoff(node, V) + vs_;
+                gi64 *oa = (gi64 *)(a.finish + off);
+                asm volatile("" : "+v"(oa));
+                gi64 *o = sts[jj] ? oa : dummy;
                 asm volatile("" : "+v"(o));  // one unconditional store per slot
                 *o = TM::to_time(Fs[jj]);
                 if (START) {
-                    gi64 *os2 = sts[jj] ? (gi64 *)(a.start + ((int64_t)node * V + vs_)) : dummy;
+                    gi64 *osa = (gi64 *)(a.start + off);
+                    asm volatile("" : "+v"(osa));
+                    gi64 *os2 = sts[jj] ? osa : dummy;
                     asm volatile("" : "+v"(os2));
                     *os2 = TM::to_time(Ss[jj]);
                 }
@@ -715,17 +731,17 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             for (int j = 0; j < VPL; j++) nkh[i][j] = kNk;
         Dyn<K, VPL> DNb;
         constexpr bool NEXT_BIG = !decltype(next_small_tag)::value;
+        const int ke1 = per_slot(rn1), qs1 = slot * ke1;   // next round's layout
         {
 #pragma unroll
             for (int i = 0; i < K; i++) {
                 // a big next round's loads go out position by position, between
                 // this round's positions
-                if (NEXT_BIG && i > 0) issue_big_at(rn1, bN, r0, DNb, i - 1);
+                if (NEXT_BIG && i > 0) issue_big_at(rn1, ke1, qs1, bN, r0, DNb, i - 1);
                 if (!wact || i >= ke) continue;
                 const int q = slot * ke + i;
                 const bool ok = q < rn;
-                const int4 *r4 = reinterpret_cast<const int4 *>(&R[q]);
-                const int4 w0 = r4[0], w1 = r4[1], w2 = r4[2];
+                const int4 w0 = rec_w(b0, q, 0), w1 = rec_w(b0, q, 1), w2 = rec_w(b0, q, 2);
                 const int64_t dur = ((int64_t)(uint32_t)w0.y << 32) | (uint32_t)w0.x;
                 const int64_t gap = UNI ? TM::w32((uint32_t)w0.z)
                                     : (((int64_t)(uint32_t)w0.w << 32) | (uint32_t)w0.z);
@@ -736,7 +752,9 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 const int cls = ok ? (int)(cl & 0xffff) : 0;
                 const uint8_t c0 = (cl >> 16) & 0xff, c1 = cl >> 24;
                 const uint32_t flags = ok ? (uint32_t)w2.z : 0u;
-                const uint32_t rb = ok ? (uint32_t)sRm[b0][q] : 0u;   // removal bits of the task
+                uint32_t rbq = sRm[b0][q];        // read on every lane: a select, not a masked read
+                asm volatile("" : "+v"(rbq));
+                const uint32_t rb = ok ? rbq : 0u;   // removal bits of the task
                 const bool head = flags & 1u;
                 U[i] = node;
                 FLk[i] = flags;
@@ -886,7 +904,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 }
             }
         }
-        if constexpr (NEXT_BIG) issue_big_at(rn1, bN, r0, DNb, K - 1);
+        if constexpr (NEXT_BIG) issue_big_at(rn1, ke1, qs1, bN, r0, DNb, K - 1);
         else issue(next_small_tag, rn1, bN, r0, DNb);
         put_next();
         // slot summaries (variant-major); slot 0 absorbs the carry and
@@ -1026,14 +1044,24 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 // (no young gather reads it); slots past ke would overlap the
                 // next slot's positions
                 if (i < ke) *reinterpret_cast<Vals<VPL> *>(&sR[q * VS + o0]) = rv;
-                if (anylast && last) *reinterpret_cast<Vals<VPL> *>(&sTC[tcx]) = rv;
+                if (__builtin_expect(anylast, 0)) {            // wave-uniform: mostly skipped
+                    if (last) *reinterpret_cast<Vals<VPL> *>(&sTC[tcx]) = rv;
+                }
             }
+            // the result address is formed on every lane (an address that
+            // no lane stores to is never used), so the choice of the dummy
+            // target is a select rather than a masked block
             const bool st = ok && lok;
-            gi64 *o = st ? (gi64 *)(a.finish + ((int64_t)U[i] * V + vf)) : dummy;
+            const int64_t off = rowoff(U[i], V) + vf;
+            gi64 *oa = (gi64 *)(a.finish + off);
+            asm volatile("" : "+v"(oa));
+            gi64 *o = st ? oa : dummy;
             asm volatile("" : "+v"(o));      // keep one unconditional global store
             store_vals(o, fv);
             if (START) {
-                gi64 *os = st ? (gi64 *)(a.start + ((int64_t)U[i] * V + vf)) : dummy;
+                gi64 *osa = (gi64 *)(a.start + off);
+                asm volatile("" : "+v"(osa));
+                gi64 *os = st ? osa : dummy;
                 asm volatile("" : "+v"(os));
                 store_vals(os, sv);
             }

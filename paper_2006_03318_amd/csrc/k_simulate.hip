@@ -370,10 +370,15 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
     // before the round that issues these loads)
     // (the layout is a compile-time choice: with a run-time branch between the
     // two layouts, the compiler would make each wait for the other's loads)
-    // word k of the record of position q in ring buffer b (indexing the LDS
-    // array keeps the address arithmetic in 32 bits)
+    // word k of the record of position q in ring buffer b: the address is
+    // formed in 32 bits, and the masks (q < RP, b < 3) let the compiler use
+    // full-rate 24-bit multiplies; as pointer arithmetic it became a
+    // quarter-rate 64-bit multiply-add
+    typedef __attribute__((address_space(3))) const u32x4 lds_u4;
+    lds_u4 *const ring = (lds_u4 *)&sRec[0][0];
     auto rec_w = [&](int b, int q, int k) -> int4 {
-        const uint4 u = sRec[b][q * 3 + k];
+        const uint32_t idx = ((uint32_t)b & 3u) * (uint32_t)RW + ((uint32_t)q & 0xffffu) * 3u + (uint32_t)k;
+        const u32x4 u = ring[idx];
         return make_int4((int)u.x, (int)u.y, (int)u.z, (int)u.w);
     };
     // offset of row `row` (nonnegative, 32 bits) of a row-major array
@@ -731,7 +736,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
             for (int j = 0; j < VPL; j++) nkh[i][j] = kNk;
         Dyn<K, VPL> DNb;
         constexpr bool NEXT_BIG = !decltype(next_small_tag)::value;
-        const int ke1 = per_slot(rn1), qs1 = slot * ke1;   // next round's layout
+        const int ke1 = per_slot(rn1);                      // next round's layout
+        const int qs1 = (int)(((uint32_t)slot & 0xffffu) * ((uint32_t)ke1 & 0xffu));
         {
 #pragma unroll
             for (int i = 0; i < K; i++) {

@@ -561,8 +561,8 @@ dd_status dd_runtime_breakdown(const dd_graph *g, const dd_variants *var, const 
     int64_t *scratch = nullptr;
     int32_t *order = nullptr;
     TRY(copy_in(&d_role, role, (size_t)g->n, s), "copy role");
-    TRY(dd::dalloc_n(&scratch, 2 * (size_t)var->V + (size_t)var->n_cls + 1, s), "alloc");
-    TRY(dd::dalloc_n(&order, (size_t)g->n + 1, s), "alloc");
+    TRY(dd::dalloc_n(&scratch, 2 * (size_t)var->V + (size_t)var->n_cls + 2, s), "alloc");
+    TRY(dd::dalloc_n(&order, 2 * (size_t)g->n + 1, s), "alloc");
     TRY(dd::launch_breakdown(g, var, d_role, d_finish, d_makespan, scratch, order, d_out, s),
         "breakdown");
     TRY(dd::note_use(g->uses, g->stream, s), "record stream use");

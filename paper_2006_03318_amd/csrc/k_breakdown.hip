@@ -32,10 +32,6 @@ constexpr int kVL = 4;            // variants per thread (divides 32)
 constexpr int64_t kChunk = 512;   // ordered tasks per workgroup
 constexpr int kBatch = 8;         // tasks whose loads are issued together
 
-__device__ __forceinline__ int64_t bd_scaled(int64_t d, const ScaleEntry &se) {
-    const uint64_t a = (uint64_t)d * (uint64_t)se.p;
-    return (int64_t)(se.magic ? (__umul64hi(a, se.magic) >> se.shift) : (a >> se.shift));
-}
 
 __device__ __forceinline__ bool has_role(uint8_t r) { return r == 1u || r == 2u; }
 
@@ -98,9 +94,21 @@ struct BdArgs {
     unsigned long long *acc;      // [2][V]: kernel time, blocked time
 };
 
+// scaled duration: MAGIC when some q of the launch is not a power of two
+// (else a shift suffices), D32 when every duration is below 2^32 (one 32x32
+// multiply); the multiply-high of the general form is four quarter-rate
+// multiplies, which bound the kernel when taken for every (task, variant)
+template <bool MAGIC, bool D32>
+__device__ __forceinline__ int64_t bd_scale(int64_t d, const ScaleEntry &se) {
+    const uint64_t a = D32 ? (uint64_t)(uint32_t)d * (uint64_t)se.p : (uint64_t)d * (uint64_t)se.p;
+    if (MAGIC && se.magic) return (int64_t)(__umul64hi(a, se.magic) >> se.shift);
+    return (int64_t)(a >> se.shift);
+}
+
 // per-task arrays are kernel arguments marked restrict, so the compiler
 // reads them with scalar loads (every lane of the workgroup needs the same
 // task's fields)
+template <bool MAGIC, bool D32>
 __global__ __launch_bounds__(kBT) void k_bd_accum(const int64_t *__restrict__ m_ptr,
                                                   const int32_t *__restrict__ order,
                                                   const uint8_t *__restrict__ role,
@@ -162,37 +170,72 @@ __global__ __launch_bounds__(kBT) void k_bd_accum(const int64_t *__restrict__ m_
 #pragma unroll
         for (int j = 0; j < kBatch; j++) {
             if (ib + j >= i1) break;               // past the chunk's end (wave-uniform)
-            const int64_t u = uu[j];
             if (cc[j] != ccls) {                   // wave-uniform: the class changed
 #pragma unroll
                 for (int t = 0; t < kVL; t++) se[t] = a.table[(int64_t)cc[j] * V + vc[t]];
                 ccls = cc[j];
             }
-            int64_t dp[kVL];
+            if (rr[j] != 1u) continue;             // waiting calls: k_bd_wait
 #pragma unroll
-            for (int t = 0; t < kVL; t++) dp[t] = ((rw[j] >> t) & 1u) ? 0 : bd_scaled(dd[j], se[t]);
-            if (rr[j] == 1u) {
-#pragma unroll
-                for (int t = 0; t < kVL; t++) ksum[t] += dp[t];
-                continue;
-            }
-            const int32_t p = tprev[u];
-            const uint32_t rp = p >= 0 ? a.rm[(int64_t)p * W + vw] >> vsh : 0u;
-#pragma unroll
-            for (int t = 0; t < kVL; t++) {
-                const int64_t start = a.finish[u * V + vc[t]] - dp[t];
-                const int64_t reached =
-                    p >= 0 ? a.finish[(int64_t)p * V + vc[t]] + (((rp >> t) & 1u) ? 0 : gap[p]) : 0;
-                wsum[t] += start - reached;
-            }
+            for (int t = 0; t < kVL; t++)
+                ksum[t] += ((rw[j] >> t) & 1u) ? 0 : bd_scale<MAGIC, D32>(dd[j], se[t]);
         }
     }
 #pragma unroll
-    for (int t = 0; t < kVL; t++) {
-        if (!ok[t]) continue;
-        if (ksum[t]) atomicAdd(&a.acc[vc[t]], (unsigned long long)ksum[t]);
-        if (wsum[t]) atomicAdd(&a.acc[V + vc[t]], (unsigned long long)wsum[t]);
+    for (int t = 0; t < kVL; t++)
+        if (ok[t] && ksum[t]) atomicAdd(&a.acc[vc[t]], (unsigned long long)ksum[t]);
+}
+
+// The waiting calls (a handful per iteration) as a list: one atomic per
+// wave that holds any.
+__global__ __launch_bounds__(kBT) void k_bd_wait_list(int64_t n, const uint8_t *__restrict__ role,
+                                                      unsigned long long *__restrict__ wcount,
+                                                      int32_t *__restrict__ wlist) {
+    const int64_t u = (int64_t)blockIdx.x * kBT + threadIdx.x;
+    const bool w = u < n && role[u] == 2u;
+    const uint64_t bal = __ballot(w);
+    if (!bal) return;
+    const int lane = threadIdx.x & 63;
+    const int first = __ffsll((unsigned long long)bal) - 1;
+    unsigned long long base = 0;
+    if (lane == first) base = atomicAdd(wcount, (unsigned long long)__popcll(bal));
+    base = (unsigned long long)__shfl((long long)base, first, 64);
+    if (w) wlist[base + __popcll(bal & ((1ull << lane) - 1ull))] = (int32_t)u;
+}
+
+// GPU-only time of every waiting call u and variant v: its start minus the
+// moment its thread reached it.  Blocks along x cover the variants (one per
+// thread, so every load and atomic is contiguous across the wave); blocks
+// along y take the calls in turn.  Contributions are nonnegative integers,
+// so the order of the atomics does not change the sums.
+template <bool MAGIC, bool D32>
+__global__ __launch_bounds__(kBT) void k_bd_wait(const unsigned long long *__restrict__ wcount,
+                                                 const int32_t *__restrict__ wlist,
+                                                 const int64_t *__restrict__ dur,
+                                                 const int64_t *__restrict__ gap,
+                                                 const uint16_t *__restrict__ cls,
+                                                 const int32_t *__restrict__ tprev, BdArgs a) {
+    const int64_t V = a.V, W = a.W;
+    const int64_t v = (int64_t)blockIdx.x * kBT + threadIdx.x;
+    if (v >= V) return;
+    const int64_t cnt = (int64_t)*wcount;
+    const int64_t vw = v >> 5;
+    const uint32_t vb = (uint32_t)(v & 31);
+    int64_t sum = 0;
+    for (int64_t i = blockIdx.y; i < cnt; i += gridDim.y) {
+        const int64_t u = wlist[i];
+        const bool rmu = (a.rm[u * W + vw] >> vb) & 1u;
+        const int64_t dp = rmu ? 0 : bd_scale<MAGIC, D32>(dur[u], a.table[(int64_t)cls[u] * V + v]);
+        const int64_t start = a.finish[u * V + v] - dp;
+        const int32_t p = tprev[u];
+        int64_t reached = 0;
+        if (p >= 0) {
+            const bool rmp = (a.rm[(int64_t)p * W + vw] >> vb) & 1u;
+            reached = a.finish[(int64_t)p * V + v] + (rmp ? 0 : gap[p]);
+        }
+        sum += start - reached;
     }
+    if (sum) atomicAdd(&a.acc[V + v], (unsigned long long)sum);
 }
 
 __global__ __launch_bounds__(kBT) void k_bd_final(int32_t V, const int64_t *__restrict__ makespan,
@@ -214,11 +257,15 @@ __global__ __launch_bounds__(kBT) void k_bd_final(int32_t V, const int64_t *__re
 hipError_t launch_breakdown(const dd_graph *g, const dd_variants *var, const uint8_t *role_dev,
                             const int64_t *finish, const int64_t *makespan, int64_t *scratch,
                             int32_t *order, int64_t *out, hipStream_t s) {
-    // scratch: [2][V] accumulators, then [n_cls + 1] class counts / cursors
+    // scratch: [2][V] accumulators, [n_cls + 1] class counts / cursors, the
+    // count of waiting calls; order: [n] tasks with a role by class, then
+    // [n] waiting calls
     unsigned long long *acc = reinterpret_cast<unsigned long long *>(scratch);
     unsigned long long *hist = acc + 2 * (size_t)var->V;
     const int64_t C = var->n_cls;
-    hipError_t e = hipMemsetAsync(scratch, 0, sizeof(int64_t) * (2 * (size_t)var->V + C + 1), s);
+    unsigned long long *wcount = hist + C + 1;
+    int32_t *wlist = order + g->n;
+    hipError_t e = hipMemsetAsync(scratch, 0, sizeof(int64_t) * (2 * (size_t)var->V + C + 2), s);
     if (e != hipSuccess) return e;
     const int64_t n = g->n;
     if (n > 0) {
@@ -237,9 +284,27 @@ hipError_t launch_breakdown(const dd_graph *g, const dd_variants *var, const uin
     const int64_t nch64 = (n + kChunk - 1) / kChunk;
     if (n > 0) {
         BdArgs a{var->V, var->W, nvb, (int32_t)nch64, var->table, var->rm_bits, finish, acc};
-        k_bd_accum<<<(unsigned)(nvb * nch64), kBT, 0, s>>>(
-            reinterpret_cast<const int64_t *>(hist + C), order, role_dev, g->dur, g->gap, g->cls,
-            g->thread_prev, a);
+        const unsigned grid = (unsigned)(nvb * nch64);
+        const int64_t *mp = reinterpret_cast<const int64_t *>(hist + C);
+        const bool d32 = g->dmax < (int64_t(1) << 32);
+        // waiting calls: at most 64 blocks of calls per variant block
+        const dim3 wg((unsigned)((var->V + kBT - 1) / kBT), 64u);
+        k_bd_wait_list<<<grid_for(n, kBT), kBT, 0, s>>>(n, role_dev, wcount, wlist);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        if (var->any_magic && d32) {
+            k_bd_accum<true, true><<<grid, kBT, 0, s>>>(mp, order, role_dev, g->dur, g->gap, g->cls, g->thread_prev, a);
+            k_bd_wait<true, true><<<wg, kBT, 0, s>>>(wcount, wlist, g->dur, g->gap, g->cls, g->thread_prev, a);
+        } else if (var->any_magic) {
+            k_bd_accum<true, false><<<grid, kBT, 0, s>>>(mp, order, role_dev, g->dur, g->gap, g->cls, g->thread_prev, a);
+            k_bd_wait<true, false><<<wg, kBT, 0, s>>>(wcount, wlist, g->dur, g->gap, g->cls, g->thread_prev, a);
+        } else if (d32) {
+            k_bd_accum<false, true><<<grid, kBT, 0, s>>>(mp, order, role_dev, g->dur, g->gap, g->cls, g->thread_prev, a);
+            k_bd_wait<false, true><<<wg, kBT, 0, s>>>(wcount, wlist, g->dur, g->gap, g->cls, g->thread_prev, a);
+        } else {
+            k_bd_accum<false, false><<<grid, kBT, 0, s>>>(mp, order, role_dev, g->dur, g->gap, g->cls, g->thread_prev, a);
+            k_bd_wait<false, false><<<wg, kBT, 0, s>>>(wcount, wlist, g->dur, g->gap, g->cls, g->thread_prev, a);
+        }
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

@@ -64,6 +64,25 @@ def test_breakdown_random(seed):
     assert_equal_arrays("random breakdown", got, want)
 
 
+@pytest.mark.parametrize("qs", [(1, 2, 4, 8), (1, 3, 5, 7)])
+def test_breakdown_long_durations(qs):
+    """Durations up to 2^40 (the 64-bit scaled-duration forms), with scales
+    that shift only and with scales that need the multiply-high; many
+    waiting calls, so the calls' blocks loop."""
+    require_gpu()
+    rng = np.random.default_rng(191_000 + qs[1])
+    g = W.random_graph_sparse(rng, 3000, 4, mean_in=0.5, window=100, n_edge_cls=1, run_len=6)
+    g.dur = rng.integers(0, 1 << 40, size=g.n).astype(np.int64)
+    assert int(g.dur.max()) >= 1 << 32
+    vs = W.random_variants(rng, g, 70, p_remove=0.2, qs=qs)
+    role = rng.integers(0, 3, size=g.n).astype(np.uint8)
+    assert (role == 2).sum() > 128
+    say("breakdown long durations qs=%s" % (qs,))
+    got = gpu_breakdown(g, vs, role)
+    want = O.breakdown(g, vs, role)
+    assert_equal_arrays("long-duration breakdown", got, want)
+
+
 def test_breakdown_full_size_sample():
     """The 2,048-variant transformer sweep: every variant's breakdown."""
     require_gpu()

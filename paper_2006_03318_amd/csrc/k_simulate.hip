@@ -914,7 +914,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         else issue(next_small_tag, rn1, bN, r0, DNb);
         put_next();
         // slot summaries (variant-major); slot 0 absorbs the carry and
-        // starts its variant (kHead); slots of idle waves are the identity
+        // starts its variant (the head value); slots of idle waves are the
+        // identity
 #pragma unroll
         for (int j = 0; j < VPL; j++) {
             const int e = (o0 + j) * NSP + slot;
@@ -1033,7 +1034,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
                 const int tcx = ((flags >> 2) & 63u) * VS + o0;
 #pragma unroll
                 for (int j = 0; j < VPL; j++) {
-                    // positions after a run head hold Dp <= kHead + weights: no effect
+                    // positions after a run head hold Dp = head value + weights
+                    // (below every time, or -inf): the carry has no effect
                     const int64_t F = TM::mx(TM::add(cin[j], Dp[i][j]), Fl[i][j]);
                     rv.x[j] = TM::add(F, Gp[i][j]);
                     fv.x[j] = TM::to_time(F);

@@ -72,8 +72,12 @@ struct alignas(16) CandEnt {
     uint32_t meta;
 };
 
-// candidates (positions with a cross-thread parent) and their requirements
-__global__ __launch_bounds__(kBS) void k_req_fill(int32_t n, Req r, uint64_t mask,
+// candidates (positions with a cross-thread parent) and their requirements;
+// with pent, the packed entries too (T <= kWinT: the first two parent
+// threads by id; T <= kEntT: the first two met in the list, which serves
+// the same test)
+constexpr int kEntT = 255;              // graph threads a packed entry can name (8 bits)
+__global__ __launch_bounds__(kBS) void k_req_fill(int32_t n, int32_t T, Req r, uint64_t mask,
                                                   const int64_t *__restrict__ cidx,
                                                   const int64_t *__restrict__ rptr_by_pos,
                                                   int64_t *__restrict__ cand_pos,
@@ -92,6 +96,8 @@ __global__ __launch_bounds__(kBS) void k_req_fill(int32_t n, Req r, uint64_t mas
     int32_t mx[kWinT];                  // largest requirement per parent thread (-1: none)
 #pragma unroll
     for (int z = 0; z < kWinT; z++) mx[z] = -1;
+    int32_t t0 = -1, t1 = -1, m0 = -1, m1 = -1;   // T > kWinT: the first two threads met
+    bool many = false;                            // a third parent thread
     for (int64_t k = r.xin_ptr[u]; k < r.xin_ptr[u + 1]; k++) {
         if (!on(mask, r.xin_cls[k])) continue;
         const int32_t s = r.xin_src[k];
@@ -102,9 +108,20 @@ __global__ __launch_bounds__(kBS) void k_req_fill(int32_t n, Req r, uint64_t mas
 #pragma unroll
         for (int z = 0; z < kWinT; z++)
             if (z == ts && (int32_t)gp > mx[z]) mx[z] = (int32_t)gp;
+        if (ts == t0) m0 = (int32_t)gp > m0 ? (int32_t)gp : m0;
+        else if (ts == t1) m1 = (int32_t)gp > m1 ? (int32_t)gp : m1;
+        else if (t0 < 0) { t0 = ts; m0 = (int32_t)gp; }
+        else if (t1 < 0) { t1 = ts; m1 = (int32_t)gp; }
+        else many = true;
         o++;
     }
-    if (!pent) return;                  // (more than kWinT threads: no windowed rounds)
+    if (!pent) return;                  // (more than kEntT threads: no packed entries)
+    if (T > kWinT) {
+        const uint32_t nd = (t0 >= 0 ? 1u : 0u) + (t1 >= 0 ? 1u : 0u) + (many ? 1u : 0u);
+        pent[i] = CandEnt{(int32_t)p, m0 < 0 ? 0 : m0, m1 < 0 ? 0 : m1,
+                          (uint32_t)(t0 < 0 ? 0 : t0) | ((uint32_t)(t1 < 0 ? 0 : t1) << 8) | (nd << 16)};
+        return;
+    }
     CandEnt ce{(int32_t)p, 0, 0, 0u};
     uint32_t nd = 0;
 #pragma unroll
@@ -137,6 +154,7 @@ __global__ __launch_bounds__(kBS) void k_cand_base(int32_t T, int64_t n, const i
 }
 
 struct KahnArgs {
+    const CandEnt *pent;      // [C] packed entries (T <= kEntT), else null
     int32_t T;
     int64_t n;
     const int64_t *base;      // [T+1]
@@ -155,20 +173,63 @@ struct KahnArgs {
     uint32_t *err;
 };
 
-__device__ __forceinline__ bool blocked(const KahnArgs &a, int64_t j) {
-    for (int64_t k = a.req_ptr[j]; k < a.req_ptr[j + 1]; k++)
-        if (a.req_gpos[k] >= a.front[a.req_chain[k]]) return true;
-    return false;
-}
+// Round state of the generic rounds: with at most kLdsT graph threads the
+// fronts, candidate cursors and thread bounds live in LDS (a requirement
+// check then reads its parent thread's front from LDS, not from global
+// memory); beyond that they stay in the global arrays.
+constexpr int kLdsT = 2048;
+constexpr int kProbe = 128;     // candidates a round probes per thread before the long-run scan
 
+template <bool L>
 __global__ __launch_bounds__(kWG) void k_kahn_rounds(KahnArgs a) {
     __shared__ int s_nlong;
     __shared__ int s_unfinished;
     __shared__ unsigned long long s_first;
     __shared__ int64_t s_carry_cnt;
+    __shared__ int64_t s_st[L ? 6 * (kLdsT + 1) : 1];
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
-    constexpr int NWAVE = kWG / 64;
+    int64_t *const front = L ? s_st : a.front;
+    int64_t *const cidx = L ? s_st + (kLdsT + 1) : a.cidx;
+    int64_t *const nfront = L ? s_st + 2 * (kLdsT + 1) : a.nfront;
+    int64_t *const ncidx = L ? s_st + 3 * (kLdsT + 1) : a.ncidx;
+    const int64_t *const base = L ? s_st + 4 * (kLdsT + 1) : a.base;
+    const int64_t *const cbase = L ? s_st + 5 * (kLdsT + 1) : a.cbase;
+    if (L) {
+        for (int t = threadIdx.x; t <= a.T; t += kWG) {
+            if (t < a.T) {
+                s_st[t] = a.front[t];
+                s_st[(kLdsT + 1) + t] = a.cidx[t];
+            }
+            s_st[4 * (kLdsT + 1) + t] = a.base[t];
+            s_st[5 * (kLdsT + 1) + t] = a.cbase[t];
+        }
+        __syncthreads();
+    }
+    // lanes per graph thread in step A: all threads in one pass when they fit
+    int gsh = 6;
+    while (gsh > 0 && ((int64_t)a.T << gsh) > kWG) gsh--;
+    const int G = 1 << gsh;
+    const unsigned long long gmask = G == 64 ? ~0ull : ((1ull << G) - 1ull);
+    // a candidate is blocked while a requirement lies at or past the front
+    // of its thread
+    auto blocked_list = [&](int64_t j) {
+        for (int64_t k = a.req_ptr[j]; k < a.req_ptr[j + 1]; k++)
+            if (a.req_gpos[k] >= front[a.req_chain[k]]) return true;
+        return false;
+    };
+    // with packed entries: one 16-byte load; only a candidate with parents
+    // on three or more threads reads its requirement list
+    auto blocked_ent = [&](const CandEnt &e, int64_t j) {
+        const uint32_t nd = e.meta >> 16;
+        if (e.g0 >= front[e.meta & 0xff]) return true;
+        if (nd > 1 && e.g1 >= front[(e.meta >> 8) & 0xff]) return true;
+        if (nd > 2) return blocked_list(j);
+        return false;
+    };
+    auto blocked = [&](int64_t j) {
+        if (a.pent) return blocked_ent(a.pent[j], j);
+        return blocked_list(j);
+    };
     int64_t nseg = 0;
     int64_t round = 0;
     for (;;) {
@@ -177,38 +238,59 @@ __global__ __launch_bounds__(kWG) void k_kahn_rounds(KahnArgs a) {
             s_unfinished = 0;
         }
         __syncthreads();
-        // A: each wave scans up to two windows of 64 candidates of a thread
-        for (int t = wave; t < a.T; t += NWAVE) {
-            const int64_t f = a.front[t], end = a.base[t + 1];
-            int64_t ci = a.cidx[t];
-            const int64_t ce = a.cbase[t + 1];
-            if (f >= end) {
-                if (lane == 0) { a.nfront[t] = f; a.ncidx[t] = ci; }
-                continue;
-            }
-            if (lane == 0) atomicAdd(&s_unfinished, 1);
-            bool done = false;
+        // A: a group of G lanes per graph thread (G = 64 when few threads,
+        // fewer when there are more, so that every thread is probed in one
+        // pass) scans up to kProbe candidates of its thread, G at a time
+        for (int t0 = 0; t0 < a.T; t0 += kWG >> gsh) {
+            const int t = t0 + (int)(threadIdx.x >> gsh);        // uniform within a group
+            const int gl = (int)threadIdx.x & (G - 1);
+            const bool act = t < a.T;
+            const int64_t f = act ? front[t] : 0, end = act ? base[t + 1] : 0;
+            int64_t ci = act ? cidx[t] : 0;
+            const int64_t ce = act ? cbase[t + 1] : 0;
+            const bool fin = !act || f >= end;
+            if (act && fin && gl == 0) { nfront[t] = f; ncidx[t] = ci; }
+            if (!fin && gl == 0) atomicAdd(&s_unfinished, 1);
+            bool done = fin;
             int64_t cnew = ce;
-            for (int w = 0; w < 2 && !done; w++) {
-                const int64_t j = ci + lane;
-                const bool b = j < ce && blocked(a, j);
+            int32_t npos = 0;                 // order position of candidate cnew (packed entries)
+            for (int w = 0; w < (kProbe >> gsh); w++) {
+                if (__all(done)) break;                           // wave-uniform
+                const int64_t j = ci + gl;
+                bool b = false;
+                int32_t pj = 0;
+                if (!done && j < ce) {
+                    if (a.pent) {
+                        const CandEnt e = a.pent[j];
+                        pj = e.pos;
+                        b = blocked_ent(e, j);
+                    } else {
+                        b = blocked_list(j);
+                    }
+                }
                 const unsigned long long bal = __ballot(b);
-                if (bal) {
-                    cnew = ci + __ffsll((long long)bal) - 1;
-                    done = true;
-                } else if (ci + 64 >= ce) {
-                    cnew = ce;
-                    done = true;
-                } else {
-                    ci += 64;
+                const unsigned long long gb = (bal >> (lane & ~(G - 1))) & gmask;
+                const int fl = gb ? __ffsll((long long)gb) - 1 : 0;
+                const int32_t pf = __shfl(pj, (lane & ~(G - 1)) + fl, 64);   // the finder's position
+                if (!done) {
+                    if (gb) {
+                        cnew = ci + fl;
+                        npos = pf;
+                        done = true;
+                    } else if (ci + G >= ce) {
+                        cnew = ce;
+                        done = true;
+                    } else {
+                        ci += G;
+                    }
                 }
             }
-            if (lane == 0) {
+            if (!fin && gl == 0) {
                 if (done) {
-                    a.ncidx[t] = cnew;
-                    a.nfront[t] = cnew < ce ? a.cand_pos[cnew] : end;
+                    ncidx[t] = cnew;
+                    nfront[t] = cnew < ce ? (a.pent ? (int64_t)npos : a.cand_pos[cnew]) : end;
                 } else {
-                    a.ncidx[t] = ci;
+                    ncidx[t] = ci;
                     a.long_list[atomicAdd(&s_nlong, 1)] = t;
                 }
             }
@@ -218,14 +300,14 @@ __global__ __launch_bounds__(kWG) void k_kahn_rounds(KahnArgs a) {
         const int nlong = s_nlong;
         for (int i = 0; i < nlong; i++) {
             const int t = a.long_list[i];
-            int64_t ci = a.ncidx[t];
-            const int64_t ce = a.cbase[t + 1];
+            int64_t ci = ncidx[t];
+            const int64_t ce = cbase[t + 1];
             int64_t cnew = ce;
             for (;;) {
                 if (threadIdx.x == 0) s_first = ~0ull;
                 __syncthreads();
                 const int64_t j = ci + threadIdx.x;
-                if (j < ce && blocked(a, j)) atomicMin(&s_first, (unsigned long long)j);
+                if (j < ce && blocked(j)) atomicMin(&s_first, (unsigned long long)j);
                 __syncthreads();
                 const unsigned long long fb = s_first;
                 __syncthreads();
@@ -234,8 +316,8 @@ __global__ __launch_bounds__(kWG) void k_kahn_rounds(KahnArgs a) {
                 ci += kWG;
             }
             if (threadIdx.x == 0) {
-                a.ncidx[t] = cnew;
-                a.nfront[t] = cnew < ce ? a.cand_pos[cnew] : a.base[t + 1];
+                ncidx[t] = cnew;
+                nfront[t] = cnew < ce ? a.cand_pos[cnew] : base[t + 1];
             }
         }
         __syncthreads();
@@ -243,18 +325,18 @@ __global__ __launch_bounds__(kWG) void k_kahn_rounds(KahnArgs a) {
         // C: emit one segment per advanced thread (packed count<<32 | length scan)
         if (threadIdx.x == 0) s_carry_cnt = 0;
         __syncthreads();
-        for (int base = 0; base < a.T; base += kWG) {
-            const int t = base + threadIdx.x;
+        for (int b0 = 0; b0 < a.T; b0 += kWG) {
+            const int t = b0 + threadIdx.x;
             int64_t len = 0;
-            if (t < a.T) len = a.nfront[t] - a.front[t];
+            if (t < a.T) len = nfront[t] - front[t];
             const int64_t packed = len > 0 ? ((int64_t(1) << 32) | len) : 0;
             int64_t tot;
             const int64_t ex = block_excl_scan<kWG>(packed, &tot);
             if (len > 0) {
-                const int64_t s = nseg + s_carry_cnt + (ex >> 32);
-                a.seg_start[s] = a.front[t];
-                a.seg_len[s] = len;
-                a.seg_step[s] = (int32_t)round;
+                const int64_t sg = nseg + s_carry_cnt + (ex >> 32);
+                a.seg_start[sg] = front[t];
+                a.seg_len[sg] = len;
+                a.seg_step[sg] = (int32_t)round;
             }
             __syncthreads();
             if (threadIdx.x == 0) s_carry_cnt += tot >> 32;
@@ -269,8 +351,8 @@ __global__ __launch_bounds__(kWG) void k_kahn_rounds(KahnArgs a) {
         nseg += adv;
         // D: advance the fronts
         for (int t = threadIdx.x; t < a.T; t += kWG) {
-            a.front[t] = a.nfront[t];
-            a.cidx[t] = a.ncidx[t];
+            front[t] = nfront[t];
+            cidx[t] = ncidx[t];
         }
         round++;
         __syncthreads();
@@ -883,7 +965,7 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
     CK(dalloc_n(&req_ptr, (size_t)Cmax + 1, s));
     CK(dalloc_n(&req_chain, (size_t)Rmax + 1, s));
     CK(dalloc_n(&req_gpos, (size_t)Rmax + 1, s));
-    if (windowed) CK(dalloc_n(&pent, (size_t)Cmax + 1, s));
+    if (T <= kEntT) CK(dalloc_n(&pent, (size_t)Cmax + 1, s));
     CK(dalloc_n(&cbase, (size_t)T + 1, s));
     CK(dalloc_n(&front, (size_t)T, s));
     CK(dalloc_n(&ci, (size_t)T, s));
@@ -896,7 +978,7 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
     CK(dalloc_n(&seg_off, N1 + 1, s));
     CK(dalloc_n(&step_seg, N1 + 1, s));
     if (n > 0) {
-        k_req_fill<<<gN, kBS, 0, s>>>((int32_t)n, rq, mask, cidx, rptr, cand_pos, req_ptr,
+        k_req_fill<<<gN, kBS, 0, s>>>((int32_t)n, T, rq, mask, cidx, rptr, cand_pos, req_ptr,
                                       req_chain, req_gpos, pent);
         CK(hipGetLastError());
     }
@@ -922,10 +1004,11 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
         k_kahn_win<<<1, kWG, 0, s>>>(wa);
         CK(hipGetLastError());
     } else {
-        KahnArgs ka{T, n, g->thread_base, cand_pos, cbase, req_ptr, req_chain, req_gpos,
+        KahnArgs ka{pent, T, n, g->thread_base, cand_pos, cbase, req_ptr, req_chain, req_gpos,
                     front, ci, nfront, nci, long_list, seg_start, seg_len, seg_step, step_seg,
                     result, err};
-        k_kahn_rounds<<<1, kWG, 0, s>>>(ka);
+        if (T <= kLdsT) k_kahn_rounds<true><<<1, kWG, 0, s>>>(ka);
+        else k_kahn_rounds<false><<<1, kWG, 0, s>>>(ka);
         CK(hipGetLastError());
     }
     CK(hipMemcpyAsync(h_res, result, 2 * sizeof(int64_t), hipMemcpyDeviceToHost, s));

@@ -85,6 +85,26 @@ def test_many_threads_chain_ranks(seed):
     assert np.array_equal(gp, ph)
 
 
+@pytest.mark.parametrize("T", [17, 33, 64, 65, 129, 255, 256, 257, 513, 1025, 2048, 2049])
+def test_kahn_rounds_thread_counts(T):
+    """Phases of graphs with more threads than the windowed rounds take: every
+    lane-group width of the probe (32 lanes per thread down to 1, and
+    several passes past 1,024 threads), packed candidate entries (up to 255
+    threads) and not, round state in LDS (up to 2,048 threads) and not;
+    tasks with parents on one, two and three or more other threads."""
+    require_gpu()
+    rng = np.random.default_rng(45_000 + T)
+    n = max(6000, 6 * T)
+    g = W.random_graph_sparse(rng, n, T, mean_in=0.9, window=400, n_edge_cls=2,
+                              run_len=int(rng.integers(1, 12)))
+    for mask in (1, 3):
+        lv, ph = O.steps(g, mask)
+        gp, nph, _ = _steps_gpu(g, mask, B.DD_PHASES)
+        say("kahn threads", T, "mask", mask, "phases", nph)
+        assert nph == int(ph.max()) + 1
+        assert np.array_equal(gp, ph)
+
+
 @pytest.mark.parametrize("k", [1, 2, 3, 4])
 def test_config_steps(k):
     require_gpu()

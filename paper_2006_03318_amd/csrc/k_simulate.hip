@@ -307,7 +307,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
     const uint32_t vsh = (uint32_t)(vvf & 31);
     const int vw = vvf >> 5;
     const int64_t V = a.V, W = a.W;
-    const int64_t nr = *n_rounds;
+    const uint32_t nr = (uint32_t)*n_rounds;   // rounds < 2^32 (at most tasks + tasks / RP + 1)
     const int o0 = lis * VPL;                 // variant offset inside the workgroup
     // stores that must not land go to one 16-byte spot per wave (one line)
     gi64 *const dummy = (gi64 *)(a.dummy + (tid >> 6) * 2);
@@ -343,7 +343,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
         sEon[tid] = a.edge_on[v0 + tid < a.V ? v0 + tid : 0];
     }
     if (any_magic) atomicOr(&sFlags, 1);
-    for (int rr = 0; rr < 2; rr++) {          // prologue: records of rounds 0 and 1
+    for (uint32_t rr = 0; rr < 2; rr++) {     // prologue: records of rounds 0 and 1
         if (rr < nr) {
             const int r0 = round_r0[rr], rn = round_rn[rr];
             const uint4 *src = reinterpret_cast<const uint4 *>(rec + r0);
@@ -457,8 +457,8 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
     // (start, size) of rounds k .. k+3, the last clamped to the final round:
     // each round loads the entry three rounds ahead, so no round waits for
     // a scalar load of its own bounds
-    auto rmeta = [&](int64_t i, int &r0_, int &rn_) {
-        const int64_t c = i < nr ? i : nr - 1;
+    auto rmeta = [&](uint32_t i, int &r0_, int &rn_) {
+        const uint32_t c = i < nr ? i : nr - 1;
         r0_ = round_r0[c];
         rn_ = round_rn[c];
     };
@@ -493,7 +493,7 @@ __global__ __launch_bounds__(NT) void k_sim_pipe(const int32_t *__restrict__ rou
     // an if/else: the compiler then sees no path through an iteration that
     // skips both bodies, so it never makes a round wait for loads of the
     // previous round, or for its stores, that were in fact consumed already.
-    int64_t k = 0;
+    uint32_t k = 0;
     auto round = [&](auto small_tag, auto next_small_tag) {
         constexpr bool SMALL_ROUND = decltype(small_tag)::value;
         const int r0 = m0r0, rn = m0rn;

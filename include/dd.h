@@ -192,8 +192,17 @@ dd_status dd_simulate_batch(const dd_graph *g, const dd_sched *sched, const dd_v
  * dd_simulate_batch_vs -- dd_simulate_batch with an explicit launch shape.
  *   variants_per_wg  variants that each workgroup owns for the whole
  *                    schedule: 0 = chosen by the library (as
- *                    dd_simulate_batch), or 1, 2, 4, 8, 16; any other value
- *                    returns DD_EINVAL.
+ *                    dd_simulate_batch), or 1, 2, 4, 8, 16;
+ *                    -1, -2, -4, -8 = the few-variant path with that many
+ *                    variants per workgroup: one launch per step, each step
+ *                    cut into chunks of 256 positions taken by separate
+ *                    workgroups (DD_EINVAL when the schedule has more than
+ *                    512 steps); any other value returns DD_EINVAL.
+ *   dd_simulate_batch itself takes the few-variant path when the variants
+ *   are fewer than 128 and the schedule has at most 512 steps of 1,024
+ *   positions or more on average.  A variant whose makespan comes back -1
+ *   hit that path's bound on waiting for an earlier chunk (which the ticket
+ *   order of its chunks rules out); its times are then not valid.
  * The results do not depend on the shape (Algorithm 1 per variant, Sec. 4.1);
  * only the number of workgroups and the kernel instance do.  For tuning, and
  * for checking every compiled instance.

@@ -52,7 +52,8 @@ def load_graph(di: DeviceInputs, stream=None):
 def simulate(di: DeviceInputs, mode=B.DD_PHASES, want_start=False, stream=None,
              outputs: Optional[list] = None, keep_handles=False, variants_per_wg: int = 0):
     """Run every batch; returns a list of (v0, v1, finish[N][Vb], start, makespan[Vb]).
-    variants_per_wg: 0 = the library's launch shape, else 1/2/4/8/16."""
+    variants_per_wg: 0 = the library's launch shape, else 1/2/4/8/16, or -1/-2/-4/-8 for
+    the few-variant path (one launch per step) with that many variants per workgroup."""
     import torch
     dev = di.tensors["dur"].device
     g = load_graph(di, stream)

@@ -514,7 +514,13 @@ dd_status simulate_impl(const dd_graph *g, const dd_sched *sched, const dd_varia
         return fail(DD_EMISMATCH, "variants switch on edge classes 0x%llx that the schedule was not built for",
                     (unsigned long long)missing);
     hipStream_t s = (hipStream_t)stream;
-    hipError_t e = dd::launch_simulate(g, sched, var, d_finish, d_start, d_makespan, vs, s);
+    // few variants over few long steps: each step cut across workgroups
+    const int sw = vs < 0 ? -vs : vs == 0 ? dd::split_width(sched, var) : 0;
+    if (sw > 0 && (int64_t)sched->h_step_ptr.size() != sched->n_steps + 1)
+        return fail(DD_EINVAL, "the split path needs a schedule of at most %lld steps (this one has %lld)",
+                    (long long)dd::kSplitMaxSteps, (long long)sched->n_steps);
+    hipError_t e = sw > 0 ? dd::launch_split(g, sched, var, d_finish, d_start, d_makespan, sw, s)
+                          : dd::launch_simulate(g, sched, var, d_finish, d_start, d_makespan, vs, s);
     if (e != hipSuccess) return hip_fail(e, "simulate launch");
     e = dd::note_use(g->uses, g->stream, s);
     if (e == hipSuccess) e = dd::note_use(sched->uses, sched->stream, s);
@@ -537,9 +543,9 @@ dd_status dd_simulate_batch_vs(const dd_graph *g, const dd_sched *sched, const d
                                int64_t *d_finish, int64_t *d_start, int64_t *d_makespan,
                                int32_t variants_per_wg, void *stream) {
     g_err[0] = 0;
-    if (variants_per_wg != 0 && variants_per_wg != 1 && variants_per_wg != 2 &&
-        variants_per_wg != 4 && variants_per_wg != 8 && variants_per_wg != 16)
-        return fail(DD_EINVAL, "variants_per_wg must be 0, 1, 2, 4, 8 or 16 (got %d)",
+    const int w = variants_per_wg < 0 ? -variants_per_wg : variants_per_wg;
+    if (!(w == 0 || w == 1 || w == 2 || w == 4 || w == 8 || (w == 16 && variants_per_wg > 0)))
+        return fail(DD_EINVAL, "variants_per_wg must be 0, 1, 2, 4, 8, 16, -1, -2, -4 or -8 (got %d)",
                     (int)variants_per_wg);
     return simulate_impl(g, sched, var, d_finish, d_start, d_makespan, variants_per_wg, stream);
 }

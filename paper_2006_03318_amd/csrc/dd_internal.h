@@ -60,6 +60,10 @@ struct alignas(16) Rec {
 };
 static_assert(sizeof(Rec) == 48, "record size");
 
+// Schedules of at most this many steps keep a host copy of their step
+// offsets: the few-variant path launches one kernel per step.
+constexpr int64_t kSplitMaxSteps = 512;
+
 // Graphs with at most this many threads keep each thread's latest release in
 // LDS during the simulation instead of gathering the previous task of a run.
 constexpr int kMaxCarryThreads = 64;
@@ -147,6 +151,8 @@ struct dd_sched {
     int32_t *node_step = nullptr; // [n]
     dd::Rec *rec = nullptr;       // [n] per position
     bool thread_carry = false;    // thread predecessors come from per-thread carries
+    std::vector<int32_t> h_step_ptr;  // host copy of step_ptr (schedules of at most
+                                      // kSplitMaxSteps steps; empty otherwise)
     mutable dd::ForeignUses uses;
 };
 
@@ -219,6 +225,14 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
 // transforms (k_transform.hip)
 hipError_t launch_build_scale_table(const dd_ratio *scale_dev, int32_t n_cls, int32_t V,
                                     ScaleEntry *table, uint32_t *err, hipStream_t s);
+
+// few-variant simulation (k_split.hip): every step cut across several
+// workgroups per variant, one launch per step.  split_width() gives the
+// variants per workgroup (1, 2, 4 or 8) when the schedule and variants suit
+// it, else 0; launch_split() takes that width.
+int split_width(const dd_sched *sch, const dd_variants *var);
+hipError_t launch_split(const dd_graph *g, const dd_sched *sch, const dd_variants *var,
+                        int64_t *finish, int64_t *start, int64_t *makespan, int vg, hipStream_t s);
 
 // simulation (k_simulate.hip)
 hipError_t launch_simulate(const dd_graph *g, const dd_sched *sch, const dd_variants *var,

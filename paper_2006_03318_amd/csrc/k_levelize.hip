@@ -1145,6 +1145,11 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
         CK(hipMemcpyAsync(&h_G, sch->gat_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
         if (mode == DD_PHASES)
             CK(hipMemcpyAsync(&h_res[1], result + 1, sizeof(int64_t), hipMemcpyDeviceToHost, s));
+        if (sch->n_steps <= kSplitMaxSteps) {
+            sch->h_step_ptr.resize((size_t)sch->n_steps + 1);
+            CK(hipMemcpyAsync(sch->h_step_ptr.data(), sch->step_ptr,
+                              sizeof(int32_t) * ((size_t)sch->n_steps + 1), hipMemcpyDeviceToHost, s));
+        }
         CK(hipStreamSynchronize(s));
         sch->max_width = (int64_t)h_w;
         sch->n_gathers = h_G;

@@ -1,0 +1,368 @@
+// Batched simulation for few-variant sweeps: every phase cut across several
+// workgroups per variant.
+//
+// What is computed is what the one-workgroup-per-variant kernel computes
+// (Sec. 4.1, Algorithm 1, with the transformations of Sec. 4.4 applied per
+// variant): for each task u and variant v,
+//     d' = removed ? 0 : floor(d * p / q),   g' = removed ? 0 : g
+//     start  = max(0, release of every parent present in v)
+//     finish = start + d',   release = finish + g'
+//     makespan[v] = max finish over tasks not removed in v.
+//
+// How.  With few variants, one workgroup per variant leaves most compute
+// units idle and walks each long phase alone.  Here each phase is one
+// launch.  Its positions are cut into chunks of L consecutive positions and
+// each workgroup takes one (variant group, chunk) pair.  Inside a run of one
+// thread the releases follow R_i = max(R_{i-1}, X_i) + w_i, so a chunk folds
+// its positions into one map c -> max(c + A, B) per variant; a run's first
+// task ignores its input (A = kHead).  A chunk
+//   1. gathers its parents' releases (all in earlier phases, so written by
+//      earlier launches) and folds its maps: lane, wave, workgroup;
+//   2. publishes its aggregate map, or, when it starts a run, its final
+//      release at once;
+//   3. finds its carry-in by looking back over the chunks before it in the
+//      phase: wave 0 reads 64 / VG of them at a time and composes them,
+//      stopping at the first that starts a run or has published its final
+//      release (chunk 0 always starts a run);
+//   4. publishes its final release, then writes finish (and start) of every
+//      position.
+// Chunks take tickets in order, so a chunk only waits for chunks whose
+// workgroups are already running and whose aggregates need nothing from
+// later chunks: no assumption on how many workgroups are resident.  Each
+// wait is bounded; a chunk that gives up marks its variants' makespan -1.
+
+#include "dd_common.h"
+#include "dd_internal.h"
+
+#include <algorithm>
+#include <atomic>
+
+namespace dd {
+namespace {
+
+constexpr int kSpNT = 256;                              // threads per workgroup
+constexpr int64_t kHead = -(int64_t(1) << 62);          // a map that ignores its input
+constexpr uint32_t kSpinMax = 1u << 18;                 // look-back polls before giving up
+
+// The look-back slot of one (step, variant group, chunk, variant).  Every
+// slot is written at most once per call and cleared before the first step,
+// so each word is its own flag: a value x is stored as x with the sign bit
+// flipped, which is never 0 for the values stored here (they lie in
+// [kHead, 2^62)), and 0 means "not yet".  Readers need no ordering between
+// the words, hence relaxed device-scope atomics only (no cache write-back
+// or invalidation, which at device scope would touch the whole L2).
+struct alignas(8) LookSlot {
+    uint64_t a, b;      // aggregate map
+    uint64_t inc;       // release at the chunk's end
+};
+__device__ __forceinline__ uint64_t enc(int64_t x) { return (uint64_t)x ^ (1ull << 63); }
+__device__ __forceinline__ int64_t dec(uint64_t w) { return (int64_t)(w ^ (1ull << 63)); }
+
+struct SplitArgs {
+    const Rec *rec;
+    const int64_t *gat_ptr;       // [n+1] gathers of each position
+    const int32_t *gat_src;       // (gathers beyond two of a position)
+    const uint8_t *gat_cls;
+    const int32_t *thread_prev;   // [n] previous task on the thread
+    const int64_t *gap;           // [n] gap of every task
+    const ScaleEntry *table;      // [n_cls][V]
+    const uint32_t *rm;           // [n][W] removal bits
+    const uint64_t *edge_on;      // [V]
+    int32_t V, W, thread_carry, ngrp;
+    int64_t *finish, *start;
+    unsigned long long *makespan; // [V], zero before the first phase
+    uint32_t *tickets;            // [n_steps][ngrp], zero before the first phase
+    LookSlot *look;               // [chunks of all steps][ngrp][VG], zero before the first phase
+};
+
+__device__ __forceinline__ int64_t scale_dur(int64_t d, const ScaleEntry &se) {
+    const uint64_t x = (uint64_t)d * (uint64_t)se.p;
+    return (int64_t)(se.magic ? (__umul64hi(x, se.magic) >> se.shift) : (x >> se.shift));
+}
+
+// (a, b) := (a, b) followed by (a2, b2)
+__device__ __forceinline__ void then(int64_t &a, int64_t &b, int64_t a2, int64_t b2) {
+    const int64_t t = b + a2;
+    b = t > b2 ? t : b2;
+    a = (a == kHead || a2 == kHead) ? kHead : a + a2;
+}
+
+// the map applied to a carry
+__device__ __forceinline__ int64_t apply(int64_t a, int64_t b, int64_t c) {
+    if (a == kHead) return b;
+    const int64_t t = c + a;
+    return t > b ? t : b;
+}
+
+__device__ __forceinline__ int64_t max64(int64_t x, int64_t y) { return x > y ? x : y; }
+
+__device__ __forceinline__ int64_t shfl64(int64_t x, int src) {
+    const int lo = __shfl((int)(uint32_t)(uint64_t)x, src, 64);
+    const int hi = __shfl((int)(uint32_t)((uint64_t)x >> 32), src, 64);
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+__device__ __forceinline__ bool cls_on(uint64_t eon, uint32_t c) {
+    return c == 255u || ((eon >> c) & 1ull);
+}
+
+__device__ __forceinline__ uint64_t ld_relaxed(const uint64_t *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_relaxed(uint64_t *p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// One phase [s0, s1): nch chunks of L = (kSpNT / VG) * K positions per
+// variant group; lane = (slot, variant), each slot K consecutive positions.
+template <int VG, int K>
+__global__ __launch_bounds__(kSpNT) void k_sim_phase(int32_t p, int32_t s0, int32_t s1,
+                                                     int32_t nch, int64_t coff, SplitArgs a) {
+    constexpr int NSL = kSpNT / VG;
+    constexpr int L = NSL * K;
+    constexpr int NWV = kSpNT / 64;
+    constexpr int NWIN = 64 / VG;             // chunks read per look-back pass
+    __shared__ int sChunk;
+    __shared__ int64_t sWA[NWV][VG], sWB[NWV][VG];
+    __shared__ int64_t sCarry[VG];
+    __shared__ unsigned long long sMs[VG];
+
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int j = tid % VG, slot = tid / VG;
+    const int g = blockIdx.x % a.ngrp;
+    const int v = g * VG + j;
+    const bool vok = v < a.V;
+    const int vv = vok ? v : 0;
+    const int64_t V = a.V, W = a.W;
+    const int vw = vv >> 5;
+    const uint32_t vbit = 1u << (vv & 31);
+    // this step's slots: [nch][ngrp][VG] from chunk offset coff
+    LookSlot *const look = a.look + coff * a.ngrp * VG;
+    auto slot_of = [&](int ch) { return look + ((int64_t)ch * a.ngrp + g) * VG + j; };
+
+    if (tid == 0) sChunk = (int)atomicAdd(&a.tickets[(int64_t)p * a.ngrp + g], 1u);
+    if (tid < VG) sMs[tid] = 0ull;
+    __syncthreads();
+    const int c = sChunk;
+    const int64_t q0 = (int64_t)s0 + (int64_t)c * L;
+    const int64_t q1 = q0 + L < (int64_t)s1 ? q0 + L : (int64_t)s1;
+    const uint64_t eon = a.edge_on[vv];
+
+    // release of a parent: its finish plus its gap when it is kept
+    auto rel = [&](int64_t s) -> int64_t {
+        const int64_t f = a.finish[s * V + vv];
+        const bool rs = a.rm[s * W + vw] & vbit;
+        return f + (rs ? 0 : a.gap[s]);
+    };
+
+    // 1. gather and fold
+    int64_t X[K], DP[K], GP[K];
+    int32_t ND[K];
+    uint32_t hd = 0, ok = 0, lv = 0;
+    int64_t la = 0, lb = kHead;               // identity
+#pragma unroll
+    for (int k = 0; k < K; k++) {
+        const int64_t q = q0 + (int64_t)slot * K + k;
+        X[k] = 0; DP[k] = 0; GP[k] = 0; ND[k] = 0;
+        if (q < q1) {
+            const Rec r = a.rec[q];
+            const int64_t u = r.node;
+            const bool live = !(a.rm[u * W + vw] & vbit);
+            const int64_t dp = live ? scale_dur(r.dur, a.table[(int64_t)(r.cls & 0xffffu) * V + vv]) : 0;
+            const int64_t gp = live ? r.gap : 0;
+            int64_t x = 0;
+            if (r.g0_src >= 0 && cls_on(eon, (r.cls >> 16) & 0xffu)) x = max64(x, rel(r.g0_src));
+            if (r.g1_src >= 0 && cls_on(eon, r.cls >> 24)) x = max64(x, rel(r.g1_src));
+            if (r.flags >> 8) {                // gathers beyond two
+                const int64_t e1 = a.gat_ptr[q + 1];
+                for (int64_t e = a.gat_ptr[q] + 2; e < e1; e++)
+                    if (cls_on(eon, a.gat_cls[e])) x = max64(x, rel(a.gat_src[e]));
+            }
+            const bool head = r.flags & 1u;
+            if (head && a.thread_carry) {      // the run's thread predecessor
+                const int32_t tp = a.thread_prev[u];
+                if (tp >= 0) x = max64(x, rel(tp));
+            }
+            X[k] = x; DP[k] = dp; GP[k] = gp; ND[k] = (int32_t)u;
+            ok |= 1u << k;
+            hd |= (head ? 1u : 0u) << k;
+            lv |= (live ? 1u : 0u) << k;
+            then(la, lb, head ? kHead : dp + gp, x + dp + gp);
+        }
+    }
+    // inclusive scan over the slots of one variant: inside the wave (lanes
+    // VG apart), then across waves
+    int64_t ia = la, ib = lb;
+#pragma unroll
+    for (int o = VG; o < 64; o <<= 1) {
+        const int64_t pa = shfl_up64(ia, o), pb = shfl_up64(ib, o);
+        if (lane >= o) {
+            int64_t na = pa, nb = pb;
+            then(na, nb, ia, ib);
+            ia = na; ib = nb;
+        }
+    }
+    if (lane >= 64 - VG) { sWA[wv][j] = ia; sWB[wv][j] = ib; }
+    const int64_t xa = shfl_up64(ia, VG), xb = shfl_up64(ib, VG);
+    __syncthreads();
+    int64_t ea = 0, eb = kHead;               // exclusive map of this slot
+    for (int w2 = 0; w2 < wv; w2++) then(ea, eb, sWA[w2][j], sWB[w2][j]);
+    if (lane >= VG) then(ea, eb, xa, xb);
+
+    // 2.-3. publish, look back, publish the chunk's final release
+    if (wv == 0) {
+        int64_t ga = 0, gb = kHead;           // the chunk's aggregate
+        for (int w2 = 0; w2 < NWV; w2++) then(ga, gb, sWA[w2][j], sWB[w2][j]);
+        const bool later = c + 1 < nch;       // a chunk after this one reads the slot
+        LookSlot *own = slot_of(c);
+        // the carry-in is needed unless the chunk's first position starts a run
+        const bool first_head = c == 0 || (__shfl((int)hd, j, 64) & 1);
+        if (later && !first_head && lane < VG) {
+            st_relaxed(&own->a, enc(ga));
+            st_relaxed(&own->b, enc(gb));
+        }
+        int64_t cin = kHead;
+        bool fail = false;
+        if (!first_head) {
+            // acc: composition of the chunks after the current window, up to
+            // c - 1 (the same in every lane of one variant; the loop runs
+            // while any variant of the wave still looks back)
+            int64_t acc_a = 0, acc_b = kHead;
+            bool done = false;
+            int dtop = c - 1;
+            const int kw = lane / VG;
+            while (__any(!done)) {
+                const int d = dtop - kw;
+                int64_t ta = 0, tb = kHead;   // identity for lanes past chunk 0
+                if (!done && d >= 0) {
+                    LookSlot *const ls = slot_of(d);
+                    uint32_t spins = 0;
+                    for (;;) {
+                        const uint64_t wi = ld_relaxed(&ls->inc);
+                        if (wi) { ta = kHead; tb = dec(wi); break; }
+                        const uint64_t wa = ld_relaxed(&ls->a), wb = ld_relaxed(&ls->b);
+                        if (wa && wb) { ta = dec(wa); tb = dec(wb); break; }
+                        if (++spins >= kSpinMax) { fail = true; ta = kHead; tb = 0; break; }
+                        __builtin_amdgcn_s_sleep(2);
+                    }
+                }
+                // T_k = (chunk dtop - k) followed by ... followed by (chunk dtop)
+#pragma unroll
+                for (int o = VG; o < 64; o <<= 1) {
+                    const int64_t pa = shfl_up64(ta, o), pb = shfl_up64(tb, o);
+                    if (lane >= o) then(ta, tb, pa, pb);
+                }
+                int64_t na = shfl64(ta, (NWIN - 1) * VG + j), nb = shfl64(tb, (NWIN - 1) * VG + j);
+                if (!done) {
+                    then(na, nb, acc_a, acc_b);
+                    acc_a = na; acc_b = nb;
+                    dtop -= NWIN;
+                    done = acc_a == kHead || dtop < 0;
+                }
+            }
+            cin = apply(acc_a, acc_b, kHead);
+        }
+        fail = __any(fail);
+        if (lane < VG) {
+            sCarry[j] = cin;
+            if (later) st_relaxed(&own->inc, enc(apply(ga, gb, cin)));
+            if (fail && vok) atomicMax(&a.makespan[v], ~0ull);
+        }
+    }
+    __syncthreads();
+
+    // 4. results
+    int64_t cr = apply(ea, eb, sCarry[j]);
+    unsigned long long ms = 0ull;
+#pragma unroll
+    for (int k = 0; k < K; k++) {
+        if (ok & (1u << k)) {
+            const int64_t st = (hd & (1u << k)) ? X[k] : max64(cr, X[k]);
+            const int64_t f = st + DP[k];
+            cr = f + GP[k];
+            if (vok) {
+                a.finish[(int64_t)ND[k] * V + v] = f;
+                if (a.start) a.start[(int64_t)ND[k] * V + v] = st;
+                if ((lv >> k) & 1u) ms = ms > (unsigned long long)f ? ms : (unsigned long long)f;
+            }
+        }
+    }
+    if (ms) atomicMax(&sMs[j], ms);
+    __syncthreads();
+    if (tid < VG && vok && sMs[tid]) atomic_max_hot(&a.makespan[v], sMs[tid]);
+}
+
+__global__ __launch_bounds__(256) void k_split_zero(uint32_t *tickets, int64_t nt, uint64_t *look,
+                                                   int64_t nl, int64_t *makespan, int64_t V) {
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < nt + nl + V; i += stride) {
+        if (i < nt) tickets[i] = 0u;
+        else if (i < nt + nl) look[i - nt] = 0ull;
+        else makespan[i - nt - nl] = 0;
+    }
+}
+
+template <int VG, int K>
+hipError_t run_phases(const dd_graph *g, const dd_sched *sch, const dd_variants *var,
+                      int64_t *finish, int64_t *start, int64_t *makespan, hipStream_t s) {
+    constexpr int L = (kSpNT / VG) * K;
+    const std::vector<int32_t> &sp = sch->h_step_ptr;
+    const int64_t ns = sch->n_steps;
+    if ((int64_t)sp.size() != ns + 1) return hipErrorInvalidValue;
+    int64_t nchunks = 0;               // chunks of all steps
+    for (int64_t p = 0; p < ns; p++) nchunks += (sp[p + 1] - sp[p] + L - 1) / L;
+    const int ngrp = (var->V + VG - 1) / VG;
+    const int64_t nt = ns * ngrp;
+    const int64_t nslot = nchunks * ngrp * VG;
+    const int64_t nl = nslot * (int64_t)(sizeof(LookSlot) / 8);
+    uint32_t *tickets = nullptr;
+    LookSlot *look = nullptr;
+    hipError_t e = dalloc_n(&tickets, (size_t)nt + 1, s);
+    if (e == hipSuccess) e = dalloc_n(&look, (size_t)nslot + 1, s);
+    if (e == hipSuccess) {
+        k_split_zero<<<grid_for(nt + nl + var->V, 256) < 1024 ? grid_for(nt + nl + var->V, 256) : 1024,
+                       256, 0, s>>>(tickets, nt, reinterpret_cast<uint64_t *>(look), nl, makespan,
+                                    var->V);
+        e = hipGetLastError();
+    }
+    SplitArgs args{sch->rec, sch->gat_ptr, sch->gat_src, sch->gat_cls, g->thread_prev, g->gap,
+                   var->table, var->rm_bits, var->edge_on, var->V, var->W,
+                   sch->thread_carry ? 1 : 0, ngrp, finish, start,
+                   reinterpret_cast<unsigned long long *>(makespan), tickets, look};
+    int64_t coff = 0;
+    for (int64_t p = 0; p < ns && e == hipSuccess; p++) {
+        const int64_t len = sp[p + 1] - sp[p];
+        if (len <= 0) continue;
+        const int32_t nch = (int32_t)((len + L - 1) / L);
+        k_sim_phase<VG, K><<<nch * ngrp, kSpNT, 0, s>>>((int32_t)p, sp[p], sp[p + 1], nch, coff, args);
+        e = hipGetLastError();
+        coff += nch;
+    }
+    dfree(tickets, s);
+    dfree(look, s);
+    return e;
+}
+
+}  // namespace
+
+int split_width(const dd_sched *sch, const dd_variants *var) {
+    if (sch->n <= 0 || var->V <= 0 || (int64_t)sch->h_step_ptr.size() != sch->n_steps + 1)
+        return 0;
+    // few variants (one workgroup each would leave most of the 256 compute
+    // units idle) and few, long phases (one launch each)
+    if (var->V >= 128 || sch->n_steps > kSplitMaxSteps || sch->n < 1024 * sch->n_steps) return 0;
+    return var->V >= 8 ? 8 : var->V >= 4 ? 4 : var->V >= 2 ? 2 : 1;
+}
+
+hipError_t launch_split(const dd_graph *g, const dd_sched *sch, const dd_variants *var,
+                        int64_t *finish, int64_t *start, int64_t *makespan, int vg, hipStream_t s) {
+    switch (vg) {
+        case 1: return run_phases<1, 1>(g, sch, var, finish, start, makespan, s);
+        case 2: return run_phases<2, 2>(g, sch, var, finish, start, makespan, s);
+        case 4: return run_phases<4, 4>(g, sch, var, finish, start, makespan, s);
+        case 8: return run_phases<8, 8>(g, sch, var, finish, start, makespan, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace dd

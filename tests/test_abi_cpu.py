@@ -45,6 +45,14 @@ def test_argument_errors_without_device(lib):
     assert lib.dd_apply_transforms(None, 1, 1, None, None, None, None,
                                    ctypes.byref(out)) == B.DD_EINVAL
     assert lib.dd_simulate_batch(None, None, None, None, None, None, None) == B.DD_EINVAL
+    # launch shapes: 0, 1, 2, 4, 8, 16 (one workgroup per variant strip),
+    # -1, -2, -4, -8 (the few-variant path); the value is checked first
+    for bad in (3, -3, -16, 32, -32):
+        assert lib.dd_simulate_batch_vs(None, None, None, None, None, None, bad, None) == B.DD_EINVAL
+        assert "variants_per_wg" in B.dd_last_error()
+    for good in (0, 1, 16, -1, -8):
+        assert lib.dd_simulate_batch_vs(None, None, None, None, None, None, good, None) == B.DD_EINVAL
+        assert "NULL handle" in B.dd_last_error()
     assert lib.dd_sched_task_steps(None, None, None) == B.DD_EINVAL
     assert lib.dd_sched_info(None, None, None, None, None) == B.DD_EINVAL
     # freeing NULL handles is a no-op

@@ -1,0 +1,162 @@
+"""Parity of the few-variant path (every step cut into chunks of 256
+positions taken by separate workgroups, a look-back over the chunks before
+each chunk for the release that enters it) with the oracle: start, finish
+and makespan bit-exact (Sec. 4.1, Algorithm 1).
+
+The cases are chosen so that runs of one thread cross many chunk
+boundaries (a single chain of 20,000 tasks is one phase of 79 chunks, more
+than one look-back pass at every width), chunks start both inside a run and
+at a run's first task, graphs have more than 64 threads (run heads gather
+their thread predecessor as an ordinary parent), tasks wait on many parents,
+and the variant count leaves the last workgroup partly idle.
+"""
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2006_03318_amd import batch as BT
+from paper_2006_03318_amd import binding as B
+from paper_2006_03318_amd import workloads as W
+from tests import helpers as H
+from tests.gpu_common import assert_equal_arrays, gpu_run, require_gpu, say
+
+pytestmark = pytest.mark.gpu
+
+WIDTHS = [-1, -2, -4, -8]
+
+
+def _check(g, vs, width, mode=B.DD_PHASES, label="", want_start=True):
+    say("split", label, "n=%d threads=%d V=%d mode=%d width=%d"
+        % (g.n, g.n_threads, vs.n_variants, mode, width))
+    S, F, M = gpu_run(g, vs, mode=mode, variants_per_wg=width, want_start=want_start)
+    oS, oF, oM, _ = O.run(g, vs, want_start=want_start)
+    assert_equal_arrays(label + " makespan", M, oM)
+    assert_equal_arrays(label + " finish", F, oF)
+    if want_start:
+        assert_equal_arrays(label + " start", S, oS)
+
+
+@pytest.mark.parametrize("seed", range(24))
+@pytest.mark.parametrize("mode", [B.DD_PHASES, B.DD_LEVELS])
+def test_random_small(seed, mode):
+    require_gpu()
+    rng = np.random.default_rng(90_000 + seed)
+    n = int(rng.integers(1, 300))
+    g = W.random_graph(rng, n, int(rng.integers(1, 5)), p_edge=float(rng.uniform(0.005, 0.05)),
+                       n_edge_cls=int(rng.integers(1, 4)),
+                       max_dur=int(rng.choice([5, 1000, 10**6])))
+    vs = W.random_variants(rng, g, int(rng.integers(1, 20)), p_remove=float(rng.uniform(0, 0.5)))
+    _check(g, vs, WIDTHS[seed % 4], mode, "small%d" % seed)
+
+
+# (tasks, threads, mean in-degree, tasks per burst on one thread, window)
+CHAINS = [(20000, 1, 0.0, 1, 64), (20000, 3, 0.01, 200, 2000), (20000, 2, 0.002, 50, 5000),
+          (30000, 4, 0.005, 500, 3000), (6000, 100, 0.01, 8, 2000), (9000, 5, 0.05, 3, 300)]
+
+
+def _chain_case(i, V):
+    n, T, mi, rl, win = CHAINS[i]
+    rng = np.random.default_rng(91_000 + i)
+    g = W.random_graph_sparse(rng, n, T, mean_in=mi, window=win, n_edge_cls=2, run_len=rl)
+    vs = W.random_variants(rng, g, V, p_remove=0.2)
+    return g, vs
+
+
+@pytest.mark.parametrize("width", WIDTHS)
+@pytest.mark.parametrize("i", range(len(CHAINS)))
+def test_long_runs(i, width):
+    require_gpu()
+    g, vs = _chain_case(i, 11 if width != -1 else 3)
+    _check(g, vs, width, B.DD_PHASES, "chains%d" % i)
+
+
+def test_many_threads_levels_mode():
+    """Every position starts a run: chunks never look back."""
+    require_gpu()
+    rng = np.random.default_rng(92_000)
+    g = W.random_graph_sparse(rng, 4000, 300, mean_in=0.5, window=50, n_edge_cls=2, run_len=2)
+    vs = W.random_variants(rng, g, 9, p_remove=0.3)
+    _check(g, vs, -8, B.DD_LEVELS, "levels-300-threads")
+
+
+def test_configs_default_and_widths():
+    """The seq2seq sweep (64 variants, 28 phases) takes this path by
+    default; every width gives the same results."""
+    require_gpu()
+    g, vs = W.config(4)
+    oS, oF, oM, _ = O.run(g, vs)
+    for width in (0, -8, -2):
+        say("split config4 width=%d" % width)
+        S, F, M = gpu_run(g, vs, variants_per_wg=width)
+        assert_equal_arrays("config4 makespan", M, oM)
+        assert_equal_arrays("config4 finish", F, oF)
+        assert_equal_arrays("config4 start", S, oS)
+
+
+def test_config1_every_width():
+    require_gpu()
+    g, vs = W.config(1)
+    for width in WIDTHS:
+        _check(g, vs, width, B.DD_PHASES, "config1", want_start=(width % 2 == 0))
+
+
+def test_wide_fan_in():
+    """A task waiting on 200 tasks of 200 other threads, in the middle of
+    a long run."""
+    require_gpu()
+    T = 201
+    thread = [1 + i for i in range(200)] + [0] * 3000
+    edges = [(i, 200 + 1500) for i in range(200)]
+    dur = [int(7 + (i * 37) % 1000) for i in range(len(thread))]
+    gap = [int((i * 11) % 5) for i in range(len(thread))]
+    g = H.graph(T, thread, edges, dur, gap)
+    vs = W.random_variants(np.random.default_rng(5), g, 13, p_remove=0.1)
+    for width in WIDTHS:
+        _check(g, vs, width, B.DD_PHASES, "fan-in")
+
+
+def test_outputs_prefilled_with_sentinel():
+    """Outputs start full of a huge sentinel: a position that is skipped, or
+    a parent read before its launch wrote it, shows up as a wrong value."""
+    import torch
+    require_gpu()
+    sent = 1 << 61
+    g, vs = _chain_case(1, 19)
+    oS, oF, oM, _ = O.run(g, vs)
+    for width in WIDTHS:
+        di = BT.to_device(g, vs)
+        outs = [(torch.full((g.n, v1 - v0), sent, dtype=torch.int64, device="cuda"),
+                 torch.full((g.n, v1 - v0), sent, dtype=torch.int64, device="cuda"),
+                 torch.full((v1 - v0,), sent, dtype=torch.int64, device="cuda"))
+                for (v0, v1, *_r) in di.batches]
+        say("split sentinel width=%d" % width)
+        res = BT.simulate(di, want_start=True, outputs=outs, variants_per_wg=width)
+        torch.cuda.synchronize()
+        for v0, v1, f, s_, m in res:
+            assert_equal_arrays("sentinel makespan", m.cpu().numpy(), oM[v0:v1])
+            assert_equal_arrays("sentinel finish", f.cpu().numpy().T, oF[v0:v1])
+            assert_equal_arrays("sentinel start", s_.cpu().numpy().T, oS[v0:v1])
+
+
+def test_repeat_calls_same_results():
+    """Look-back slots and tickets are cleared by every call: a second call
+    on the same handles gives the same results."""
+    import torch
+    require_gpu()
+    g, vs = _chain_case(3, 8)
+    di = BT.to_device(g, vs)
+    a = BT.simulate(di, variants_per_wg=-8, keep_handles=True)
+    res, gh, hs = a
+    torch.cuda.synchronize()
+    first = [(f.cpu().numpy().copy(), m.cpu().numpy().copy()) for (_, _, f, _, m) in res]
+    stream = torch.cuda.current_stream()
+    for (v0, v1, fin, st, ms), (sch, var) in zip(res, hs):
+        B.dd_simulate_batch_vs(gh, sch, var, fin, None, ms, -8, stream)
+    torch.cuda.synchronize()
+    for (f0, m0), (_, _, f, _, m) in zip(first, res):
+        assert_equal_arrays("repeat finish", f.cpu().numpy(), f0)
+        assert_equal_arrays("repeat makespan", m.cpu().numpy(), m0)
+    for sch, var in hs:
+        B.dd_sched_free(sch)
+        B.dd_variants_free(var)
+    B.dd_graph_free(gh)

@@ -282,6 +282,7 @@ def main():
             ev[k + 2].record(stream)
             if binfo[bi] is None:
                 binfo[bi] = B.dd_sched_info(sch)
+                binfo[bi]["plan"] = B.dd_simulate_plan(sch, var)
             if not info:
                 info.update(binfo[bi])
             hs.append((sch, var))
@@ -324,12 +325,20 @@ def main():
     nbytes = sum(algorithmic_bytes(g.n, v1 - v0, bi_["n_gathers"], di.n_cls)
                  for (v0, v1, *_r), bi_ in zip(di.batches, binfo))
     achieved = nbytes / (sim_ms / 1e3) / 1e9
+    # the few-variant path (negative plan) launches one kernel per step (plus
+    # one that clears its look-back slots); its "launch" here is the whole
+    # simulate call of a batch
+    split = all(b["plan"] < 0 for b in binfo)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": measured_traffic(args.config, g.n, vs.n_variants),
-                "kernel": "k_sim_pipe", "algorithmic_bytes_per_launch": int(nbytes),
+                "traffic": None if split else measured_traffic(args.config, g.n, vs.n_variants),
+                "kernel": "k_sim_phase" if split else "k_sim_pipe",
+                "algorithmic_bytes_per_launch": int(nbytes),
                 "avg_launch_ms": round(sim_ms / len(di.batches), 4),
-                "launches_per_step": len(di.batches)}
+                "launches_per_step": len(di.batches),
+                "kernel_launches_per_step": int(sum(b["n_steps"] + 1 if b["plan"] < 0 else 1
+                                                    for b in binfo)),
+                "variants_per_workgroup": [b["plan"] for b in binfo]}
 
     # the runtime breakdown (CPU-only / GPU-only / CPU+GPU parallel) of every
     # variant, after the timed steps

@@ -200,9 +200,7 @@ dd_status dd_simulate_batch(const dd_graph *g, const dd_sched *sched, const dd_v
  *                    512 steps); any other value returns DD_EINVAL.
  *   dd_simulate_batch itself takes the few-variant path when the variants
  *   are fewer than 128 and the schedule has at most 512 steps of 1,024
- *   positions or more on average.  A variant whose makespan comes back -1
- *   hit that path's bound on waiting for an earlier chunk (which the ticket
- *   order of its chunks rules out); its times are then not valid.
+ *   positions or more on average.
  * The results do not depend on the shape (Algorithm 1 per variant, Sec. 4.1);
  * only the number of workgroups and the kernel instance do.  For tuning, and
  * for checking every compiled instance.
@@ -210,6 +208,19 @@ dd_status dd_simulate_batch(const dd_graph *g, const dd_sched *sched, const dd_v
 dd_status dd_simulate_batch_vs(const dd_graph *g, const dd_sched *sched, const dd_variants *var,
                                int64_t *d_finish, int64_t *d_start, int64_t *d_makespan,
                                int32_t variants_per_wg, void *stream);
+
+/*
+ * dd_set_lookback_polls -- how long a chunk of the few-variant path waits
+ * for an earlier chunk (Sec. 4.1: the releases of one thread's run carried
+ * across chunks).  A chunk reads the aggregate that each earlier chunk of its
+ * run publishes; after `polls` unanswered reads it folds that chunk itself
+ * from the inputs, which come from earlier launches, so no chunk ever depends
+ * on another workgroup being resident.  The results do not depend on the
+ * value.  polls < 0 restores the default (4,096); 0 makes every chunk fold
+ * its predecessors itself (for tests of that fallback).  Applies to calls
+ * made after it, process-wide.
+ */
+void dd_set_lookback_polls(int32_t polls);
 
 /*
  * dd_simulate_batch_noalloc -- dd_simulate_batch for callers that cannot
@@ -304,6 +315,16 @@ dd_status dd_release_cache(void);
 
 /* Step (level or phase) of every task: int32 [n], host or device pointer. */
 dd_status dd_sched_task_steps(const dd_sched *sched, int32_t *steps_out, void *stream);
+
+/*
+ * dd_simulate_plan -- the launch shape dd_simulate_batch takes for these
+ * handles, in the terms of dd_simulate_batch_vs: *variants_per_wg = 1, 2, 4,
+ * 8 or 16 (one workgroup per strip of that many variants for the whole
+ * schedule, one launch) or -1, -2, -4 (the few-variant path, one launch per
+ * step).  DD_EINVAL on a NULL argument.
+ */
+dd_status dd_simulate_plan(const dd_sched *sched, const dd_variants *var,
+                           int32_t *variants_per_wg);
 
 /* Schedule shape: steps, thread runs (segments), widest step, gather entries. */
 dd_status dd_sched_info(const dd_sched *sched, int64_t *n_steps, int64_t *n_segments,

@@ -67,6 +67,8 @@ def lib():
         "dd_apply_transforms": (_i32, [_vp, _i32, _i32, _vp, _vp, _vp, _vp, ctypes.POINTER(_vp)]),
         "dd_simulate_batch": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _vp]),
         "dd_simulate_batch_vs": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _i32, _vp]),
+        "dd_set_lookback_polls": (None, [_i32]),
+        "dd_simulate_plan": (_i32, [_vp, _vp, ctypes.POINTER(_i32)]),
         "dd_release_cache": (_i32, []),
         "dd_simulate_batch_noalloc": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _vp]),
         "dd_runtime_breakdown": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _vp]),
@@ -195,6 +197,18 @@ def dd_simulate_batch_vs(g, sched, var, d_finish, d_start, d_makespan, variants_
                                     _ptr(d_start, "int64"), _ptr(d_makespan, "int64"),
                                     int(variants_per_wg), _stream(stream))
     _check(rc)
+
+
+def dd_simulate_plan(sched, var) -> int:
+    """Launch shape dd_simulate_batch takes: > 0 variants per workgroup of the
+    strip kernel, < 0 the few-variant path (one launch per step)."""
+    w = _i32()
+    _check(lib().dd_simulate_plan(sched, var, ctypes.byref(w)))
+    return int(w.value)
+
+
+def dd_set_lookback_polls(polls: int):
+    lib().dd_set_lookback_polls(int(polls))
 
 
 def dd_runtime_breakdown(g, var, role, d_finish, d_makespan, d_out, stream=None):

@@ -550,6 +550,8 @@ dd_status dd_simulate_batch_vs(const dd_graph *g, const dd_sched *sched, const d
     return simulate_impl(g, sched, var, d_finish, d_start, d_makespan, variants_per_wg, stream);
 }
 
+void dd_set_lookback_polls(int32_t polls) { dd::split_set_polls(polls); }
+
 dd_status dd_runtime_breakdown(const dd_graph *g, const dd_variants *var, const uint8_t *role,
                                const int64_t *d_finish, const int64_t *d_makespan,
                                int64_t *d_out, void *stream) {
@@ -685,6 +687,15 @@ dd_status dd_sched_task_steps(const dd_sched *sched, int32_t *steps_out, void *s
                                   hipMemcpyDefault, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) return hip_fail(e, "copy steps");
+    return DD_OK;
+}
+
+dd_status dd_simulate_plan(const dd_sched *sched, const dd_variants *var,
+                           int32_t *variants_per_wg) {
+    g_err[0] = 0;
+    if (!sched || !var || !variants_per_wg) return fail(DD_EINVAL, "NULL argument");
+    const int sw = dd::split_width(sched, var);
+    *variants_per_wg = sw > 0 ? -sw : dd::strip_width(var->V);
     return DD_OK;
 }
 

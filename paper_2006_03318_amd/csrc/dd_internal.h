@@ -231,8 +231,20 @@ hipError_t launch_build_scale_table(const dd_ratio *scale_dev, int32_t n_cls, in
 // variants per workgroup (1, 2, 4 or 8) when the schedule and variants suit
 // it, else 0; launch_split() takes that width.
 int split_width(const dd_sched *sch, const dd_variants *var);
+// look-back polls of one slot before a lane folds that chunk itself
+// (negative: the default)
+void split_set_polls(int32_t polls);
 hipError_t launch_split(const dd_graph *g, const dd_sched *sch, const dd_variants *var,
                         int64_t *finish, int64_t *start, int64_t *makespan, int vg, hipStream_t s);
+
+// variants per workgroup of the one-workgroup-per-strip kernel when the
+// caller leaves it to the library: enough workgroups to cover the 256
+// compute units, then the widest rows
+inline int strip_width(int64_t V) {
+    int vs = 1;
+    while (vs < 16 && V / (vs * 2) >= 256) vs *= 2;
+    return vs;
+}
 
 // simulation (k_simulate.hip)
 hipError_t launch_simulate(const dd_graph *g, const dd_sched *sch, const dd_variants *var,

@@ -1328,12 +1328,7 @@ hipError_t launch_pipe(const dd_graph *g, const dd_sched *sch, const dd_variants
 // arguments.
 template <class F>
 auto with_shape(const dd_variants *var, int vs_hint, F &&f) {
-    int vs = vs_hint;
-    if (vs <= 0) {
-        // enough workgroups to cover the 256 compute units, then widest rows
-        vs = 1;
-        while (vs < 16 && (int64_t)var->V / (vs * 2) >= 256) vs *= 2;
-    }
+    const int vs = vs_hint > 0 ? vs_hint : strip_width(var->V);
     const bool pair = (var->V % 2) == 0;
     switch (vs) {
         case 1: return f(std::integral_constant<int, 1>{}, std::integral_constant<int, 1>{},

@@ -21,15 +21,17 @@
 //   2. publishes its aggregate map, or, when it starts a run, its final
 //      release at once;
 //   3. finds its carry-in by looking back over the chunks before it in the
-//      phase: wave 0 reads 64 / VG of them at a time and composes them,
-//      stopping at the first that starts a run or has published its final
+//      phase: every thread reads one (chunk, variant) slot, so a pass covers
+//      256 / VG chunks, composed in the wave and then across waves; it stops
+//      at the first chunk that starts a run or has published its final
 //      release (chunk 0 always starts a run);
 //   4. publishes its final release, then writes finish (and start) of every
 //      position.
-// Chunks take tickets in order, so a chunk only waits for chunks whose
-// workgroups are already running and whose aggregates need nothing from
-// later chunks: no assumption on how many workgroups are resident.  Each
-// wait is bounded; a chunk that gives up marks its variants' makespan -1.
+// A chunk never depends on another workgroup running: every input of a
+// chunk's aggregate comes from earlier launches, so a lane that has polled
+// an earlier chunk's slot for long enough (that chunk's workgroup may not
+// have started yet) folds that chunk itself and goes on.  No assumption on
+// how many workgroups are resident or in which order they start.
 
 #include "dd_common.h"
 #include "dd_internal.h"
@@ -42,7 +44,8 @@ namespace {
 
 constexpr int kSpNT = 256;                              // threads per workgroup
 constexpr int64_t kHead = -(int64_t(1) << 62);          // a map that ignores its input
-constexpr uint32_t kSpinMax = 1u << 18;                 // look-back polls before giving up
+constexpr int32_t kPolls = 1 << 12;                     // look-back polls before a lane folds
+                                                        // the chunk itself
 
 // The look-back slot of one (step, variant group, chunk, variant).  Every
 // slot is written at most once per call and cleared before the first step,
@@ -69,9 +72,9 @@ struct SplitArgs {
     const uint32_t *rm;           // [n][W] removal bits
     const uint64_t *edge_on;      // [V]
     int32_t V, W, thread_carry, ngrp;
+    int32_t polls;                // look-back polls of one slot before the lane folds the chunk
     int64_t *finish, *start;
     unsigned long long *makespan; // [V], zero before the first phase
-    uint32_t *tickets;            // [n_steps][ngrp], zero before the first phase
     LookSlot *look;               // [chunks of all steps][ngrp][VG], zero before the first phase
 };
 
@@ -96,12 +99,6 @@ __device__ __forceinline__ int64_t apply(int64_t a, int64_t b, int64_t c) {
 
 __device__ __forceinline__ int64_t max64(int64_t x, int64_t y) { return x > y ? x : y; }
 
-__device__ __forceinline__ int64_t shfl64(int64_t x, int src) {
-    const int lo = __shfl((int)(uint32_t)(uint64_t)x, src, 64);
-    const int hi = __shfl((int)(uint32_t)((uint64_t)x >> 32), src, 64);
-    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
-}
-
 __device__ __forceinline__ bool cls_on(uint64_t eon, uint32_t c) {
     return c == 255u || ((eon >> c) & 1ull);
 }
@@ -121,9 +118,9 @@ __global__ __launch_bounds__(kSpNT) void k_sim_phase(int32_t p, int32_t s0, int3
     constexpr int NSL = kSpNT / VG;
     constexpr int L = NSL * K;
     constexpr int NWV = kSpNT / 64;
-    constexpr int NWIN = 64 / VG;             // chunks read per look-back pass
-    __shared__ int sChunk;
+    __shared__ int sFirst;
     __shared__ int64_t sWA[NWV][VG], sWB[NWV][VG];
+    __shared__ int64_t sLA[NWV][VG], sLB[NWV][VG];
     __shared__ int64_t sCarry[VG];
     __shared__ unsigned long long sMs[VG];
 
@@ -140,19 +137,50 @@ __global__ __launch_bounds__(kSpNT) void k_sim_phase(int32_t p, int32_t s0, int3
     LookSlot *const look = a.look + coff * a.ngrp * VG;
     auto slot_of = [&](int ch) { return look + ((int64_t)ch * a.ngrp + g) * VG + j; };
 
-    if (tid == 0) sChunk = (int)atomicAdd(&a.tickets[(int64_t)p * a.ngrp + g], 1u);
-    if (tid < VG) sMs[tid] = 0ull;
-    __syncthreads();
-    const int c = sChunk;
+    const int c = (int)(blockIdx.x / a.ngrp);
+    auto chunk_end = [&](int ch) {
+        const int64_t e = (int64_t)s0 + (int64_t)(ch + 1) * L;
+        return e < (int64_t)s1 ? e : (int64_t)s1;
+    };
     const int64_t q0 = (int64_t)s0 + (int64_t)c * L;
-    const int64_t q1 = q0 + L < (int64_t)s1 ? q0 + L : (int64_t)s1;
+    const int64_t q1 = chunk_end(c);
     const uint64_t eon = a.edge_on[vv];
+    if (tid < VG) sMs[tid] = 0ull;
 
     // release of a parent: its finish plus its gap when it is kept
     auto rel = [&](int64_t s) -> int64_t {
         const int64_t f = a.finish[s * V + vv];
         const bool rs = a.rm[s * W + vw] & vbit;
         return f + (rs ? 0 : a.gap[s]);
+    };
+
+    // one position for this lane's variant: latest parent release x,
+    // duration dp and gap gp as transformed, run start, kept
+    struct Pos {
+        int64_t x, dp, gp;
+        int32_t u;
+        bool head, live;
+    };
+    auto position = [&](int64_t q) -> Pos {
+        const Rec r = a.rec[q];
+        const int64_t u = r.node;
+        const bool live = !(a.rm[u * W + vw] & vbit);
+        const int64_t dp = live ? scale_dur(r.dur, a.table[(int64_t)(r.cls & 0xffffu) * V + vv]) : 0;
+        const int64_t gp = live ? r.gap : 0;
+        int64_t x = 0;
+        if (r.g0_src >= 0 && cls_on(eon, (r.cls >> 16) & 0xffu)) x = max64(x, rel(r.g0_src));
+        if (r.g1_src >= 0 && cls_on(eon, r.cls >> 24)) x = max64(x, rel(r.g1_src));
+        if (r.flags >> 8) {                    // gathers beyond two
+            const int64_t e1 = a.gat_ptr[q + 1];
+            for (int64_t e = a.gat_ptr[q] + 2; e < e1; e++)
+                if (cls_on(eon, a.gat_cls[e])) x = max64(x, rel(a.gat_src[e]));
+        }
+        const bool head = r.flags & 1u;
+        if (head && a.thread_carry) {          // the run's thread predecessor
+            const int32_t tp = a.thread_prev[u];
+            if (tp >= 0) x = max64(x, rel(tp));
+        }
+        return Pos{x, dp, gp, (int32_t)u, head, live};
     };
 
     // 1. gather and fold
@@ -165,29 +193,12 @@ __global__ __launch_bounds__(kSpNT) void k_sim_phase(int32_t p, int32_t s0, int3
         const int64_t q = q0 + (int64_t)slot * K + k;
         X[k] = 0; DP[k] = 0; GP[k] = 0; ND[k] = 0;
         if (q < q1) {
-            const Rec r = a.rec[q];
-            const int64_t u = r.node;
-            const bool live = !(a.rm[u * W + vw] & vbit);
-            const int64_t dp = live ? scale_dur(r.dur, a.table[(int64_t)(r.cls & 0xffffu) * V + vv]) : 0;
-            const int64_t gp = live ? r.gap : 0;
-            int64_t x = 0;
-            if (r.g0_src >= 0 && cls_on(eon, (r.cls >> 16) & 0xffu)) x = max64(x, rel(r.g0_src));
-            if (r.g1_src >= 0 && cls_on(eon, r.cls >> 24)) x = max64(x, rel(r.g1_src));
-            if (r.flags >> 8) {                // gathers beyond two
-                const int64_t e1 = a.gat_ptr[q + 1];
-                for (int64_t e = a.gat_ptr[q] + 2; e < e1; e++)
-                    if (cls_on(eon, a.gat_cls[e])) x = max64(x, rel(a.gat_src[e]));
-            }
-            const bool head = r.flags & 1u;
-            if (head && a.thread_carry) {      // the run's thread predecessor
-                const int32_t tp = a.thread_prev[u];
-                if (tp >= 0) x = max64(x, rel(tp));
-            }
-            X[k] = x; DP[k] = dp; GP[k] = gp; ND[k] = (int32_t)u;
+            const Pos ps = position(q);
+            X[k] = ps.x; DP[k] = ps.dp; GP[k] = ps.gp; ND[k] = ps.u;
             ok |= 1u << k;
-            hd |= (head ? 1u : 0u) << k;
-            lv |= (live ? 1u : 0u) << k;
-            then(la, lb, head ? kHead : dp + gp, x + dp + gp);
+            hd |= (ps.head ? 1u : 0u) << k;
+            lv |= (ps.live ? 1u : 0u) << k;
+            then(la, lb, ps.head ? kHead : ps.dp + ps.gp, ps.x + ps.dp + ps.gp);
         }
     }
     // inclusive scan over the slots of one variant: inside the wave (lanes
@@ -203,6 +214,7 @@ __global__ __launch_bounds__(kSpNT) void k_sim_phase(int32_t p, int32_t s0, int3
         }
     }
     if (lane >= 64 - VG) { sWA[wv][j] = ia; sWB[wv][j] = ib; }
+    if (tid == 0) sFirst = c == 0 || (hd & 1u);
     const int64_t xa = shfl_up64(ia, VG), xb = shfl_up64(ib, VG);
     __syncthreads();
     int64_t ea = 0, eb = kHead;               // exclusive map of this slot
@@ -210,64 +222,68 @@ __global__ __launch_bounds__(kSpNT) void k_sim_phase(int32_t p, int32_t s0, int3
     if (lane >= VG) then(ea, eb, xa, xb);
 
     // 2.-3. publish, look back, publish the chunk's final release
-    if (wv == 0) {
-        int64_t ga = 0, gb = kHead;           // the chunk's aggregate
-        for (int w2 = 0; w2 < NWV; w2++) then(ga, gb, sWA[w2][j], sWB[w2][j]);
-        const bool later = c + 1 < nch;       // a chunk after this one reads the slot
-        LookSlot *own = slot_of(c);
-        // the carry-in is needed unless the chunk's first position starts a run
-        const bool first_head = c == 0 || (__shfl((int)hd, j, 64) & 1);
-        if (later && !first_head && lane < VG) {
-            st_relaxed(&own->a, enc(ga));
-            st_relaxed(&own->b, enc(gb));
-        }
-        int64_t cin = kHead;
-        bool fail = false;
-        if (!first_head) {
-            // acc: composition of the chunks after the current window, up to
-            // c - 1 (the same in every lane of one variant; the loop runs
-            // while any variant of the wave still looks back)
-            int64_t acc_a = 0, acc_b = kHead;
-            bool done = false;
-            int dtop = c - 1;
-            const int kw = lane / VG;
-            while (__any(!done)) {
-                const int d = dtop - kw;
-                int64_t ta = 0, tb = kHead;   // identity for lanes past chunk 0
-                if (!done && d >= 0) {
-                    LookSlot *const ls = slot_of(d);
-                    uint32_t spins = 0;
-                    for (;;) {
-                        const uint64_t wi = ld_relaxed(&ls->inc);
-                        if (wi) { ta = kHead; tb = dec(wi); break; }
-                        const uint64_t wa = ld_relaxed(&ls->a), wb = ld_relaxed(&ls->b);
-                        if (wa && wb) { ta = dec(wa); tb = dec(wb); break; }
-                        if (++spins >= kSpinMax) { fail = true; ta = kHead; tb = 0; break; }
-                        __builtin_amdgcn_s_sleep(2);
+    int64_t ga = 0, gb = kHead;               // the chunk's aggregate
+    for (int w2 = 0; w2 < NWV; w2++) then(ga, gb, sWA[w2][j], sWB[w2][j]);
+    const bool later = c + 1 < nch;           // a chunk after this one reads the slot
+    LookSlot *const own = slot_of(c);
+    // the carry-in is needed unless the chunk's first position starts a run
+    const bool first_head = sFirst != 0;
+    if (later && !first_head && tid < VG) {
+        st_relaxed(&own->a, enc(ga));
+        st_relaxed(&own->b, enc(gb));
+    }
+    int64_t cin = kHead;
+    if (!first_head) {
+        // every thread reads chunk dtop - slot for its variant, so one pass
+        // covers NSL chunks; acc composes the chunks after the current
+        // window up to c - 1 (the same in every thread of one variant)
+        int64_t acc_a = 0, acc_b = kHead;
+        bool done = false;
+        int dtop = c - 1;
+        for (;;) {
+            const int d = dtop - slot;
+            int64_t ta = 0, tb = kHead;       // identity past chunk 0
+            if (!done && d >= 0) {
+                LookSlot *const ls = slot_of(d);
+                for (int32_t n = 0;; n++) {
+                    if (n >= a.polls) {       // fold chunk d here
+                        const int64_t e = chunk_end(d);
+                        for (int64_t q = (int64_t)s0 + (int64_t)d * L; q < e; q++) {
+                            const Pos ps = position(q);
+                            then(ta, tb, ps.head ? kHead : ps.dp + ps.gp, ps.x + ps.dp + ps.gp);
+                        }
+                        break;
                     }
-                }
-                // T_k = (chunk dtop - k) followed by ... followed by (chunk dtop)
-#pragma unroll
-                for (int o = VG; o < 64; o <<= 1) {
-                    const int64_t pa = shfl_up64(ta, o), pb = shfl_up64(tb, o);
-                    if (lane >= o) then(ta, tb, pa, pb);
-                }
-                int64_t na = shfl64(ta, (NWIN - 1) * VG + j), nb = shfl64(tb, (NWIN - 1) * VG + j);
-                if (!done) {
-                    then(na, nb, acc_a, acc_b);
-                    acc_a = na; acc_b = nb;
-                    dtop -= NWIN;
-                    done = acc_a == kHead || dtop < 0;
+                    const uint64_t wi = ld_relaxed(&ls->inc);
+                    if (wi) { ta = kHead; tb = dec(wi); break; }
+                    const uint64_t wa = ld_relaxed(&ls->a), wb = ld_relaxed(&ls->b);
+                    if (wa && wb) { ta = dec(wa); tb = dec(wb); break; }
+                    __builtin_amdgcn_s_sleep(2);
                 }
             }
-            cin = apply(acc_a, acc_b, kHead);
+            // in the wave: (earlier chunk) followed by (later chunks)
+#pragma unroll
+            for (int o = VG; o < 64; o <<= 1) {
+                const int64_t pa = shfl_up64(ta, o), pb = shfl_up64(tb, o);
+                if (lane >= o) then(ta, tb, pa, pb);
+            }
+            if (lane >= 64 - VG) { sLA[wv][j] = ta; sLB[wv][j] = tb; }
+            __syncthreads();
+            if (!done) {
+                int64_t na = 0, nb = kHead;   // the last wave holds the earliest chunks
+                for (int w2 = NWV - 1; w2 >= 0; w2--) then(na, nb, sLA[w2][j], sLB[w2][j]);
+                then(na, nb, acc_a, acc_b);
+                acc_a = na; acc_b = nb;
+                dtop -= NSL;
+                done = acc_a == kHead || dtop < 0;
+            }
+            if (!__syncthreads_or(done ? 0 : 1)) break;
         }
-        fail = __any(fail);
-        if (lane < VG) {
-            sCarry[j] = cin;
-            if (later) st_relaxed(&own->inc, enc(apply(ga, gb, cin)));
-            if (fail && vok) atomicMax(&a.makespan[v], ~0ull);
-        }
+        cin = apply(acc_a, acc_b, kHead);
+    }
+    if (tid < VG) {
+        sCarry[j] = cin;
+        if (later) st_relaxed(&own->inc, enc(apply(ga, gb, cin)));
     }
     __syncthreads();
 
@@ -289,18 +305,19 @@ __global__ __launch_bounds__(kSpNT) void k_sim_phase(int32_t p, int32_t s0, int3
     }
     if (ms) atomicMax(&sMs[j], ms);
     __syncthreads();
-    if (tid < VG && vok && sMs[tid]) atomic_max_hot(&a.makespan[v], sMs[tid]);
+    if (tid < VG && vok && sMs[tid]) atomicMax(&a.makespan[v], sMs[tid]);
 }
 
-__global__ __launch_bounds__(256) void k_split_zero(uint32_t *tickets, int64_t nt, uint64_t *look,
-                                                   int64_t nl, int64_t *makespan, int64_t V) {
+__global__ __launch_bounds__(256) void k_split_zero(uint64_t *look, int64_t nl, int64_t *makespan,
+                                                   int64_t V) {
     const int64_t stride = (int64_t)gridDim.x * 256;
-    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < nt + nl + V; i += stride) {
-        if (i < nt) tickets[i] = 0u;
-        else if (i < nt + nl) look[i - nt] = 0ull;
-        else makespan[i - nt - nl] = 0;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < nl + V; i += stride) {
+        if (i < nl) look[i] = 0ull;
+        else makespan[i - nl] = 0;
     }
 }
+
+std::atomic<int32_t> g_polls{kPolls};
 
 template <int VG, int K>
 hipError_t run_phases(const dd_graph *g, const dd_sched *sch, const dd_variants *var,
@@ -312,23 +329,20 @@ hipError_t run_phases(const dd_graph *g, const dd_sched *sch, const dd_variants 
     int64_t nchunks = 0;               // chunks of all steps
     for (int64_t p = 0; p < ns; p++) nchunks += (sp[p + 1] - sp[p] + L - 1) / L;
     const int ngrp = (var->V + VG - 1) / VG;
-    const int64_t nt = ns * ngrp;
     const int64_t nslot = nchunks * ngrp * VG;
     const int64_t nl = nslot * (int64_t)(sizeof(LookSlot) / 8);
-    uint32_t *tickets = nullptr;
     LookSlot *look = nullptr;
-    hipError_t e = dalloc_n(&tickets, (size_t)nt + 1, s);
-    if (e == hipSuccess) e = dalloc_n(&look, (size_t)nslot + 1, s);
+    hipError_t e = dalloc_n(&look, (size_t)nslot + 1, s);
     if (e == hipSuccess) {
-        k_split_zero<<<grid_for(nt + nl + var->V, 256) < 1024 ? grid_for(nt + nl + var->V, 256) : 1024,
-                       256, 0, s>>>(tickets, nt, reinterpret_cast<uint64_t *>(look), nl, makespan,
-                                    var->V);
+        const int zg = grid_for(nl + var->V, 256);
+        k_split_zero<<<zg < 1024 ? zg : 1024, 256, 0, s>>>(reinterpret_cast<uint64_t *>(look), nl,
+                                                          makespan, var->V);
         e = hipGetLastError();
     }
     SplitArgs args{sch->rec, sch->gat_ptr, sch->gat_src, sch->gat_cls, g->thread_prev, g->gap,
                    var->table, var->rm_bits, var->edge_on, var->V, var->W,
-                   sch->thread_carry ? 1 : 0, ngrp, finish, start,
-                   reinterpret_cast<unsigned long long *>(makespan), tickets, look};
+                   sch->thread_carry ? 1 : 0, ngrp, g_polls.load(), finish, start,
+                   reinterpret_cast<unsigned long long *>(makespan), look};
     int64_t coff = 0;
     for (int64_t p = 0; p < ns && e == hipSuccess; p++) {
         const int64_t len = sp[p + 1] - sp[p];
@@ -338,12 +352,13 @@ hipError_t run_phases(const dd_graph *g, const dd_sched *sch, const dd_variants 
         e = hipGetLastError();
         coff += nch;
     }
-    dfree(tickets, s);
     dfree(look, s);
     return e;
 }
 
 }  // namespace
+
+void split_set_polls(int32_t polls) { g_polls.store(polls < 0 ? kPolls : polls); }
 
 int split_width(const dd_sched *sch, const dd_variants *var) {
     if (sch->n <= 0 || var->V <= 0 || (int64_t)sch->h_step_ptr.size() != sch->n_steps + 1)
@@ -351,7 +366,7 @@ int split_width(const dd_sched *sch, const dd_variants *var) {
     // few variants (one workgroup each would leave most of the 256 compute
     // units idle) and few, long phases (one launch each)
     if (var->V >= 128 || sch->n_steps > kSplitMaxSteps || sch->n < 1024 * sch->n_steps) return 0;
-    return var->V >= 8 ? 8 : var->V >= 4 ? 4 : var->V >= 2 ? 2 : 1;
+    return var->V >= 4 ? 4 : var->V >= 2 ? 2 : 1;
 }
 
 hipError_t launch_split(const dd_graph *g, const dd_sched *sch, const dd_variants *var,

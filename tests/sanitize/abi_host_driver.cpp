@@ -42,6 +42,10 @@ hipError_t simulate_noalloc(const dd_graph *, const dd_sched *, const dd_variant
     *limit = 0;
     STUB;
 }
+int split_width(const dd_sched *, const dd_variants *) { return 0; }
+hipError_t launch_split(const dd_graph *, const dd_sched *, const dd_variants *, int64_t *, int64_t *,
+                        int64_t *, int, hipStream_t) { STUB; }
+void split_set_polls(int32_t) {}
 hipError_t launch_breakdown(const dd_graph *, const dd_variants *, const uint8_t *, const int64_t *,
                             const int64_t *, int64_t *, int32_t *, int64_t *, hipStream_t) { STUB; }
 hipError_t build_event_lists(const dd_graph *, EventLists *, hipStream_t) { STUB; }
@@ -104,6 +108,15 @@ int main() {
     EXPECT(strstr(dd_last_error(), "variants_per_wg") != nullptr, "width message");
     EXPECT(dd_simulate_batch_vs(nullptr, nullptr, nullptr, dummy, nullptr, dummy, 32, nullptr) == DD_EINVAL, "width 32 rejected");
     EXPECT(dd_simulate_batch_vs(nullptr, nullptr, nullptr, dummy, nullptr, dummy, 16, nullptr) == DD_EINVAL, "width 16 NULL handles");
+    EXPECT(dd_simulate_batch_vs(nullptr, nullptr, nullptr, dummy, nullptr, dummy, -3, nullptr) == DD_EINVAL, "width -3 rejected");
+    EXPECT(dd_simulate_batch_vs(nullptr, nullptr, nullptr, dummy, nullptr, dummy, -16, nullptr) == DD_EINVAL, "width -16 rejected");
+    EXPECT(dd_simulate_batch_vs(nullptr, nullptr, nullptr, dummy, nullptr, dummy, -8, nullptr) == DD_EINVAL, "width -8 NULL handles");
+    {
+        int32_t w = 0;
+        EXPECT(dd_simulate_plan(nullptr, nullptr, &w) == DD_EINVAL && has_msg(), "plan of NULL handles");
+    }
+    dd_set_lookback_polls(0);
+    dd_set_lookback_polls(-1);
     EXPECT(dd_runtime_breakdown(nullptr, nullptr, nullptr, dummy, dummy, dummy, nullptr) == DD_EINVAL, "breakdown NULL handles");
     EXPECT(dd_simulate_batch_noalloc(nullptr, nullptr, nullptr, dummy, nullptr, dummy, nullptr) == DD_EINVAL, "no-alloc NULL handles");
     EXPECT(dd_simulate_policy(nullptr, nullptr, 0, nullptr, nullptr, dummy, nullptr, dummy, nullptr) == DD_EINVAL, "policy NULL handles");

@@ -85,7 +85,7 @@ def test_configs_default_and_widths():
     require_gpu()
     g, vs = W.config(4)
     oS, oF, oM, _ = O.run(g, vs)
-    for width in (0, -8, -2):
+    for width in (0, -8, -4, -2):
         say("split config4 width=%d" % width)
         S, F, M = gpu_run(g, vs, variants_per_wg=width)
         assert_equal_arrays("config4 makespan", M, oM)
@@ -139,8 +139,8 @@ def test_outputs_prefilled_with_sentinel():
 
 
 def test_repeat_calls_same_results():
-    """Look-back slots and tickets are cleared by every call: a second call
-    on the same handles gives the same results."""
+    """Look-back slots are cleared by every call: a second call on the same
+    handles gives the same results."""
     import torch
     require_gpu()
     g, vs = _chain_case(3, 8)
@@ -160,3 +160,17 @@ def test_repeat_calls_same_results():
         B.dd_sched_free(sch)
         B.dd_variants_free(var)
     B.dd_graph_free(gh)
+
+
+def test_chunks_fold_their_predecessors_when_told_not_to_wait():
+    """With no polls allowed, every chunk that needs the release entering it
+    folds the chunks before it itself (the path a chunk takes when an
+    earlier chunk's workgroup has not started): the same results."""
+    require_gpu()
+    try:
+        B.dd_set_lookback_polls(0)
+        for i, width in ((0, -8), (1, -8), (3, -4), (0, -1), (5, -2)):
+            g, vs = _chain_case(i, 11 if width != -1 else 3)
+            _check(g, vs, width, B.DD_PHASES, "fold-predecessors%d" % i)
+    finally:
+        B.dd_set_lookback_polls(-1)

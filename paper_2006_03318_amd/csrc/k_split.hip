@@ -155,21 +155,51 @@ __global__ __launch_bounds__(kSpNT) void k_sim_phase(int32_t p, int32_t s0, int3
     };
 
     // one position for this lane's variant: latest parent release x,
-    // duration dp and gap gp as transformed, run start, kept
+    // duration dp and gap gp as transformed, run start, kept.  In three
+    // stages, so that a lane issues the loads of all its positions before
+    // it waits for any: the record; what the record points at (the task's
+    // removal word and scale entry, each inline parent's finish, removal
+    // word and gap); the arithmetic, with the rare loads (parents beyond
+    // two, a run's thread predecessor).
     struct Pos {
         int64_t x, dp, gp;
         int32_t u;
         bool head, live;
     };
-    auto position = [&](int64_t q) -> Pos {
-        const Rec r = a.rec[q];
+    struct Deps {
+        ScaleEntry se;
+        int64_t f0, g0, f1, g1;
+        uint32_t rmw, r0w, r1w;
+    };
+    auto deps_of = [&](const Rec &r) -> Deps {
         const int64_t u = r.node;
-        const bool live = !(a.rm[u * W + vw] & vbit);
-        const int64_t dp = live ? scale_dur(r.dur, a.table[(int64_t)(r.cls & 0xffffu) * V + vv]) : 0;
+        Deps d{};
+        d.rmw = a.rm[u * W + vw];
+        d.se = a.table[(int64_t)(r.cls & 0xffffu) * V + vv];
+        if (r.g0_src >= 0) {
+            const int64_t s0i = r.g0_src;
+            d.f0 = a.finish[s0i * V + vv];
+            d.r0w = a.rm[s0i * W + vw];
+            d.g0 = a.gap[s0i];
+        }
+        if (r.g1_src >= 0) {
+            const int64_t s1i = r.g1_src;
+            d.f1 = a.finish[s1i * V + vv];
+            d.r1w = a.rm[s1i * W + vw];
+            d.g1 = a.gap[s1i];
+        }
+        return d;
+    };
+    auto position_of = [&](int64_t q, const Rec &r, const Deps &d) -> Pos {
+        const int64_t u = r.node;
+        const bool live = !(d.rmw & vbit);
+        const int64_t dp = live ? scale_dur(r.dur, d.se) : 0;
         const int64_t gp = live ? r.gap : 0;
         int64_t x = 0;
-        if (r.g0_src >= 0 && cls_on(eon, (r.cls >> 16) & 0xffu)) x = max64(x, rel(r.g0_src));
-        if (r.g1_src >= 0 && cls_on(eon, r.cls >> 24)) x = max64(x, rel(r.g1_src));
+        if (r.g0_src >= 0 && cls_on(eon, (r.cls >> 16) & 0xffu))
+            x = max64(x, d.f0 + ((d.r0w & vbit) ? 0 : d.g0));
+        if (r.g1_src >= 0 && cls_on(eon, r.cls >> 24))
+            x = max64(x, d.f1 + ((d.r1w & vbit) ? 0 : d.g1));
         if (r.flags >> 8) {                    // gathers beyond two
             const int64_t e1 = a.gat_ptr[q + 1];
             for (int64_t e = a.gat_ptr[q] + 2; e < e1; e++)
@@ -182,18 +212,31 @@ __global__ __launch_bounds__(kSpNT) void k_sim_phase(int32_t p, int32_t s0, int3
         }
         return Pos{x, dp, gp, (int32_t)u, head, live};
     };
+    auto position = [&](int64_t q) -> Pos {
+        const Rec r = a.rec[q];
+        return position_of(q, r, deps_of(r));
+    };
 
     // 1. gather and fold
     int64_t X[K], DP[K], GP[K];
     int32_t ND[K];
     uint32_t hd = 0, ok = 0, lv = 0;
     int64_t la = 0, lb = kHead;               // identity
+    Rec R[K];
+    Deps D[K];
+#pragma unroll
+    for (int k = 0; k < K; k++) {              // positions past the chunk read its last one
+        const int64_t q = q0 + (int64_t)slot * K + k;
+        R[k] = a.rec[q < q1 ? q : q1 - 1];
+    }
+#pragma unroll
+    for (int k = 0; k < K; k++) D[k] = deps_of(R[k]);
 #pragma unroll
     for (int k = 0; k < K; k++) {
         const int64_t q = q0 + (int64_t)slot * K + k;
         X[k] = 0; DP[k] = 0; GP[k] = 0; ND[k] = 0;
         if (q < q1) {
-            const Pos ps = position(q);
+            const Pos ps = position_of(q, R[k], D[k]);
             X[k] = ps.x; DP[k] = ps.dp; GP[k] = ps.gp; ND[k] = ps.u;
             ok |= 1u << k;
             hd |= (ps.head ? 1u : 0u) << k;
@@ -366,7 +409,7 @@ int split_width(const dd_sched *sch, const dd_variants *var) {
     // few variants (one workgroup each would leave most of the 256 compute
     // units idle) and few, long phases (one launch each)
     if (var->V >= 128 || sch->n_steps > kSplitMaxSteps || sch->n < 1024 * sch->n_steps) return 0;
-    return var->V >= 4 ? 4 : var->V >= 2 ? 2 : 1;
+    return var->V >= 8 ? 8 : var->V >= 4 ? 4 : var->V >= 2 ? 2 : 1;
 }
 
 hipError_t launch_split(const dd_graph *g, const dd_sched *sch, const dd_variants *var,

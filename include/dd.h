@@ -199,8 +199,9 @@ dd_status dd_simulate_batch(const dd_graph *g, const dd_sched *sched, const dd_v
  *                    workgroups (DD_EINVAL when the schedule has more than
  *                    512 steps); any other value returns DD_EINVAL.
  *   dd_simulate_batch itself takes the few-variant path when the variants
- *   are fewer than 128 and the schedule has at most 512 steps of 1,024
- *   positions or more on average.
+ *   are fewer than 128, the schedule has at most 512 steps, and its steps
+ *   hold more than about 4.4 rounds of 512 positions on average (where that
+ *   path measured faster).
  * The results do not depend on the shape (Algorithm 1 per variant, Sec. 4.1);
  * only the number of workgroups and the kernel instance do.  For tuning, and
  * for checking every compiled instance.

@@ -406,10 +406,25 @@ void split_set_polls(int32_t polls) { g_polls.store(polls < 0 ? kPolls : polls);
 int split_width(const dd_sched *sch, const dd_variants *var) {
     if (sch->n <= 0 || var->V <= 0 || (int64_t)sch->h_step_ptr.size() != sch->n_steps + 1)
         return 0;
-    // few variants (one workgroup each would leave most of the 256 compute
-    // units idle) and few, long phases (one launch each)
-    if (var->V >= 128 || sch->n_steps > kSplitMaxSteps || sch->n < 1024 * sch->n_steps) return 0;
-    return var->V >= 8 ? 8 : var->V >= 4 ? 4 : var->V >= 2 ? 2 : 1;
+    // Few variants only (one workgroup each would leave most of the 256
+    // compute units idle).  Then by measured cost: the one-workgroup-per-
+    // variant kernel takes about 1.8 us per round of 512 positions, this path
+    // about 8 us per step (a launch and its chain of memory trips), so it
+    // wins when steps hold more than about 4.4 rounds on average.
+    if (var->V >= 128) return 0;
+    const std::vector<int32_t> &sp = sch->h_step_ptr;
+    int64_t rounds = 0, wmax = 0;
+    for (int64_t p = 0; p < sch->n_steps; p++) {
+        const int64_t len = sp[p + 1] - sp[p];
+        rounds += (len + 511) / 512;
+        wmax = std::max<int64_t>(wmax, len);
+    }
+    if (rounds * 9 <= sch->n_steps * 40) return 0;
+    // 8 variants per workgroup when the widest step then still gives about
+    // 1.5 workgroups per compute unit, else 4 (more, smaller workgroups)
+    const int64_t wg8 = (int64_t)((var->V + 7) / 8) * ((wmax + 255) / 256);
+    if (var->V >= 8 && wg8 >= 384) return 8;
+    return var->V >= 4 ? 4 : var->V >= 2 ? 2 : 1;
 }
 
 hipError_t launch_split(const dd_graph *g, const dd_sched *sch, const dd_variants *var,

@@ -174,3 +174,31 @@ def test_chunks_fold_their_predecessors_when_told_not_to_wait():
             _check(g, vs, width, B.DD_PHASES, "fold-predecessors%d" % i)
     finally:
         B.dd_set_lookback_polls(-1)
+
+
+def _plan(g, vs):
+    import torch
+    di = BT.to_device(g, vs)
+    res, gh, hs = BT.simulate(di, keep_handles=True)
+    torch.cuda.synchronize()
+    plans = [B.dd_simulate_plan(s_, v_) for s_, v_ in hs]
+    for s_, v_ in hs:
+        B.dd_sched_free(s_)
+        B.dd_variants_free(v_)
+    B.dd_graph_free(gh)
+    return plans
+
+
+def test_launch_plan():
+    """dd_simulate_batch takes the few-variant path only where it measured
+    faster: few variants over steps of several rounds of 512 positions."""
+    require_gpu()
+    g, vs = W.config(4)                       # 28 long phases, 64 variants
+    assert _plan(g, vs) == [-8]
+    g, vs = W.config(1)                       # short phases
+    assert _plan(g, vs) == [1]
+    g, vs = W.config(2)                       # 256 variants
+    assert _plan(g, vs) == [1]
+    rng = np.random.default_rng(500)          # one phase of 20,000 tasks, 5 variants
+    g = W.random_graph_sparse(rng, 20000, 1, mean_in=0.0, window=64, n_edge_cls=1)
+    assert _plan(g, W.random_variants(rng, g, 5, p_remove=0.1)) == [-4]

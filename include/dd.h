@@ -199,7 +199,7 @@ dd_status dd_simulate_batch(const dd_graph *g, const dd_sched *sched, const dd_v
  *                    workgroups (DD_EINVAL when the schedule has more than
  *                    512 steps); any other value returns DD_EINVAL.
  *   dd_simulate_batch itself takes the few-variant path when the variants
- *   are fewer than 128, the schedule has at most 512 steps, and its steps
+ *   are fewer than 1,024, the schedule has at most 512 steps, and its steps
  *   hold more than about 4.4 rounds of 512 positions on average (where that
  *   path measured faster).
  * The results do not depend on the shape (Algorithm 1 per variant, Sec. 4.1);
@@ -321,7 +321,7 @@ dd_status dd_sched_task_steps(const dd_sched *sched, int32_t *steps_out, void *s
  * dd_simulate_plan -- the launch shape dd_simulate_batch takes for these
  * handles, in the terms of dd_simulate_batch_vs: *variants_per_wg = 1, 2, 4,
  * 8 or 16 (one workgroup per strip of that many variants for the whole
- * schedule, one launch) or -1, -2, -4 (the few-variant path, one launch per
+ * schedule, one launch) or -1, -2, -4, -8 (the few-variant path, one launch per
  * step).  DD_EINVAL on a NULL argument.
  */
 dd_status dd_simulate_plan(const dd_sched *sched, const dd_variants *var,

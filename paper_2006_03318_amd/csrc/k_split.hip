@@ -406,12 +406,14 @@ void split_set_polls(int32_t polls) { g_polls.store(polls < 0 ? kPolls : polls);
 int split_width(const dd_sched *sch, const dd_variants *var) {
     if (sch->n <= 0 || var->V <= 0 || (int64_t)sch->h_step_ptr.size() != sch->n_steps + 1)
         return 0;
-    // Few variants only (one workgroup each would leave most of the 256
-    // compute units idle).  Then by measured cost: the one-workgroup-per-
-    // variant kernel takes about 1.8 us per round of 512 positions, this path
-    // about 8 us per step (a launch and its chain of memory trips), so it
-    // wins when steps hold more than about 4.4 rounds on average.
-    if (var->V >= 128) return 0;
+    // Fewer than 1,024 variants only: below that the one-workgroup-per-strip
+    // kernel either leaves compute units idle or runs its workgroups in two
+    // passes (one variant per workgroup up to 511 variants, two up to
+    // 1,023).  Then by measured cost: that kernel takes about 1.8 us per round
+    // of 512 positions, this path about 8 us per step (a launch and its
+    // chain of memory trips), so this one wins when steps hold more than
+    // about 4.4 rounds on average.
+    if (var->V >= 1024) return 0;
     const std::vector<int32_t> &sp = sch->h_step_ptr;
     int64_t rounds = 0, wmax = 0;
     for (int64_t p = 0; p < sch->n_steps; p++) {

@@ -191,14 +191,19 @@ def _plan(g, vs):
 
 def test_launch_plan():
     """dd_simulate_batch takes the few-variant path only where it measured
-    faster: few variants over steps of several rounds of 512 positions."""
+    faster: fewer than 1,024 variants over steps of several rounds of 512
+    positions."""
     require_gpu()
     g, vs = W.config(4)                       # 28 long phases, 64 variants
     assert _plan(g, vs) == [-8]
     g, vs = W.config(1)                       # short phases
     assert _plan(g, vs) == [1]
-    g, vs = W.config(2)                       # 256 variants
+    g, vs = W.config(2)                       # 256 variants, short phases
     assert _plan(g, vs) == [1]
+    g, vs = W.config(4, variants=768)         # long phases, 768 variants
+    assert _plan(g, vs) == [-8]
+    g, vs = W.config(4, variants=1024)        # the strip kernel is faster from here
+    assert _plan(g, vs) == [4]
     rng = np.random.default_rng(500)          # one phase of 20,000 tasks, 5 variants
     g = W.random_graph_sparse(rng, 20000, 1, mean_in=0.0, window=64, n_edge_cls=1)
     assert _plan(g, W.random_variants(rng, g, 5, p_remove=0.1)) == [-4]

@@ -227,8 +227,10 @@ void dd_set_lookback_polls(int32_t polls);
  * dd_simulate_batch_noalloc -- dd_simulate_batch for callers that cannot
  * allocate device memory (code under HIP graph capture, tight serving loops,
  * harnesses that forbid hipMalloc).  Same arguments, results and errors as
- * dd_simulate_batch (default launch shape); it calls no hipMalloc, hipFree
- * or other allocating routine and records no events.
+ * dd_simulate_batch; it always runs the one-workgroup-per-strip kernel with
+ * the library's strip width (never the few-variant path, whose look-back
+ * slots it would have to allocate), calls no hipMalloc, hipFree or other
+ * allocating routine and records no events.
  *   Its working memory (round table, scan sums, per-position removal bits)
  *   lives in one array of 64 MiB per GPU inside the library, held until the
  *   process ends.  A batch needs about n*V/8 + 16*n_steps + 4*n/64 bytes of

@@ -391,6 +391,10 @@ hipError_t run_phases(const dd_graph *g, const dd_sched *sch, const dd_variants 
         const int64_t len = sp[p + 1] - sp[p];
         if (len <= 0) continue;
         const int32_t nch = (int32_t)((len + L - 1) / L);
+        if ((int64_t)nch * ngrp > INT32_MAX) {   // more workgroups than one launch takes
+            e = hipErrorInvalidConfiguration;
+            break;
+        }
         k_sim_phase<VG, K><<<nch * ngrp, kSpNT, 0, s>>>((int32_t)p, sp[p], sp[p + 1], nch, coff, args);
         e = hipGetLastError();
         coff += nch;

@@ -207,3 +207,29 @@ def test_launch_plan():
     rng = np.random.default_rng(500)          # one phase of 20,000 tasks, 5 variants
     g = W.random_graph_sparse(rng, 20000, 1, mean_in=0.0, window=64, n_edge_cls=1)
     assert _plan(g, W.random_variants(rng, g, 5, p_remove=0.1)) == [-4]
+
+
+def test_seq2seq_768_variants_full_size():
+    """The seq2seq workload with 768 variants takes the few-variant path by
+    default (8 variants per workgroup, about 90 chunks per long phase x 96
+    groups): every makespan, and the finish column of every 16th variant,
+    bit-exact against the oracle."""
+    import torch
+    require_gpu()
+    g, vs = W.config(4, variants=768)
+    di = BT.to_device(g, vs)
+    res, gh, hs = BT.simulate(di, keep_handles=True)
+    torch.cuda.synchronize()
+    assert [B.dd_simulate_plan(s_, v_) for s_, v_ in hs] == [-8]
+    (v0, v1, fin, _st, ms), = res
+    sample = list(range(0, vs.n_variants, 16))
+    cols = fin.index_select(1, torch.tensor(sample, device=fin.device)).cpu().numpy().T
+    ms_h = ms.cpu().numpy()
+    for s_, v_ in hs:
+        B.dd_sched_free(s_)
+        B.dd_variants_free(v_)
+    B.dd_graph_free(gh)
+    _, _, oM, _ = O.run(g, vs, want_start=False, want_finish=False)
+    assert_equal_arrays("seq2seq-768 makespan", ms_h, oM)
+    _, oF, _, _ = O.run(g, vs, variants=sample, want_start=False)
+    assert_equal_arrays("seq2seq-768 finish (sampled)", cols, oF)

@@ -111,8 +111,11 @@ __device__ __forceinline__ void st_relaxed(uint64_t *p, uint64_t v) {
 }
 
 // One phase [s0, s1): nch chunks of L = (kSpNT / VG) * K positions per
-// variant group; lane = (slot, variant), each slot K consecutive positions.
-template <int VG, int K>
+// variant group; lane = (slot, variant), each slot K consecutive positions,
+// whose loads go out S positions at a time (S = K: every load of a lane in
+// flight together, for launches of few workgroups; S = K / 2: fewer
+// registers and more resident waves, for launches of many).
+template <int VG, int K, int S>
 __global__ __launch_bounds__(kSpNT) void k_sim_phase(int32_t p, int32_t s0, int32_t s1,
                                                      int32_t nch, int64_t coff, SplitArgs a) {
     constexpr int NSL = kSpNT / VG;
@@ -222,26 +225,31 @@ __global__ __launch_bounds__(kSpNT) void k_sim_phase(int32_t p, int32_t s0, int3
     int32_t ND[K];
     uint32_t hd = 0, ok = 0, lv = 0;
     int64_t la = 0, lb = kHead;               // identity
-    Rec R[K];
-    Deps D[K];
+    static_assert(K % S == 0, "stages of whole positions");
 #pragma unroll
-    for (int k = 0; k < K; k++) {              // positions past the chunk read its last one
-        const int64_t q = q0 + (int64_t)slot * K + k;
-        R[k] = a.rec[q < q1 ? q : q1 - 1];
-    }
+    for (int h = 0; h < K; h += S) {
+        Rec R[S];
+        Deps D[S];
 #pragma unroll
-    for (int k = 0; k < K; k++) D[k] = deps_of(R[k]);
+        for (int i = 0; i < S; i++) {          // positions past the chunk read its last one
+            const int64_t q = q0 + (int64_t)slot * K + h + i;
+            R[i] = a.rec[q < q1 ? q : q1 - 1];
+        }
 #pragma unroll
-    for (int k = 0; k < K; k++) {
-        const int64_t q = q0 + (int64_t)slot * K + k;
-        X[k] = 0; DP[k] = 0; GP[k] = 0; ND[k] = 0;
-        if (q < q1) {
-            const Pos ps = position_of(q, R[k], D[k]);
-            X[k] = ps.x; DP[k] = ps.dp; GP[k] = ps.gp; ND[k] = ps.u;
-            ok |= 1u << k;
-            hd |= (ps.head ? 1u : 0u) << k;
-            lv |= (ps.live ? 1u : 0u) << k;
-            then(la, lb, ps.head ? kHead : ps.dp + ps.gp, ps.x + ps.dp + ps.gp);
+        for (int i = 0; i < S; i++) D[i] = deps_of(R[i]);
+#pragma unroll
+        for (int i = 0; i < S; i++) {
+            const int k = h + i;
+            const int64_t q = q0 + (int64_t)slot * K + k;
+            X[k] = 0; DP[k] = 0; GP[k] = 0; ND[k] = 0;
+            if (q < q1) {
+                const Pos ps = position_of(q, R[i], D[i]);
+                X[k] = ps.x; DP[k] = ps.dp; GP[k] = ps.gp; ND[k] = ps.u;
+                ok |= 1u << k;
+                hd |= (ps.head ? 1u : 0u) << k;
+                lv |= (ps.live ? 1u : 0u) << k;
+                then(la, lb, ps.head ? kHead : ps.dp + ps.gp, ps.x + ps.dp + ps.gp);
+            }
         }
     }
     // inclusive scan over the slots of one variant: inside the wave (lanes
@@ -362,7 +370,7 @@ __global__ __launch_bounds__(256) void k_split_zero(uint64_t *look, int64_t nl, 
 
 std::atomic<int32_t> g_polls{kPolls};
 
-template <int VG, int K>
+template <int VG, int K, int S>
 hipError_t run_phases(const dd_graph *g, const dd_sched *sch, const dd_variants *var,
                       int64_t *finish, int64_t *start, int64_t *makespan, hipStream_t s) {
     constexpr int L = (kSpNT / VG) * K;
@@ -395,7 +403,7 @@ hipError_t run_phases(const dd_graph *g, const dd_sched *sch, const dd_variants 
             e = hipErrorInvalidConfiguration;
             break;
         }
-        k_sim_phase<VG, K><<<nch * ngrp, kSpNT, 0, s>>>((int32_t)p, sp[p], sp[p + 1], nch, coff, args);
+        k_sim_phase<VG, K, S><<<nch * ngrp, kSpNT, 0, s>>>((int32_t)p, sp[p], sp[p + 1], nch, coff, args);
         e = hipGetLastError();
         coff += nch;
     }
@@ -436,10 +444,21 @@ int split_width(const dd_sched *sch, const dd_variants *var) {
 hipError_t launch_split(const dd_graph *g, const dd_sched *sch, const dd_variants *var,
                         int64_t *finish, int64_t *start, int64_t *makespan, int vg, hipStream_t s) {
     switch (vg) {
-        case 1: return run_phases<1, 1>(g, sch, var, finish, start, makespan, s);
-        case 2: return run_phases<2, 2>(g, sch, var, finish, start, makespan, s);
-        case 4: return run_phases<4, 4>(g, sch, var, finish, start, makespan, s);
-        case 8: return run_phases<8, 8>(g, sch, var, finish, start, makespan, s);
+        case 1: return run_phases<1, 1, 1>(g, sch, var, finish, start, makespan, s);
+        case 2: return run_phases<2, 2, 2>(g, sch, var, finish, start, makespan, s);
+        case 4: return run_phases<4, 4, 4>(g, sch, var, finish, start, makespan, s);
+        case 8: {
+            // half the loads in flight when the widest step needs 1,024 or
+            // more workgroups (occupancy then matters more than one lane's
+            // overlap: 768 variants 1.66 against 1.85 ms, 64 variants 0.33
+            // against 0.31 ms)
+            int64_t wmax = 0;
+            const std::vector<int32_t> &sp = sch->h_step_ptr;
+            for (size_t p = 0; p + 1 < sp.size(); p++) wmax = std::max<int64_t>(wmax, sp[p + 1] - sp[p]);
+            if ((int64_t)((var->V + 7) / 8) * ((wmax + 255) / 256) >= 1024)
+                return run_phases<8, 8, 4>(g, sch, var, finish, start, makespan, s);
+            return run_phases<8, 8, 8>(g, sch, var, finish, start, makespan, s);
+        }
         default: return hipErrorInvalidValue;
     }
 }

@@ -233,3 +233,31 @@ def test_seq2seq_768_variants_full_size():
     assert_equal_arrays("seq2seq-768 makespan", ms_h, oM)
     _, oF, _, _ = O.run(g, vs, variants=sample, want_start=False)
     assert_equal_arrays("seq2seq-768 finish (sampled)", cols, oF)
+
+
+def test_too_many_steps_for_the_split_path():
+    """A schedule of more than 512 steps keeps no host copy of its step
+    offsets: asking for the few-variant path returns DD_EINVAL (nothing
+    launched), and the default path serves it."""
+    import torch
+    require_gpu()
+    n = 600                                   # ping-pong over two threads: one phase per task
+    g = H.graph(2, [i % 2 for i in range(n)], [(i, i + 1) for i in range(n - 1)],
+                [10 + i % 7 for i in range(n)], [i % 3 for i in range(n)])
+    vs = W.random_variants(np.random.default_rng(3), g, 5, p_remove=0.2)
+    di = BT.to_device(g, vs)
+    res, gh, hs = BT.simulate(di, keep_handles=True)
+    torch.cuda.synchronize()
+    (v0, v1, fin, st, ms), = res
+    (sch, var), = hs
+    assert B.dd_sched_info(sch)["n_steps"] == n
+    assert B.dd_simulate_plan(sch, var) == 1
+    with pytest.raises(B.DDError) as ei:
+        B.dd_simulate_batch_vs(gh, sch, var, fin, None, ms, -8)
+    assert ei.value.code == B.DD_EINVAL and "512 steps" in ei.value.msg
+    ms_h = ms.cpu().numpy()
+    B.dd_sched_free(sch)
+    B.dd_variants_free(var)
+    B.dd_graph_free(gh)
+    _, _, oM, _ = O.run(g, vs, want_start=False, want_finish=False)
+    assert_equal_arrays("ping-pong makespan", ms_h, oM)

@@ -322,25 +322,43 @@ __global__ __launch_bounds__(kWG) void k_kahn_rounds(KahnArgs a) {
         }
         __syncthreads();
         if (s_unfinished == 0) break;                 // every thread at its end
-        // C: emit one segment per advanced thread (packed count<<32 | length scan)
-        if (threadIdx.x == 0) s_carry_cnt = 0;
-        __syncthreads();
-        for (int b0 = 0; b0 < a.T; b0 += kWG) {
-            const int t = b0 + threadIdx.x;
-            int64_t len = 0;
-            if (t < a.T) len = nfront[t] - front[t];
-            const int64_t packed = len > 0 ? ((int64_t(1) << 32) | len) : 0;
-            int64_t tot;
-            const int64_t ex = block_excl_scan<kWG>(packed, &tot);
-            if (len > 0) {
-                const int64_t sg = nseg + s_carry_cnt + (ex >> 32);
-                a.seg_start[sg] = front[t];
-                a.seg_len[sg] = len;
-                a.seg_step[sg] = (int32_t)round;
+        // C: emit one segment per advanced thread.  Up to 64 threads: one
+        // wave ranks them with a ballot; else a workgroup scan of packed
+        // count<<32 | length per block of kWG threads.
+        if (a.T <= 64) {
+            if (threadIdx.x < 64) {
+                const int t = (int)threadIdx.x;
+                const int64_t len = t < a.T ? nfront[t] - front[t] : 0;
+                const unsigned long long bal = __ballot(len > 0);
+                if (len > 0) {
+                    const int64_t sg = nseg + __popcll(bal & ((1ull << t) - 1ull));
+                    a.seg_start[sg] = front[t];
+                    a.seg_len[sg] = len;
+                    a.seg_step[sg] = (int32_t)round;
+                }
+                if (t == 0) s_carry_cnt = __popcll(bal);
             }
             __syncthreads();
-            if (threadIdx.x == 0) s_carry_cnt += tot >> 32;
+        } else {
+            if (threadIdx.x == 0) s_carry_cnt = 0;
             __syncthreads();
+            for (int b0 = 0; b0 < a.T; b0 += kWG) {
+                const int t = b0 + threadIdx.x;
+                int64_t len = 0;
+                if (t < a.T) len = nfront[t] - front[t];
+                const int64_t packed = len > 0 ? ((int64_t(1) << 32) | len) : 0;
+                int64_t tot;
+                const int64_t ex = block_excl_scan<kWG>(packed, &tot);
+                if (len > 0) {
+                    const int64_t sg = nseg + s_carry_cnt + (ex >> 32);
+                    a.seg_start[sg] = front[t];
+                    a.seg_len[sg] = len;
+                    a.seg_step[sg] = (int32_t)round;
+                }
+                __syncthreads();
+                if (threadIdx.x == 0) s_carry_cnt += tot >> 32;
+                __syncthreads();
+            }
         }
         const int64_t adv = s_carry_cnt;
         if (adv == 0) {                               // stalled: cycle

@@ -250,7 +250,7 @@ __global__ __launch_bounds__(kWG) void k_kahn_rounds(KahnArgs a) {
             const int64_t ce = act ? cbase[t + 1] : 0;
             const bool fin = !act || f >= end;
             if (act && fin && gl == 0) { nfront[t] = f; ncidx[t] = ci; }
-            if (!fin && gl == 0) atomicAdd(&s_unfinished, 1);
+            if (!fin && gl == 0) s_unfinished = 1;   // a flag: every writer stores 1
             bool done = fin;
             int64_t cnew = ce;
             int32_t npos = 0;                 // order position of candidate cnew (packed entries)

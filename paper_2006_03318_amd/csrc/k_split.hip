@@ -44,6 +44,8 @@ namespace {
 
 constexpr int kSpNT = 256;                              // threads per workgroup
 constexpr int64_t kHead = -(int64_t(1) << 62);          // a map that ignores its input
+constexpr int64_t kHeadMaxWg = 1024;    // a one-chunk step rides on a next launch of at most
+                                        // this many workgroups
 constexpr int32_t kPolls = 1 << 12;                     // look-back polls before a lane folds
                                                         // the chunk itself
 
@@ -110,14 +112,20 @@ __device__ __forceinline__ void st_relaxed(uint64_t *p, uint64_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// One phase [s0, s1): nch chunks of L = (kSpNT / VG) * K positions per
+// One phase [ps0, ps1): pnch chunks of L = (kSpNT / VG) * K positions per
 // variant group; lane = (slot, variant), each slot K consecutive positions,
 // whose loads go out S positions at a time (S = K: every load of a lane in
 // flight together, for launches of few workgroups; S = K / 2: fewer
-// registers and more resident waves, for launches of many).
+// registers and more resident waves, for launches of many).  When the
+// phase before it is a single chunk [h0, h1) (h1 > h0), every workgroup
+// first computes that phase itself and writes its results (the same
+// values from every workgroup of a group), so it needs no launch of its
+// own: its parents lie in earlier launches, and a workgroup barrier makes
+// the workgroup's own writes visible to its loads.
 template <int VG, int K, int S>
-__global__ __launch_bounds__(kSpNT) void k_sim_phase(int32_t p, int32_t s0, int32_t s1,
-                                                     int32_t nch, int64_t coff, SplitArgs a) {
+__global__ __launch_bounds__(kSpNT) void k_sim_phase(int32_t p, int32_t ps0, int32_t ps1,
+                                                     int32_t pnch, int64_t pcoff, int32_t h0,
+                                                     int32_t h1, SplitArgs a) {
     constexpr int NSL = kSpNT / VG;
     constexpr int L = NSL * K;
     constexpr int NWV = kSpNT / 64;
@@ -136,18 +144,21 @@ __global__ __launch_bounds__(kSpNT) void k_sim_phase(int32_t p, int32_t s0, int3
     const int64_t V = a.V, W = a.W;
     const int vw = vv >> 5;
     const uint32_t vbit = 1u << (vv & 31);
+    const uint64_t eon = a.edge_on[vv];
+
+    // chunk c of the phase [s0, s1) of nch chunks, whose look-back slots
+    // start at chunk offset coff; keep = add to the makespan
+    auto run_chunk = [&](const int32_t s0, const int32_t s1, const int32_t nch, const int c,
+                         const int64_t coff, const bool keep) {
     // this step's slots: [nch][ngrp][VG] from chunk offset coff
     LookSlot *const look = a.look + coff * a.ngrp * VG;
     auto slot_of = [&](int ch) { return look + ((int64_t)ch * a.ngrp + g) * VG + j; };
-
-    const int c = (int)(blockIdx.x / a.ngrp);
     auto chunk_end = [&](int ch) {
         const int64_t e = (int64_t)s0 + (int64_t)(ch + 1) * L;
         return e < (int64_t)s1 ? e : (int64_t)s1;
     };
     const int64_t q0 = (int64_t)s0 + (int64_t)c * L;
     const int64_t q1 = chunk_end(c);
-    const uint64_t eon = a.edge_on[vv];
     if (tid < VG) sMs[tid] = 0ull;
 
     // release of a parent: its finish plus its gap when it is kept
@@ -356,7 +367,17 @@ __global__ __launch_bounds__(kSpNT) void k_sim_phase(int32_t p, int32_t s0, int3
     }
     if (ms) atomicMax(&sMs[j], ms);
     __syncthreads();
-    if (tid < VG && vok && sMs[tid]) atomicMax(&a.makespan[v], sMs[tid]);
+    if (keep && tid < VG && vok && sMs[tid]) atomicMax(&a.makespan[v], sMs[tid]);
+    };
+
+    const int c = (int)(blockIdx.x / a.ngrp);
+    if (h1 > h0) {
+        // the one-chunk phase before this one (only chunk 0 adds it to the
+        // makespan); the barrier orders its writes before this phase's loads
+        run_chunk(h0, h1, 1, 0, 0, c == 0);
+        __syncthreads();
+    }
+    run_chunk(ps0, ps1, pnch, c, pcoff, true);
 }
 
 __global__ __launch_bounds__(256) void k_split_zero(uint64_t *look, int64_t nl, int64_t *makespan,
@@ -395,6 +416,7 @@ hipError_t run_phases(const dd_graph *g, const dd_sched *sch, const dd_variants 
                    sch->thread_carry ? 1 : 0, ngrp, g_polls.load(), finish, start,
                    reinterpret_cast<unsigned long long *>(makespan), look};
     int64_t coff = 0;
+    int32_t h0 = 0, h1 = 0;                  // a pending one-chunk step
     for (int64_t p = 0; p < ns && e == hipSuccess; p++) {
         const int64_t len = sp[p + 1] - sp[p];
         if (len <= 0) continue;
@@ -403,9 +425,23 @@ hipError_t run_phases(const dd_graph *g, const dd_sched *sch, const dd_variants 
             e = hipErrorInvalidConfiguration;
             break;
         }
-        k_sim_phase<VG, K, S><<<nch * ngrp, kSpNT, 0, s>>>((int32_t)p, sp[p], sp[p + 1], nch, coff, args);
+        // a one-chunk step waits to ride on the next step's launch (unless
+        // one is already waiting, it is the last step, or that launch has
+        // more than kHeadMaxWg workgroups, each of which would redo it)
+        int64_t pn = p + 1;
+        while (pn < ns && sp[pn + 1] == sp[pn]) pn++;
+        const int64_t wg_next = pn < ns ? (sp[pn + 1] - sp[pn] + L - 1) / L * ngrp : 0;
+        if (nch == 1 && h1 == h0 && pn < ns && wg_next <= kHeadMaxWg) {
+            h0 = sp[p];
+            h1 = sp[p + 1];
+            coff += nch;
+            continue;
+        }
+        k_sim_phase<VG, K, S><<<nch * ngrp, kSpNT, 0, s>>>((int32_t)p, sp[p], sp[p + 1], nch, coff,
+                                                           h0, h1, args);
         e = hipGetLastError();
         coff += nch;
+        h0 = h1 = 0;
     }
     dfree(look, s);
     return e;

@@ -325,9 +325,9 @@ def main():
     nbytes = sum(algorithmic_bytes(g.n, v1 - v0, bi_["n_gathers"], di.n_cls)
                  for (v0, v1, *_r), bi_ in zip(di.batches, binfo))
     achieved = nbytes / (sim_ms / 1e3) / 1e9
-    # the few-variant path (negative plan) launches one kernel per step (plus
-    # one that clears its look-back slots); its "launch" here is the whole
-    # simulate call of a batch
+    # the few-variant path (negative plan) launches a kernel per step of
+    # more than one chunk (plus one that clears its look-back slots); its
+    # "launch" here is the whole simulate call of a batch
     split = all(b["plan"] < 0 for b in binfo)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
@@ -336,8 +336,6 @@ def main():
                 "algorithmic_bytes_per_launch": int(nbytes),
                 "avg_launch_ms": round(sim_ms / len(di.batches), 4),
                 "launches_per_step": len(di.batches),
-                "kernel_launches_per_step": int(sum(b["n_steps"] + 1 if b["plan"] < 0 else 1
-                                                    for b in binfo)),
                 "variants_per_workgroup": [b["plan"] for b in binfo]}
 
     # the runtime breakdown (CPU-only / GPU-only / CPU+GPU parallel) of every

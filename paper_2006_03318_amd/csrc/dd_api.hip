@@ -200,6 +200,52 @@ void join_uses(ForeignUses &u, hipStream_t own) {
     u.ev.clear();
 }
 
+namespace {
+// this host thread's pinned buffer of at least `bytes`; a buffer that is
+// outgrown is kept (a copy queued earlier may still target it)
+char *stage_buf(size_t bytes, hipError_t *e) {
+    thread_local char *buf = nullptr;
+    thread_local size_t cap = 0;
+    *e = hipSuccess;
+    if (bytes > cap) {
+        size_t c = cap ? cap : 4096;
+        while (c < bytes) c *= 2;
+        char *nb = nullptr;
+        *e = hipHostMalloc(reinterpret_cast<void **>(&nb), c, hipHostMallocDefault);
+        if (*e != hipSuccess) return nullptr;
+        buf = nb;
+        cap = c;
+    }
+    return buf;
+}
+}  // namespace
+
+ReadBack::ReadBack(hipStream_t s, size_t cap) : s_(s) {
+    cap_ = cap + 8 * 16;                  // room for aligning up to 16 items
+    buf_ = stage_buf(cap_, &err_);
+}
+
+hipError_t ReadBack::add(void *dst, const void *src, size_t n) {
+    if (err_ != hipSuccess) return err_;
+    const size_t off = (used_ + 7) & ~size_t(7);
+    if (off + n > cap_) return err_ = hipErrorInvalidValue;
+    err_ = hipMemcpyAsync(buf_ + off, src, n, hipMemcpyDefault, s_);
+    if (err_ == hipSuccess) {
+        items_.push_back(Item{dst, off, n});
+        used_ = off + n;
+    }
+    return err_;
+}
+
+hipError_t ReadBack::finish() {
+    if (err_ == hipSuccess) err_ = hipStreamSynchronize(s_);
+    if (err_ == hipSuccess)
+        for (const Item &it : items_) memcpy(it.dst, buf_ + it.off, it.n);
+    items_.clear();
+    used_ = 0;
+    return err_;
+}
+
 }  // namespace dd
 
 #define TRY(x, what)                                           \
@@ -275,9 +321,12 @@ dd_status dd_graph_load_ex(int32_t n, int32_t n_threads, const int64_t *in_ptr,
     int64_t E = 0;
 
     TRY(copy_in(&d_in_ptr, in_ptr, N1, s), "copy in_ptr");
-    TRY(hipMemcpyAsync(&ends[0], d_in_ptr, sizeof(int64_t), hipMemcpyDeviceToHost, s), "read in_ptr");
-    TRY(hipMemcpyAsync(&ends[1], d_in_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s), "read in_ptr");
-    TRY(hipStreamSynchronize(s), "sync");
+    {
+        dd::ReadBack rb(s, 2 * sizeof(int64_t));
+        TRY(rb.add(&ends[0], d_in_ptr, sizeof(int64_t)), "read in_ptr");
+        TRY(rb.add(&ends[1], d_in_ptr + n, sizeof(int64_t)), "read in_ptr");
+        TRY(rb.finish(), "sync");
+    }
     if (ends[0] != 0) { st = fail(DD_EINVAL, "in_ptr[0] != 0"); goto fail_out; }
     E = ends[1];
     if (E < 0 || E >= (int64_t(1) << 31)) { st = fail(DD_EINVAL, "edge count outside [0, 2^31)"); goto fail_out; }
@@ -305,13 +354,17 @@ dd_status dd_graph_load_ex(int32_t n, int32_t n_threads, const int64_t *in_ptr,
     TRY(dd::dalloc_n(&rank2, N1, s), "alloc");
     TRY(dd::dalloc_n(&cnt, N1, s), "alloc");
     if (n > 0) TRY(dd::launch_rank_tiles(g, nxt, nxt2, rank2, cnt, err, s), "rank chains");
-    TRY(hipMemcpyAsync(h_err2, err, sizeof(h_err2), hipMemcpyDeviceToHost, s), "read err");
-    TRY(hipStreamSynchronize(s), "sync");
+    {
+        dd::ReadBack rb(s, sizeof(h_err2));
+        TRY(rb.add(h_err2, err, sizeof(h_err2)), "read err");
+        TRY(rb.finish(), "sync");
+    }
     if (h_err2[1] && !h_err2[0]) {
         // more tile exits than one workgroup ranks: plain pointer jumping
         TRY(dd::launch_rank_chains(g, succ, nxt, nxt2, rank2, err, s), "rank chains");
-        TRY(hipMemcpyAsync(h_err2, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "read err");
-        TRY(hipStreamSynchronize(s), "sync");
+        dd::ReadBack rb(s, sizeof(uint32_t));
+        TRY(rb.add(h_err2, err, sizeof(uint32_t)), "read err");
+        TRY(rb.finish(), "sync");
     }
     h_err = h_err2[0];
     if (h_err) { st = map_err_bits(h_err); goto fail_out; }
@@ -322,8 +375,9 @@ dd_status dd_graph_load_ex(int32_t n, int32_t n_threads, const int64_t *in_ptr,
         g->xin_src = d_in_src; d_in_src = nullptr;
         g->xin_cls = d_ecls; d_ecls = nullptr;
         g->n_cross = E;
-        TRY(hipMemcpyAsync(&hs, stats, sizeof(hs), hipMemcpyDeviceToHost, s), "read stats");
-        TRY(hipStreamSynchronize(s), "sync");
+        dd::ReadBack rb(s, sizeof(hs));
+        TRY(rb.add(&hs, stats, sizeof(hs)), "read stats");
+        TRY(rb.finish(), "sync");
     } else {
         TRY(dd::dalloc_n(&g->thread_base, (size_t)n_threads + 1, s), "alloc");
         TRY(dd::dalloc_n(&len, (size_t)n_threads + 1, s), "alloc");
@@ -340,10 +394,11 @@ dd_status dd_graph_load_ex(int32_t n, int32_t n_threads, const int64_t *in_ptr,
         TRY(dd::dalloc_n(&g->xin_src, (size_t)E + 1, s), "alloc");
         TRY(dd::dalloc_n(&g->xin_cls, (size_t)E + 1, s), "alloc");
         if (n > 0) TRY(dd::launch_cross_fill(g, d_in_ptr, d_in_src, edge_cls ? d_ecls : nullptr, s), "cross fill");
-        TRY(hipMemcpyAsync(&h_err, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "read err");
-        TRY(hipMemcpyAsync(&g->n_cross, g->xin_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s), "read");
-        TRY(hipMemcpyAsync(&hs, stats, sizeof(hs), hipMemcpyDeviceToHost, s), "read stats");
-        TRY(hipStreamSynchronize(s), "sync");
+        dd::ReadBack rb(s, sizeof(uint32_t) + sizeof(int64_t) + sizeof(hs));
+        TRY(rb.add(&h_err, err, sizeof(uint32_t)), "read err");
+        TRY(rb.add(&g->n_cross, g->xin_ptr + n, sizeof(int64_t)), "read");
+        TRY(rb.add(&hs, stats, sizeof(hs)), "read stats");
+        TRY(rb.finish(), "sync");
     }
     if (h_err) { st = map_err_bits(h_err); goto fail_out; }
     g->dsum = ((__int128)hs.dsum_hi << 32) + (__int128)hs.dsum_lo;
@@ -443,13 +498,16 @@ dd_status dd_apply_transforms(const dd_graph *g, int32_t n_variants, int32_t n_c
     TRY(dd::dalloc_n(&x->edge_on, (size_t)n_variants, s), "alloc edge_on");
     h_on = (uint64_t *)malloc(sizeof(uint64_t) * (size_t)n_variants);
     if (!h_on) { st = fail(DD_ENOMEM, "host allocation"); goto fail_out; }
-    if (edge_on) {
-        TRY(hipMemcpyAsync(h_on, edge_on, sizeof(uint64_t) * (size_t)n_variants, hipMemcpyDefault, s), "read edge_on");
-    } else {
-        for (int32_t v = 0; v < n_variants; v++) h_on[v] = ~0ull;
+    {
+        dd::ReadBack rb(s, sizeof(uint64_t) * (size_t)n_variants + sizeof(h_err));
+        if (edge_on) {
+            TRY(rb.add(h_on, edge_on, sizeof(uint64_t) * (size_t)n_variants), "read edge_on");
+        } else {
+            for (int32_t v = 0; v < n_variants; v++) h_on[v] = ~0ull;
+        }
+        TRY(rb.add(h_err, err, sizeof(h_err)), "read err");
+        TRY(rb.finish(), "sync");
     }
-    TRY(hipMemcpyAsync(h_err, err, sizeof(h_err), hipMemcpyDeviceToHost, s), "read err");
-    TRY(hipStreamSynchronize(s), "sync");
     TRY(hipMemcpyAsync(x->edge_on, h_on, sizeof(uint64_t) * (size_t)n_variants, hipMemcpyHostToDevice, s), "copy edge_on");
     x->used_mask = 0;
     x->all_mask = ~0ull;
@@ -630,8 +688,11 @@ dd_status dd_simulate_policy(const dd_graph *g, const dd_variants *var, int32_t 
     TRY(copy_in(&err, (const uint32_t *)nullptr, 1, s), "alloc");
     TRY(dd::launch_sim_event(g, g->ev, var, policy, d_pp, d_prio, ref, est, d_finish, d_start,
                              d_makespan, err, s), "simulate");
-    TRY(hipMemcpyAsync(&h_err, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "read err");
-    TRY(hipStreamSynchronize(s), "sync");
+    {
+        dd::ReadBack rb(s, sizeof(uint32_t));
+        TRY(rb.add(&h_err, err, sizeof(uint32_t)), "read err");
+        TRY(rb.finish(), "sync");
+    }
     TRY(dd::note_use(g->uses, g->stream, s), "record stream use");
     TRY(dd::note_use(var->uses, var->stream, s), "record stream use");
     if (h_err & 2u)

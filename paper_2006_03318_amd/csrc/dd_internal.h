@@ -173,6 +173,27 @@ struct dd_variants {
 
 namespace dd {
 
+// Read-backs of small results through a pinned host buffer (one per host
+// thread, kept until the process ends).  A copy from the device into
+// pageable memory waits for its stream by itself (about 10 us each); into
+// pinned memory it is a plain DMA, so the queued copies of one read-back
+// cost one synchronization.  cap = the bytes that will be queued.
+class ReadBack {
+public:
+    ReadBack(hipStream_t s, size_t cap);
+    // queue a copy of n bytes from src (device or host) into dst
+    hipError_t add(void *dst, const void *src, size_t n);
+    // wait for the stream, then fill every queued dst
+    hipError_t finish();
+private:
+    struct Item { void *dst; size_t off, n; };
+    hipStream_t s_;
+    char *buf_ = nullptr;
+    size_t cap_ = 0, used_ = 0;
+    hipError_t err_ = hipSuccess;
+    std::vector<Item> items_;
+};
+
 // device memory (cache of blocks kept per device and stream)
 hipError_t dalloc(void **p, size_t bytes, hipStream_t s);
 void dfree(void *p, hipStream_t s);

@@ -1029,9 +1029,12 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
         else k_kahn_rounds<false><<<1, kWG, 0, s>>>(ka);
         CK(hipGetLastError());
     }
-    CK(hipMemcpyAsync(h_res, result, 2 * sizeof(int64_t), hipMemcpyDeviceToHost, s));
-    CK(hipMemcpyAsync(&h_err, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s));
-    CK(hipStreamSynchronize(s));
+    {
+        ReadBack rb(s, 2 * sizeof(int64_t) + sizeof(uint32_t));
+        CK(rb.add(h_res, result, 2 * sizeof(int64_t)));
+        CK(rb.add(&h_err, err, sizeof(uint32_t)));
+        CK(rb.finish());
+    }
     if (h_err & ERR_KAHN_CYCLE) {
         snprintf(msg, msg_len, "dependencies plus thread order contain a cycle "
                                "(Kahn rounds stalled after %lld steps)", (long long)h_res[0]);
@@ -1089,8 +1092,11 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
                          g->xin_src, g->xin_cls, mask, level, lmax};
             k_levels<<<1, kWG, 0, s>>>(la);
             CK(hipGetLastError());
-            CK(hipMemcpyAsync(&h_lmax, lmax, sizeof(h_lmax), hipMemcpyDeviceToHost, s));
-            CK(hipStreamSynchronize(s));
+            {
+                ReadBack rb(s, sizeof(h_lmax));
+                CK(rb.add(&h_lmax, lmax, sizeof(h_lmax)));
+                CK(rb.finish());
+            }
             dfree(tmp_ptr, s);
             dfree(lmax, s);
             const int64_t nl = n > 0 ? (int64_t)h_lmax + 1 : 0;
@@ -1159,16 +1165,17 @@ dd_status levelize_device(const dd_graph *g, uint64_t mask, int32_t mode, dd_sch
         k_step_width<<<grid_for(sch->n_steps, kBS), kBS, 0, s>>>(sch->n_steps, sch->step_ptr, wmax);
         CK(hipGetLastError());
         int64_t h_G = 0;
-        CK(hipMemcpyAsync(&h_w, wmax, sizeof(h_w), hipMemcpyDeviceToHost, s));
-        CK(hipMemcpyAsync(&h_G, sch->gat_ptr + n, sizeof(int64_t), hipMemcpyDeviceToHost, s));
-        if (mode == DD_PHASES)
-            CK(hipMemcpyAsync(&h_res[1], result + 1, sizeof(int64_t), hipMemcpyDeviceToHost, s));
-        if (sch->n_steps <= kSplitMaxSteps) {
-            sch->h_step_ptr.resize((size_t)sch->n_steps + 1);
-            CK(hipMemcpyAsync(sch->h_step_ptr.data(), sch->step_ptr,
-                              sizeof(int32_t) * ((size_t)sch->n_steps + 1), hipMemcpyDeviceToHost, s));
-        }
-        CK(hipStreamSynchronize(s));
+        const bool keep_steps = sch->n_steps <= kSplitMaxSteps;
+        if (keep_steps) sch->h_step_ptr.resize((size_t)sch->n_steps + 1);
+        ReadBack rb(s, sizeof(h_w) + 2 * sizeof(int64_t) +
+                           (keep_steps ? sizeof(int32_t) * ((size_t)sch->n_steps + 1) : 0));
+        CK(rb.add(&h_w, wmax, sizeof(h_w)));
+        CK(rb.add(&h_G, sch->gat_ptr + n, sizeof(int64_t)));
+        if (mode == DD_PHASES) CK(rb.add(&h_res[1], result + 1, sizeof(int64_t)));
+        if (keep_steps)
+            CK(rb.add(sch->h_step_ptr.data(), sch->step_ptr,
+                      sizeof(int32_t) * ((size_t)sch->n_steps + 1)));
+        CK(rb.finish());
         sch->max_width = (int64_t)h_w;
         sch->n_gathers = h_G;
         if (mode == DD_PHASES) sch->n_segments = h_res[1];
